@@ -1,0 +1,203 @@
+/*
+ * hetpipe.h -- C ABI of the MI355X (gfx950) implementation of HetPipe's
+ * data-parallel hot path: one pipeline stage's CNN training step and the
+ * Wave Synchronous Parallel (WSP) weight update (HetPipe, arXiv 2005.14038).
+ *
+ * Objects
+ *   hp_stage  one pipeline stage: a list of layers executed on one GPU
+ *             (Sec. 3, pipelined model parallelism inside a virtual worker).
+ *   hp_ps     the parameter server holding the global weights w_g and the
+ *             global clock c_g (Sec. 5), resident in device memory.
+ *   hp_vw     one virtual worker's WSP state for the stage: the ring of the
+ *             s_local+1 live weight versions, the wave accumulator u~, the
+ *             local clock and the pulled global clock (Sec. 4 and Sec. 5).
+ *
+ * Conventions for every call
+ *   * All tensors are device pointers (HIP global memory) owned by the caller
+ *     unless stated otherwise, and must stay valid until the work enqueued on
+ *     the object's stream has completed.  Activations are NHWC fp32;
+ *     parameters, gradients, ring versions, u~ and w_g are flat fp32 vectors
+ *     in the stage's parameter layout (hp_stage_param_layout).
+ *   * Every object is bound to the HIP stream given at creation; device work
+ *     is enqueued asynchronously on it.  Clocks and protocol state live on the
+ *     host and are updated synchronously by the calls.  No call synchronises
+ *     the device except *_destroy.  Objects are not thread-safe.
+ *   * Every call returns a status: HP_OK, HP_WOULD_BLOCK (hp_wsp_pull only) or
+ *     a negative error.  Errors never abort; hp_last_error() describes the
+ *     last error of the calling thread.
+ */
+#ifndef HETPIPE_H
+#define HETPIPE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---------------------------------------------------------------- status */
+#define HP_OK            0
+#define HP_WOULD_BLOCK   1   /* pull gate closed: the clock bound needs other VWs' pushes */
+#define HP_ERR_ARG     (-1)  /* NULL pointer, bad shape, bad layer description */
+#define HP_ERR_STATE   (-2)  /* call out of protocol order (see each call) */
+#define HP_ERR_HIP     (-3)  /* a HIP launch or runtime call failed */
+#define HP_ERR_NOMEM   (-4)  /* device allocation failed */
+
+/* ----------------------------------------------------------- layer kinds */
+#define HP_CONV        1   /* C -> K channels, R x S window, stride, pad, optional bias */
+#define HP_FC          2   /* C = in features (input flattened in (h,w,c) order), K = out */
+#define HP_RELU        3
+#define HP_MAXPOOL     4   /* R x S window, stride, pad; padded taps never win */
+#define HP_BN          5   /* training-mode batch-norm over (n,h,w), C channels, eps */
+#define HP_ADD         6   /* residual add of in0 and in1 */
+#define HP_GAP         7   /* global average pool over (h,w) */
+#define HP_SOFTMAX_CE  8   /* softmax cross-entropy head, K = classes; must be last */
+
+/* ------------------------------------------------------ arithmetic modes */
+#define HP_FP32  0         /* fp32 operands, fp32 accumulation */
+#define HP_BF16  1         /* contraction operands rounded to bf16 (RNE), fp32 accumulation;
+                              everything else, and all stored state, fp32 */
+
+/* One layer of a stage.  Layers are listed in topological order; layer i's
+ * output is value i and in0/in1 name the values a layer reads (-1 is the
+ * stage input).  Parameters of the layers are concatenated in list order:
+ *   HP_CONV  weight [K][R][S][C], then bias [K] if bias != 0
+ *   HP_FC    weight [K][C] ([out][in]), then bias [K] if bias != 0
+ *   HP_BN    gamma [C], then beta [C]
+ * Fields a kind does not use are ignored. */
+typedef struct hp_layer {
+    int32_t kind;
+    int32_t in0, in1;
+    int32_t C, K;
+    int32_t R, S;
+    int32_t stride, pad;
+    int32_t bias;
+    float eps;
+} hp_layer;
+
+typedef struct hp_stage hp_stage;
+typedef struct hp_ps hp_ps;
+typedef struct hp_vw hp_vw;
+
+/* ================================================================ stage */
+
+/* Create a stage for minibatches of `batch` inputs of shape H x W x C (NHWC).
+ * Allocates the activation stash, gradient buffers and workspaces on the
+ * current HIP device; `stream` is a hipStream_t (NULL = default stream).
+ * Errors: HP_ERR_ARG for an inconsistent layer list (shape mismatch, a loss
+ * head that is not last, unknown kind), HP_ERR_NOMEM. */
+int hp_stage_create(const hp_layer *layers, int n_layers, int batch, int H, int W, int C,
+                    int dtype_mode, void *stream, hp_stage **out);
+int hp_stage_destroy(hp_stage *st);
+
+/* Number of fp32 parameters P of the stage. */
+int hp_stage_param_count(const hp_stage *st, size_t *count);
+/* Offset and length (in floats) of layer `layer`'s parameters in the flat
+ * vector; both are 0 for a layer without parameters. */
+int hp_stage_param_layout(const hp_stage *st, int layer, size_t *offset, size_t *count);
+/* Per-image shape of layer `layer`'s output (layer -1: the stage output;
+ * a loss head reports its logits).  dims = {H, W, C}; FC/GAP give {1, 1, C}. */
+int hp_stage_output_shape(const hp_stage *st, int layer, int dims[3]);
+/* Bytes of device memory the stage holds. */
+int hp_stage_device_bytes(const hp_stage *st, size_t *bytes);
+
+/* Forward pass of one minibatch (HetPipe Sec. 3: the layers of the stage in
+ * order) at weights `w` (flat fp32, length P).  `x` is the stage input
+ * [batch][H][W][C].  If the stage ends in HP_SOFTMAX_CE, `labels` (int32
+ * [batch]) must be non-NULL, `loss` receives the mean cross-entropy (one
+ * device float) and `y`, if non-NULL, the logits [batch][classes].  Otherwise
+ * `labels` and `loss` must be NULL and `y` receives the stage output.
+ * The activations needed by the backward pass are kept inside the stage. */
+int hp_stage_forward(hp_stage *st, const float *w, const float *x, float *y,
+                     const int32_t *labels, float *loss);
+
+/* Backward pass of the minibatch whose forward ran last, at the same weights
+ * `w` (Sec. 4: a minibatch's forward and backward use one weight version).
+ * `dy` is the gradient at the stage output (NULL iff the stage ends in the
+ * loss head).  `grad` (flat fp32, length P) is overwritten with the weight
+ * gradient.  If `dx` is non-NULL it receives the gradient with respect to the
+ * stage input; with dx == NULL the first layer's data gradient is skipped.
+ * Errors: HP_ERR_STATE if no forward preceded or `w` differs from it. */
+int hp_stage_backward(hp_stage *st, const float *w, const float *dy, float *dx, float *grad);
+
+/* ==================================================== parameter server */
+
+/* Create the parameter server for N virtual workers with clock-distance
+ * bound D (Sec. 5) holding w_g = copy of w0 (device pointer, P floats).
+ * The server owns w_g.  c_g starts at 0. */
+int hp_ps_create(size_t P, const float *w0, int N, int D, void *stream, hp_ps **out);
+int hp_ps_destroy(hp_ps *ps);
+/* Device pointer to w_g (read-only for the caller) and the global clock. */
+int hp_ps_weights(const hp_ps *ps, const float **wg);
+int hp_ps_clock(const hp_ps *ps, int *c_global);
+
+/* ======================================================= virtual worker */
+
+/* Register virtual worker `id` (0 <= id < N) with the server.  The wave length
+ * is W = s_local + 1 (Sec. 4: s_local = N_m - 1).  All W ring versions start
+ * as copies of the server's current w_g (w_1 = ... = w_W = w_0). */
+int hp_vw_create(hp_ps *ps, int id, int s_local, hp_vw **out);
+int hp_vw_destroy(hp_vw *vw);
+
+/* Weights for the VW's next minibatch q = p+1: the ring version holding the
+ * local updates 1 .. q-W (Sec. 4) -- a device pointer into the ring, valid
+ * until this VW's next hp_wsp_local_update.  Errors: HP_ERR_STATE if a
+ * completed wave has not been pushed yet, or its pull has not succeeded. */
+int hp_wsp_weights(hp_vw *vw, const float **w);
+
+/* Local update after minibatch q completes (Sec. 4: w_local = w_local + u_q,
+ * u_q = -lr * grad) and wave accumulation (Sec. 5: u~ sums the wave's u_q).
+ * Computes, element by element in fp32 without fused multiply-add,
+ *   u = (-lr) * grad;  ring[(q-1) mod W] = ring[(q-2) mod W] + u;
+ *   u~ = u (first minibatch of a wave) or u~ + u,
+ * and advances p.  `grad` is caller-owned (P floats).
+ * Errors: HP_ERR_STATE if hp_wsp_weights was not called for this minibatch. */
+int hp_wsp_local_update(hp_vw *vw, const float *grad, float lr);
+
+/* Push at the end of wave c (Sec. 5): w_g = w_g + u~, the VW's local clock
+ * becomes c+1 and c_g = min over VWs of their local clocks.  `ps` must be the
+ * server the VW was created with.
+ * Errors: HP_ERR_STATE unless the VW just completed a wave it has not pushed. */
+int hp_wsp_push_wave(hp_vw *vw, hp_ps *ps);
+
+/* Clock-bound gate after a push (Sec. 5, global staleness bound): the VW with
+ * local clock c needs weights holding all VWs' waves 0 .. c-D-1.  If its last
+ * pull already covers that, nothing happens (HP_OK).  Else if c_g >= c-D, w_g
+ * is copied into the ring slot of the next wave's last minibatch, the pulled
+ * clock becomes c_g (HP_OK).  Else HP_WOULD_BLOCK: the VW may not start a new
+ * minibatch until a later hp_wsp_pull returns HP_OK, after other VWs pushed.
+ * Never blocks the host thread.  A call with no pending gate returns HP_OK. */
+int hp_wsp_pull(hp_vw *vw, hp_ps *ps);
+
+/* Host-side bookkeeping of a VW (exact integers). */
+typedef struct hp_wsp_state {
+    int64_t p;          /* minibatches completed */
+    int32_t W;          /* wave length s_local + 1 */
+    int32_t c;          /* local clock: waves pushed */
+    int32_t g;          /* global clock reflected by the last pull */
+    int32_t push_due;   /* a completed wave awaits hp_wsp_push_wave */
+    int32_t gated;      /* a push happened and its pull has not succeeded */
+    int32_t next_slot;  /* ring slot the next minibatch reads */
+    int32_t n_vw;       /* N */
+} hp_wsp_state_t;
+int hp_wsp_state(const hp_vw *vw, hp_wsp_state_t *out);
+
+/* Version vector of the weights the next minibatch will read: V[n] = number
+ * of minibatch updates of VW n contained in them (n < N).  `V` is host memory
+ * of N int64 entries. */
+int hp_wsp_version(const hp_vw *vw, int64_t *V);
+
+/* Device pointers of the VW's ring and of u~ (P floats), owned by the VW; for
+ * inspection.  Ring slot s starts at ring + s * slot_stride (slot_stride >= P,
+ * a multiple of 64 floats so every slot is 256-byte aligned). */
+int hp_wsp_buffers(const hp_vw *vw, const float **ring, size_t *slot_stride,
+                   const float **utilde);
+
+/* Description of the last error on the calling thread ("" if none). */
+const char *hp_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* HETPIPE_H */

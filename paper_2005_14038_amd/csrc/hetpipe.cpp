@@ -1,0 +1,729 @@
+// Host runtime of the HetPipe stage step and WSP engine: the C ABI of
+// include/hetpipe.h.
+//
+//  * hp_stage: validates the layer list, derives every layer's shape and
+//    parameter offsets, plans each contraction (tile shape, split-K), owns the
+//    activation stash, per-layer gradient buffers and one shared workspace,
+//    and enqueues the forward / backward launch sequence on its stream.
+//    ReLUs that directly follow a conv, FC, batch-norm or residual add whose
+//    only consumer they are are fused into the producer's kernel.
+//  * hp_ps / hp_vw: the parameter server and the virtual workers.  Device
+//    state (w_g, the weight ring, u~) is updated by the kernels in wsp.hip;
+//    clocks, the push/pull protocol and the version vectors are host integers
+//    updated synchronously, so bookkeeping never waits on the device.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/hetpipe.h"
+#include "kernels.h"
+
+using namespace hp;
+
+namespace {
+
+thread_local std::string g_last_error;
+
+int fail(int code, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    g_last_error = buf;
+    return code;
+}
+
+#define HP_HIP(expr)                                                                  \
+    do {                                                                              \
+        hipError_t _e = (expr);                                                       \
+        if (_e != hipSuccess)                                                         \
+            return fail(_e == hipErrorOutOfMemory ? HP_ERR_NOMEM : HP_ERR_HIP,         \
+                        "%s failed: %s", #expr, hipGetErrorString(_e));               \
+    } while (0)
+
+struct Node {
+    hp_layer L{};
+    int inH = 0, inW = 0, inC = 0;      // per-image input shape (in0)
+    int H = 0, W = 0, C = 0;            // per-image output shape
+    size_t out_elems = 0;               // batch * H * W * C
+    int consumers = 0;
+    bool relu_fused = false;            // producer applies the ReLU (this node is a ReLU)
+    bool fuses_relu = false;            // this node applies its consumer ReLU
+    float* y = nullptr;                 // forward output (a fused ReLU aliases its producer)
+    float* g = nullptr;                 // gradient of the output
+    bool g_written = false;
+    const float* g_alias = nullptr;     // gradient handed over without a copy (ReLU -> BN)
+    size_t p_off = 0, p_cnt = 0;        // all parameters of the node
+    size_t w_off = 0, b_off = 0;        // conv/fc weight, bias; bn gamma, beta
+    ConvGeo geo{};
+    GemmPlan fwd{}, dgrad{}, wgrad{};
+    float* mean = nullptr;
+    float* invstd = nullptr;
+};
+
+size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+}  // namespace
+
+struct hp_stage {
+    std::vector<Node> nodes;
+    int batch = 0, H = 0, W = 0, C = 0;
+    int dtype = HP_FP32;
+    hipStream_t stream = nullptr;
+    size_t P = 0;
+    size_t ws_floats = 0;
+    float* ws = nullptr;
+    std::vector<void*> allocs;
+    size_t bytes = 0;
+    bool has_loss = false;
+    // forward bookkeeping for backward
+    const float* fwd_w = nullptr;
+    const float* fwd_x = nullptr;
+    bool fwd_done = false;
+};
+
+struct hp_vw;
+
+struct hp_ps {
+    size_t P = 0;
+    float* wg = nullptr;
+    int N = 0, D = 0;
+    hipStream_t stream = nullptr;
+    std::vector<int> clock;          // local clock of each VW
+    std::vector<int64_t> pushed;     // waves of each VW contained in w_g
+    std::vector<hp_vw*> vws;
+    int cg = 0;
+};
+
+struct hp_vw {
+    hp_ps* ps = nullptr;
+    int id = 0;
+    int W = 1;
+    size_t P = 0, stride = 0;
+    float* ring = nullptr;
+    float* ut = nullptr;
+    int64_t p = 0;
+    int c = 0, g = 0;
+    bool in_flight = false, push_due = false, need_pull = false;
+    std::vector<std::vector<int64_t>> V;   // [W][N] version vectors of the ring slots
+};
+
+namespace {
+
+int dev_alloc(hp_stage* st, float** p, size_t floats) {
+    if (floats == 0) { *p = nullptr; return HP_OK; }
+    void* q = nullptr;
+    hipError_t e = hipMalloc(&q, floats * sizeof(float));
+    if (e != hipSuccess)
+        return fail(e == hipErrorOutOfMemory ? HP_ERR_NOMEM : HP_ERR_HIP,
+                    "hipMalloc(%zu bytes): %s", floats * sizeof(float), hipGetErrorString(e));
+    st->allocs.push_back(q);
+    st->bytes += floats * sizeof(float);
+    *p = (float*)q;
+    return HP_OK;
+}
+
+int num_cus() {
+    int dev = 0, n = 256;
+    if (hipGetDevice(&dev) == hipSuccess)
+        (void)hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev);
+    return n > 0 ? n : 256;
+}
+
+int shape_of(const hp_stage* st, int idx, int& H, int& W, int& C) {
+    if (idx == -1) { H = st->H; W = st->W; C = st->C; return HP_OK; }
+    if (idx < 0 || idx >= (int)st->nodes.size()) return HP_ERR_ARG;
+    const Node& n = st->nodes[idx];
+    H = n.H; W = n.W; C = n.C;
+    return HP_OK;
+}
+
+int build_stage(hp_stage* st, const hp_layer* layers, int n_layers) {
+    st->nodes.resize(n_layers);
+    const int cus = num_cus();
+    size_t off = 0;
+    for (int i = 0; i < n_layers; ++i) {
+        Node& nd = st->nodes[i];
+        nd.L = layers[i];
+        const hp_layer& L = nd.L;
+        if (L.in0 < -1 || L.in0 >= i)
+            return fail(HP_ERR_ARG, "layer %d: input %d is not an earlier layer", i, L.in0);
+        if (L.in0 >= 0 && st->nodes[L.in0].L.kind == HP_SOFTMAX_CE)
+            return fail(HP_ERR_ARG, "layer %d reads the loss head", i);
+        shape_of(st, L.in0, nd.inH, nd.inW, nd.inC);
+        if (L.in0 >= 0) st->nodes[L.in0].consumers++;
+        const int B = st->batch;
+        switch (L.kind) {
+            case HP_CONV:
+            case HP_FC: {
+                int R = L.R, S = L.S, stride = L.stride, pad = L.pad;
+                int inH = nd.inH, inW = nd.inW, inC = nd.inC;
+                if (L.kind == HP_FC) {
+                    // an FC layer is a 1x1 convolution over the flattened input
+                    inC = nd.inH * nd.inW * nd.inC;
+                    inH = inW = 1;
+                    R = S = stride = 1;
+                    pad = 0;
+                    if (L.C != inC)
+                        return fail(HP_ERR_ARG, "layer %d: FC expects %d inputs, got %d", i, L.C, inC);
+                } else if (L.C != inC) {
+                    return fail(HP_ERR_ARG, "layer %d: conv expects %d channels, got %d", i, L.C, inC);
+                }
+                if (L.K <= 0 || R <= 0 || S <= 0 || stride <= 0 || pad < 0)
+                    return fail(HP_ERR_ARG, "layer %d: bad conv/FC geometry", i);
+                int P = (inH + 2 * pad - R) / stride + 1;
+                int Q = (inW + 2 * pad - S) / stride + 1;
+                if (P <= 0 || Q <= 0) return fail(HP_ERR_ARG, "layer %d: empty output", i);
+                nd.geo = ConvGeo{B, inH, inW, inC, L.K, R, S, P, Q, stride, pad};
+                nd.H = P; nd.W = Q; nd.C = L.K;
+                nd.w_off = off;
+                nd.p_off = off;
+                off += (size_t)L.K * R * S * inC;
+                if (L.bias) { nd.b_off = off; off += L.K; }
+                nd.p_cnt = off - nd.p_off;
+                nd.fwd = plan_gemm(OP_FWD, nd.geo, st->dtype, cus);
+                nd.dgrad = plan_gemm(OP_DGRAD, nd.geo, st->dtype, cus);
+                nd.wgrad = plan_gemm(OP_WGRAD, nd.geo, st->dtype, cus);
+                st->ws_floats = std::max({st->ws_floats, nd.fwd.ws_floats, nd.dgrad.ws_floats,
+                                          nd.wgrad.ws_floats});
+                if (L.bias)
+                    st->ws_floats = std::max(st->ws_floats,
+                                             colsum_ws_floats((long)B * P * Q, L.K));
+                break;
+            }
+            case HP_RELU:
+                nd.H = nd.inH; nd.W = nd.inW; nd.C = nd.inC;
+                break;
+            case HP_MAXPOOL: {
+                if (L.R <= 0 || L.S <= 0 || L.stride <= 0 || L.pad < 0 || L.pad >= L.R ||
+                    L.pad >= L.S)
+                    return fail(HP_ERR_ARG, "layer %d: bad pooling geometry", i);
+                nd.H = (nd.inH + 2 * L.pad - L.R) / L.stride + 1;
+                nd.W = (nd.inW + 2 * L.pad - L.S) / L.stride + 1;
+                nd.C = nd.inC;
+                if (nd.H <= 0 || nd.W <= 0) return fail(HP_ERR_ARG, "layer %d: empty output", i);
+                break;
+            }
+            case HP_BN:
+                if (L.C != nd.inC)
+                    return fail(HP_ERR_ARG, "layer %d: BN expects %d channels, got %d", i, L.C, nd.inC);
+                nd.H = nd.inH; nd.W = nd.inW; nd.C = nd.inC;
+                nd.p_off = nd.w_off = off;
+                off += L.C;
+                nd.b_off = off;
+                off += L.C;
+                nd.p_cnt = 2 * (size_t)L.C;
+                st->ws_floats = std::max(st->ws_floats, bn_ws_floats((long)B * nd.H * nd.W, L.C));
+                break;
+            case HP_ADD: {
+                int h, w, c;
+                if (L.in1 < -1 || L.in1 >= i || shape_of(st, L.in1, h, w, c) != HP_OK)
+                    return fail(HP_ERR_ARG, "layer %d: bad second input %d", i, L.in1);
+                if (h != nd.inH || w != nd.inW || c != nd.inC)
+                    return fail(HP_ERR_ARG, "layer %d: residual add of mismatched shapes", i);
+                if (L.in1 >= 0) st->nodes[L.in1].consumers++;
+                nd.H = nd.inH; nd.W = nd.inW; nd.C = nd.inC;
+                break;
+            }
+            case HP_GAP:
+                nd.H = 1; nd.W = 1; nd.C = nd.inC;
+                break;
+            case HP_SOFTMAX_CE:
+                if (i != n_layers - 1) return fail(HP_ERR_ARG, "loss head must be the last layer");
+                if (L.in0 < 0) return fail(HP_ERR_ARG, "loss head needs logits from a layer");
+                if (nd.inH * nd.inW * nd.inC != L.K)
+                    return fail(HP_ERR_ARG, "layer %d: %d classes but %d logits", i, L.K,
+                                nd.inH * nd.inW * nd.inC);
+                nd.H = 1; nd.W = 1; nd.C = 0;
+                st->has_loss = true;
+                st->ws_floats = std::max(st->ws_floats, (size_t)B);
+                break;
+            default:
+                return fail(HP_ERR_ARG, "layer %d: unknown kind %d", i, L.kind);
+        }
+        nd.out_elems = (size_t)B * nd.H * nd.W * nd.C;
+    }
+    st->P = off;
+    // ReLU fusion: a ReLU reading a conv / FC / BN / add that has no other consumer
+    for (int i = 0; i < n_layers; ++i) {
+        Node& nd = st->nodes[i];
+        if (nd.L.kind != HP_RELU || nd.L.in0 < 0) continue;
+        Node& pr = st->nodes[nd.L.in0];
+        int k = pr.L.kind;
+        if ((k == HP_CONV || k == HP_FC || k == HP_BN || k == HP_ADD) && pr.consumers == 1 &&
+            !pr.fuses_relu) {
+            pr.fuses_relu = true;
+            nd.relu_fused = true;
+        }
+    }
+    // device buffers
+    for (int i = 0; i < n_layers; ++i) {
+        Node& nd = st->nodes[i];
+        if (nd.L.kind == HP_SOFTMAX_CE) continue;
+        if (nd.relu_fused) {
+            nd.y = st->nodes[nd.L.in0].y;
+        } else {
+            int rc = dev_alloc(st, &nd.y, nd.out_elems);
+            if (rc) return rc;
+        }
+        int rc = dev_alloc(st, &nd.g, nd.out_elems);
+        if (rc) return rc;
+        if (nd.L.kind == HP_BN) {
+            if ((rc = dev_alloc(st, &nd.mean, nd.C))) return rc;
+            if ((rc = dev_alloc(st, &nd.invstd, nd.C))) return rc;
+        }
+    }
+    return dev_alloc(st, &st->ws, std::max<size_t>(st->ws_floats, 64));
+}
+
+int launch_ok(hipError_t e, const char* what, int layer) {
+    if (e != hipSuccess)
+        return fail(HP_ERR_HIP, "launch of %s (layer %d) failed: %s", what, layer,
+                    hipGetErrorString(e));
+    return HP_OK;
+}
+
+}  // namespace
+
+// =================================================================== stage
+
+extern "C" int hp_stage_create(const hp_layer* layers, int n_layers, int batch, int H, int W,
+                               int C, int dtype_mode, void* stream, hp_stage** out) {
+    if (!out) return fail(HP_ERR_ARG, "hp_stage_create: out is NULL");
+    *out = nullptr;
+    if (!layers || n_layers <= 0 || batch <= 0 || H <= 0 || W <= 0 || C <= 0)
+        return fail(HP_ERR_ARG, "hp_stage_create: bad arguments");
+    if (dtype_mode != HP_FP32 && dtype_mode != HP_BF16)
+        return fail(HP_ERR_ARG, "hp_stage_create: unknown dtype mode %d", dtype_mode);
+    hp_stage* st = new hp_stage();
+    st->batch = batch; st->H = H; st->W = W; st->C = C;
+    st->dtype = dtype_mode;
+    st->stream = (hipStream_t)stream;
+    int rc = build_stage(st, layers, n_layers);
+    if (rc != HP_OK) {
+        std::string msg = g_last_error;
+        hp_stage_destroy(st);
+        g_last_error = msg;
+        return rc;
+    }
+    *out = st;
+    return HP_OK;
+}
+
+extern "C" int hp_stage_destroy(hp_stage* st) {
+    if (!st) return HP_OK;
+    if (st->stream || !st->allocs.empty()) (void)hipStreamSynchronize(st->stream);
+    for (void* p : st->allocs) (void)hipFree(p);
+    delete st;
+    return HP_OK;
+}
+
+extern "C" int hp_stage_param_count(const hp_stage* st, size_t* count) {
+    if (!st || !count) return fail(HP_ERR_ARG, "hp_stage_param_count: NULL argument");
+    *count = st->P;
+    return HP_OK;
+}
+
+extern "C" int hp_stage_param_layout(const hp_stage* st, int layer, size_t* offset, size_t* count) {
+    if (!st || !offset || !count) return fail(HP_ERR_ARG, "hp_stage_param_layout: NULL argument");
+    if (layer < 0 || layer >= (int)st->nodes.size())
+        return fail(HP_ERR_ARG, "hp_stage_param_layout: no layer %d", layer);
+    *offset = st->nodes[layer].p_cnt ? st->nodes[layer].p_off : 0;
+    *count = st->nodes[layer].p_cnt;
+    return HP_OK;
+}
+
+extern "C" int hp_stage_output_shape(const hp_stage* st, int layer, int dims[3]) {
+    if (!st || !dims) return fail(HP_ERR_ARG, "hp_stage_output_shape: NULL argument");
+    int n = (int)st->nodes.size();
+    if (layer == -1) layer = st->has_loss ? n - 2 : n - 1;
+    if (layer < 0 || layer >= n) return fail(HP_ERR_ARG, "hp_stage_output_shape: no layer %d", layer);
+    const Node& nd = st->nodes[layer];
+    dims[0] = nd.H; dims[1] = nd.W; dims[2] = nd.C;
+    return HP_OK;
+}
+
+extern "C" int hp_stage_device_bytes(const hp_stage* st, size_t* bytes) {
+    if (!st || !bytes) return fail(HP_ERR_ARG, "hp_stage_device_bytes: NULL argument");
+    *bytes = st->bytes;
+    return HP_OK;
+}
+
+extern "C" int hp_stage_forward(hp_stage* st, const float* w, const float* x, float* y,
+                                const int32_t* labels, float* loss) {
+    if (!st || !x || (!w && st->P)) return fail(HP_ERR_ARG, "hp_stage_forward: NULL argument");
+    if (st->has_loss && (!labels || !loss))
+        return fail(HP_ERR_ARG, "hp_stage_forward: loss head needs labels and loss");
+    if (!st->has_loss && (labels || loss))
+        return fail(HP_ERR_ARG, "hp_stage_forward: stage has no loss head");
+    if (!st->has_loss && !y) return fail(HP_ERR_ARG, "hp_stage_forward: y is NULL");
+    hipStream_t s = st->stream;
+    const int B = st->batch;
+    for (size_t i = 0; i < st->nodes.size(); ++i) {
+        Node& nd = st->nodes[i];
+        const hp_layer& L = nd.L;
+        const float* in = L.in0 < 0 ? x : st->nodes[L.in0].y;
+        hipError_t e = hipSuccess;
+        switch (L.kind) {
+            case HP_CONV:
+            case HP_FC: {
+                int epi = (L.bias ? EPI_BIAS : 0) | (nd.fuses_relu ? EPI_RELU : 0);
+                e = launch_gemm(nd.fwd, nd.geo, in, w + nd.w_off, nd.y,
+                                L.bias ? w + nd.b_off : nullptr, epi, st->ws, s);
+                break;
+            }
+            case HP_RELU:
+                if (!nd.relu_fused) e = launch_relu_fwd(in, nd.y, nd.out_elems, s);
+                break;
+            case HP_MAXPOOL:
+                e = launch_maxpool_fwd(in, nd.y, B, nd.inH, nd.inW, nd.inC, L.R, L.S, L.stride,
+                                       L.pad, nd.H, nd.W, s);
+                break;
+            case HP_BN:
+                e = launch_bn_fwd(in, (long)B * nd.H * nd.W, nd.C, w + nd.w_off, w + nd.b_off,
+                                  L.eps, nd.y, nd.mean, nd.invstd, nd.fuses_relu ? 1 : 0, st->ws, s);
+                break;
+            case HP_ADD: {
+                const float* in1 = L.in1 < 0 ? x : st->nodes[L.in1].y;
+                e = launch_add_fwd(in, in1, nd.y, nd.out_elems, nd.fuses_relu ? 1 : 0, s);
+                break;
+            }
+            case HP_GAP:
+                e = launch_gap_fwd(in, nd.y, B, nd.inH * nd.inW, nd.C, s);
+                break;
+            case HP_SOFTMAX_CE: {
+                // dz goes straight into the logits' gradient buffer
+                Node& lg = st->nodes[L.in0];
+                e = launch_softmax_ce(in, labels, B, L.K, loss, lg.g, st->ws, s);
+                if (e == hipSuccess && y)
+                    e = hipMemcpyAsync(y, in, (size_t)B * L.K * sizeof(float),
+                                       hipMemcpyDeviceToDevice, s);
+                break;
+            }
+        }
+        int rc = launch_ok(e, "forward", (int)i);
+        if (rc) return rc;
+    }
+    if (!st->has_loss) {
+        Node& last = st->nodes.back();
+        HP_HIP(hipMemcpyAsync(y, last.y, last.out_elems * sizeof(float), hipMemcpyDeviceToDevice, s));
+    }
+    st->fwd_w = w;
+    st->fwd_x = x;
+    st->fwd_done = true;
+    return HP_OK;
+}
+
+extern "C" int hp_stage_backward(hp_stage* st, const float* w, const float* dy, float* dx,
+                                 float* grad) {
+    if (!st || !grad || (!w && st->P)) return fail(HP_ERR_ARG, "hp_stage_backward: NULL argument");
+    if (!st->fwd_done) return fail(HP_ERR_STATE, "hp_stage_backward: no forward pass to differentiate");
+    if (w != st->fwd_w)
+        return fail(HP_ERR_STATE, "hp_stage_backward: weights differ from the forward pass");
+    if (st->has_loss && dy) return fail(HP_ERR_ARG, "hp_stage_backward: loss stage takes no dy");
+    if (!st->has_loss && !dy) return fail(HP_ERR_ARG, "hp_stage_backward: dy is NULL");
+    hipStream_t s = st->stream;
+    const int B = st->batch;
+    const int n = (int)st->nodes.size();
+    const float* x = st->fwd_x;
+    for (Node& nd : st->nodes) {
+        nd.g_written = false;
+        nd.g_alias = nullptr;
+    }
+    bool dx_written = false;
+    if (st->has_loss) st->nodes[st->nodes.back().L.in0].g_written = true;  // dz from forward
+
+    // destination of a gradient sent to value j: (pointer, accumulate?)
+    auto dest = [&](int j, float** p, int* acc) -> bool {
+        if (j < 0) {
+            if (!dx) return false;
+            *p = dx;
+            *acc = dx_written ? 1 : 0;
+            dx_written = true;
+            return true;
+        }
+        *p = st->nodes[j].g;
+        *acc = st->nodes[j].g_written ? 1 : 0;
+        st->nodes[j].g_written = true;
+        return true;
+    };
+
+    for (int i = n - 1; i >= 0; --i) {
+        Node& nd = st->nodes[i];
+        const hp_layer& L = nd.L;
+        if (L.kind == HP_SOFTMAX_CE) continue;
+        const float* gin;
+        if (i == n - 1 && !st->has_loss) gin = dy;
+        else if (nd.g_alias) gin = nd.g_alias;
+        else if (nd.g_written) gin = nd.g;
+        else continue;   // no gradient reaches this value
+        const float* in = L.in0 < 0 ? x : st->nodes[L.in0].y;
+        hipError_t e = hipSuccess;
+        float* d;
+        int acc;
+        switch (L.kind) {
+            case HP_CONV:
+            case HP_FC: {
+                e = launch_gemm(nd.wgrad, nd.geo, in, gin, grad + nd.w_off, nullptr, 0, st->ws, s);
+                if (e == hipSuccess && L.bias)
+                    e = launch_colsum(gin, (long)B * nd.H * nd.W, nd.C, grad + nd.b_off, st->ws, s);
+                if (e == hipSuccess && dest(L.in0, &d, &acc))
+                    e = launch_gemm(nd.dgrad, nd.geo, gin, w + nd.w_off, d, nullptr,
+                                    acc ? EPI_ACCUM : 0, st->ws, s);
+                break;
+            }
+            case HP_RELU: {
+                const bool into_bn = nd.relu_fused && st->nodes[L.in0].L.kind == HP_BN;
+                if (into_bn) {
+                    // the BN backward applies the ReLU mask itself: hand it this gradient
+                    Node& pr = st->nodes[L.in0];
+                    pr.g_alias = gin;
+                    pr.g_written = true;
+                } else if (dest(L.in0, &d, &acc)) {
+                    e = launch_relu_bwd(nd.y, gin, d, nd.out_elems, acc, s);
+                }
+                break;
+            }
+            case HP_MAXPOOL:
+                if (dest(L.in0, &d, &acc))
+                    e = launch_maxpool_bwd(in, gin, d, B, nd.inH, nd.inW, nd.inC, L.R, L.S,
+                                           L.stride, L.pad, nd.H, nd.W, acc, s);
+                break;
+            case HP_BN: {
+                // with a fused ReLU, nd.y holds the ReLU output and serves as the mask
+                bool want = dest(L.in0, &d, &acc);
+                e = launch_bn_bwd(in, gin, nd.fuses_relu ? nd.y : nullptr, (long)B * nd.H * nd.W,
+                                  nd.C, w + nd.w_off, nd.mean, nd.invstd, want ? d : nullptr,
+                                  grad + nd.w_off, grad + nd.b_off, want ? acc : 0, st->ws, s);
+                break;
+            }
+            case HP_ADD: {
+                if (dest(L.in0, &d, &acc)) e = launch_copy_or_acc(gin, d, nd.out_elems, acc, s);
+                if (e == hipSuccess && dest(L.in1, &d, &acc))
+                    e = launch_copy_or_acc(gin, d, nd.out_elems, acc, s);
+                break;
+            }
+            case HP_GAP:
+                if (dest(L.in0, &d, &acc))
+                    e = launch_gap_bwd(gin, d, B, nd.inH * nd.inW, nd.C, acc, s);
+                break;
+        }
+        int rc = launch_ok(e, "backward", i);
+        if (rc) return rc;
+    }
+    st->fwd_done = false;
+    return HP_OK;
+}
+
+// ======================================================== parameter server
+
+extern "C" int hp_ps_create(size_t P, const float* w0, int N, int D, void* stream, hp_ps** out) {
+    if (!out) return fail(HP_ERR_ARG, "hp_ps_create: out is NULL");
+    *out = nullptr;
+    if (P == 0 || !w0 || N <= 0 || D < 0) return fail(HP_ERR_ARG, "hp_ps_create: bad arguments");
+    hp_ps* ps = new hp_ps();
+    ps->P = P; ps->N = N; ps->D = D;
+    ps->stream = (hipStream_t)stream;
+    ps->clock.assign(N, 0);
+    ps->pushed.assign(N, 0);
+    ps->vws.assign(N, nullptr);
+    hipError_t e = hipMalloc(&ps->wg, round_up(P, 64) * sizeof(float));
+    if (e != hipSuccess) {
+        delete ps;
+        return fail(e == hipErrorOutOfMemory ? HP_ERR_NOMEM : HP_ERR_HIP, "hp_ps_create: %s",
+                    hipGetErrorString(e));
+    }
+    e = launch_wsp_copy(w0, ps->wg, P, ps->stream);
+    if (e != hipSuccess) {
+        (void)hipFree(ps->wg);
+        delete ps;
+        return fail(HP_ERR_HIP, "hp_ps_create: copy failed: %s", hipGetErrorString(e));
+    }
+    *out = ps;
+    return HP_OK;
+}
+
+extern "C" int hp_ps_destroy(hp_ps* ps) {
+    if (!ps) return HP_OK;
+    for (hp_vw* v : ps->vws)
+        if (v) v->ps = nullptr;
+    (void)hipStreamSynchronize(ps->stream);
+    (void)hipFree(ps->wg);
+    delete ps;
+    return HP_OK;
+}
+
+extern "C" int hp_ps_weights(const hp_ps* ps, const float** wg) {
+    if (!ps || !wg) return fail(HP_ERR_ARG, "hp_ps_weights: NULL argument");
+    *wg = ps->wg;
+    return HP_OK;
+}
+
+extern "C" int hp_ps_clock(const hp_ps* ps, int* c_global) {
+    if (!ps || !c_global) return fail(HP_ERR_ARG, "hp_ps_clock: NULL argument");
+    *c_global = ps->cg;
+    return HP_OK;
+}
+
+// ========================================================== virtual worker
+
+extern "C" int hp_vw_create(hp_ps* ps, int id, int s_local, hp_vw** out) {
+    if (!out) return fail(HP_ERR_ARG, "hp_vw_create: out is NULL");
+    *out = nullptr;
+    if (!ps || id < 0 || id >= ps->N || s_local < 0)
+        return fail(HP_ERR_ARG, "hp_vw_create: bad arguments");
+    if (ps->vws[id]) return fail(HP_ERR_STATE, "hp_vw_create: VW %d already exists", id);
+    hp_vw* v = new hp_vw();
+    v->ps = ps;
+    v->id = id;
+    v->W = s_local + 1;
+    v->P = ps->P;
+    v->stride = round_up(ps->P, 64);     // 256-byte aligned ring slots
+    hipError_t e = hipMalloc(&v->ring, (size_t)v->W * v->stride * sizeof(float));
+    if (e == hipSuccess) e = hipMalloc(&v->ut, v->stride * sizeof(float));
+    if (e != hipSuccess) {
+        if (v->ring) (void)hipFree(v->ring);
+        delete v;
+        return fail(e == hipErrorOutOfMemory ? HP_ERR_NOMEM : HP_ERR_HIP, "hp_vw_create: %s",
+                    hipGetErrorString(e));
+    }
+    // w_1 = ... = w_W = the server's current weights
+    for (int s = 0; s < v->W && e == hipSuccess; ++s)
+        e = launch_wsp_copy(ps->wg, v->ring + (size_t)s * v->stride, v->P, ps->stream);
+    if (e != hipSuccess) {
+        (void)hipFree(v->ring);
+        (void)hipFree(v->ut);
+        delete v;
+        return fail(HP_ERR_HIP, "hp_vw_create: copy failed: %s", hipGetErrorString(e));
+    }
+    v->V.assign(v->W, std::vector<int64_t>(ps->N, 0));
+    for (int n = 0; n < ps->N; ++n) {
+        // a VW created after others pushed starts from w_g and its contents
+        for (int s = 0; s < v->W; ++s) v->V[s][n] = (int64_t)v->W * ps->pushed[n];
+    }
+    ps->vws[id] = v;
+    *out = v;
+    return HP_OK;
+}
+
+extern "C" int hp_vw_destroy(hp_vw* v) {
+    if (!v) return HP_OK;
+    if (v->ps) {
+        (void)hipStreamSynchronize(v->ps->stream);
+        v->ps->vws[v->id] = nullptr;
+    } else {
+        (void)hipDeviceSynchronize();
+    }
+    (void)hipFree(v->ring);
+    (void)hipFree(v->ut);
+    delete v;
+    return HP_OK;
+}
+
+extern "C" int hp_wsp_weights(hp_vw* v, const float** w) {
+    if (!v || !w) return fail(HP_ERR_ARG, "hp_wsp_weights: NULL argument");
+    if (!v->ps) return fail(HP_ERR_STATE, "hp_wsp_weights: parameter server destroyed");
+    if (v->push_due) return fail(HP_ERR_STATE, "hp_wsp_weights: wave %d not pushed yet", v->c);
+    if (v->need_pull)
+        return fail(HP_ERR_STATE, "hp_wsp_weights: VW %d is gated by the clock bound", v->id);
+    int slot = (int)(v->p % v->W);
+    *w = v->ring + (size_t)slot * v->stride;
+    v->in_flight = true;
+    return HP_OK;
+}
+
+extern "C" int hp_wsp_local_update(hp_vw* v, const float* grad, float lr) {
+    if (!v || !grad) return fail(HP_ERR_ARG, "hp_wsp_local_update: NULL argument");
+    if (!v->ps) return fail(HP_ERR_STATE, "hp_wsp_local_update: parameter server destroyed");
+    if (!v->in_flight)
+        return fail(HP_ERR_STATE, "hp_wsp_local_update: no minibatch was started (hp_wsp_weights)");
+    const int64_t q = v->p + 1;
+    const int W = v->W;
+    const int slot = (int)((q - 1) % W);
+    const int newest = (int)((q - 2 + W) % W);
+    const int first = ((q - 1) % W) == 0;
+    hipError_t e = launch_wsp_local_update(grad, v->ring + (size_t)newest * v->stride,
+                                           v->ring + (size_t)slot * v->stride, v->ut, v->P, lr,
+                                           first, v->ps->stream);
+    if (e != hipSuccess) return fail(HP_ERR_HIP, "local update launch: %s", hipGetErrorString(e));
+    std::vector<int64_t> nv = v->V[newest];
+    nv[v->id] += 1;
+    v->V[slot] = nv;
+    v->p = q;
+    v->in_flight = false;
+    if (q % W == 0) v->push_due = true;
+    return HP_OK;
+}
+
+extern "C" int hp_wsp_push_wave(hp_vw* v, hp_ps* ps) {
+    if (!v || !ps) return fail(HP_ERR_ARG, "hp_wsp_push_wave: NULL argument");
+    if (v->ps != ps) return fail(HP_ERR_ARG, "hp_wsp_push_wave: VW belongs to another server");
+    if (!v->push_due)
+        return fail(HP_ERR_STATE, "hp_wsp_push_wave: VW %d has no completed, unpushed wave", v->id);
+    hipError_t e = launch_wsp_push(ps->wg, v->ut, v->P, ps->stream);
+    if (e != hipSuccess) return fail(HP_ERR_HIP, "push launch: %s", hipGetErrorString(e));
+    ps->pushed[v->id] += 1;
+    v->c = (int)(v->p / v->W);
+    ps->clock[v->id] = v->c;
+    ps->cg = *std::min_element(ps->clock.begin(), ps->clock.end());
+    v->push_due = false;
+    v->need_pull = true;
+    return HP_OK;
+}
+
+extern "C" int hp_wsp_pull(hp_vw* v, hp_ps* ps) {
+    if (!v || !ps) return fail(HP_ERR_ARG, "hp_wsp_pull: NULL argument");
+    if (v->ps != ps) return fail(HP_ERR_ARG, "hp_wsp_pull: VW belongs to another server");
+    if (!v->need_pull) return HP_OK;
+    const int need = v->c - ps->D;
+    if (v->g >= need) {            // the last pull still satisfies the bound
+        v->need_pull = false;
+        return HP_OK;
+    }
+    if (ps->cg < need) return HP_WOULD_BLOCK;
+    const int slot = (int)((v->p - 1) % v->W);
+    hipError_t e = launch_wsp_copy(ps->wg, v->ring + (size_t)slot * v->stride, v->P, ps->stream);
+    if (e != hipSuccess) return fail(HP_ERR_HIP, "pull launch: %s", hipGetErrorString(e));
+    for (int n = 0; n < ps->N; ++n) v->V[slot][n] = (int64_t)v->W * ps->pushed[n];
+    v->g = ps->cg;
+    v->need_pull = false;
+    return HP_OK;
+}
+
+extern "C" int hp_wsp_state(const hp_vw* v, hp_wsp_state_t* out) {
+    if (!v || !out) return fail(HP_ERR_ARG, "hp_wsp_state: NULL argument");
+    out->p = v->p;
+    out->W = v->W;
+    out->c = v->c;
+    out->g = v->g;
+    out->push_due = v->push_due ? 1 : 0;
+    out->gated = v->need_pull ? 1 : 0;
+    out->next_slot = (int)(v->p % v->W);
+    out->n_vw = v->ps ? v->ps->N : (int)v->V[0].size();
+    return HP_OK;
+}
+
+extern "C" int hp_wsp_version(const hp_vw* v, int64_t* V) {
+    if (!v || !V) return fail(HP_ERR_ARG, "hp_wsp_version: NULL argument");
+    const std::vector<int64_t>& vv = v->V[(size_t)(v->p % v->W)];
+    for (size_t n = 0; n < vv.size(); ++n) V[n] = vv[n];
+    return HP_OK;
+}
+
+extern "C" int hp_wsp_buffers(const hp_vw* v, const float** ring, size_t* slot_stride,
+                              const float** utilde) {
+    if (!v || !ring || !slot_stride || !utilde)
+        return fail(HP_ERR_ARG, "hp_wsp_buffers: NULL argument");
+    *ring = v->ring;
+    *slot_stride = v->stride;
+    *utilde = v->ut;
+    return HP_OK;
+}
+
+extern "C" const char* hp_last_error(void) { return g_last_error.c_str(); }

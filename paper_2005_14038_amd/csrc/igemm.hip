@@ -1,0 +1,468 @@
+// Implicit-GEMM convolution / FC contractions on CDNA4 MFMA (gfx950).
+//
+// One kernel template covers the three contractions of a convolution layer
+// (an FC layer is a 1x1 convolution on a 1x1 map):
+//
+//   forward  out[m = (n,p,q)][k]     = sum_{(r,s,c)} x[n, p*st-pad+r, q*st-pad+s, c] w[k,r,s,c]
+//   dgrad    out[m = (n,h,w)][c]     = sum_{(r,s,k)} dy[n, (h+pad-r)/st, (w+pad-s)/st, k] w[k,r,s,c]
+//                                      (only taps where the division is exact and in range)
+//   wgrad    out[k][j = (r,s,c)]     = sum_{(n,p,q)} dy[n,p,q,k] x[n, p*st-pad+r, q*st-pad+s, c]
+//
+// The operands are gathered straight from the NHWC activations and the KRSC
+// weights ("implicit" im2col: nothing is materialised), staged through LDS in
+// [BK][BM] / [BK][BN] tiles (the GEMM's row index contiguous), double
+// buffered, and fed to v_mfma_f32_32x32x2_f32.  256 threads = 4 wave64s, each
+// owning a 64x64 block of the output as 2x2 MFMA 32x32 tiles.
+//
+// Long reductions (weight gradients reduce over N*P*Q, FC layers over their
+// fan-in) are split over blockIdx.y; each split writes a partial tile to a
+// workspace and a second kernel adds the partials in a fixed order, so results
+// are deterministic.  In bf16 mode every operand is rounded to bfloat16 (RNE)
+// when it is staged; products of bf16 values are exact in fp32 and the
+// accumulation stays fp32.
+#include "kernels.h"
+
+namespace hp {
+
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+
+namespace {
+
+constexpr int NT = 256;   // threads per workgroup
+constexpr int BK = 16;    // reduction tile
+constexpr int PAD = 4;    // LDS row padding (floats)
+
+struct KArgs {
+    ConvGeo g;
+    const float* a;
+    const float* b;
+    float* out;
+    const float* bias;
+    long M, Ncols, Kred;
+    int kchunk;
+    int tiles_m, tiles_n;
+    int splits;
+    int epi;
+};
+
+__device__ __forceinline__ float round_bf16(float x) {
+    unsigned u = __float_as_uint(x);
+    u = (u + 0x7FFFu + ((u >> 16) & 1u)) & 0xFFFF0000u;
+    return __uint_as_float(u);
+}
+
+template <bool BF>
+__device__ __forceinline__ float cvt(float x) {
+    if constexpr (BF) return round_bf16(x);
+    else return x;
+}
+
+// ---- operand gathers -------------------------------------------------------
+// Each returns VW consecutive elements along the operand's contiguous axis
+// (zero where the element lies outside the problem or in the padding).
+
+template <int VW>
+__device__ __forceinline__ void load_vec(const float* p, bool ok, float* v) {
+    if constexpr (VW == 4) {
+        if (ok) {
+            float4 t = *reinterpret_cast<const float4*>(p);
+            v[0] = t.x; v[1] = t.y; v[2] = t.z; v[3] = t.w;
+        } else {
+            v[0] = v[1] = v[2] = v[3] = 0.f;
+        }
+    } else {
+        v[0] = ok ? *p : 0.f;
+    }
+}
+
+template <int OP, int BM, int BN, int VW, bool BF>
+__global__ void __launch_bounds__(NT, 2) igemm_kernel(KArgs args) {
+    constexpr int LDA = BM + PAD;
+    constexpr int LDB = BN + PAD;
+    constexpr int WAVES_N = BN / 64;           // wave grid: (BM/64) x (BN/64) = 4
+    static_assert((BM / 64) * (BN / 64) == 4, "4 waves of 64x64");
+    __shared__ float smem[2 * BK * (LDA + LDB)];
+
+    const ConvGeo& g = args.g;
+    const int t = threadIdx.x;
+    const int lane = t & 63;
+    const int wave = t >> 6;
+    const int wm = (wave / WAVES_N) * 64;
+    const int wn = (wave % WAVES_N) * 64;
+
+    // XCD-aware tile order: consecutive workgroup ids are dealt round-robin to
+    // the 8 XCDs; give each XCD a contiguous run of tiles (n fastest) so tiles
+    // that share A rows share that XCD's L2.
+    const int ntiles = args.tiles_m * args.tiles_n;
+    int bid = blockIdx.x;
+    if ((ntiles & 7) == 0) bid = (bid & 7) * (ntiles >> 3) + (bid >> 3);
+    const int tm = bid / args.tiles_n;
+    const int tn = bid % args.tiles_n;
+    const long m0 = (long)tm * BM;
+    const long n0 = (long)tn * BN;
+    const int z = blockIdx.y;
+    const long kbeg = (long)z * args.kchunk;
+    const long kend = min(kbeg + (long)args.kchunk, args.Kred);
+    const int ktiles = (int)((kend - kbeg + BK - 1) / BK);
+
+    // ---- per-thread staging coordinates ----
+    // A: OP_FWD / OP_DGRAD gather rows m with the reduction index contiguous
+    // ("k-major"); OP_WGRAD reads dy rows (reduction index = row) with m = k
+    // contiguous ("m-major").  B: OP_FWD reads weight rows (k-major);
+    // OP_DGRAD / OP_WGRAD read rows indexed by the reduction with n contiguous.
+    constexpr bool A_KMAJ = (OP != OP_WGRAD);
+    constexpr bool B_KMAJ = (OP == OP_FWD);
+    constexpr int AV = A_KMAJ ? (BM * BK / VW / NT) : (BM * BK / VW / NT);
+    constexpr int BV = (BN * BK / VW / NT);
+    static_assert(AV >= 1 && BV >= 1, "tile too small");
+
+    // A, k-major: vector i covers row (t + i*NT) / (BK/VW), reduction offset kva
+    constexpr int KVPR = BK / VW;               // vectors per k-major row
+    constexpr int AVPR = BM / VW;               // vectors per m-major row (A)
+    constexpr int BVPR = BN / VW;               // vectors per n-major row (B)
+
+    // precomputed per-row data for gathered rows
+    int arow_base[AV];   // FWD: n*H*W*C ; DGRAD: n*P*Q*K ; WGRAD: column m (k-out)
+    int arow_h[AV], arow_w[AV];
+    bool arow_ok[AV];
+    int akv = 0;
+    if constexpr (A_KMAJ) {
+        akv = (t % KVPR) * VW;
+#pragma unroll
+        for (int i = 0; i < AV; ++i) {
+            long m = m0 + (t + i * NT) / KVPR;
+            arow_ok[i] = m < args.M;
+            long mm = arow_ok[i] ? m : 0;
+            if constexpr (OP == OP_FWD) {
+                int q = (int)(mm % g.Q); long tt = mm / g.Q;
+                int p = (int)(tt % g.P); int n = (int)(tt / g.P);
+                arow_base[i] = n * g.H * g.W * g.C;
+                arow_h[i] = p * g.st - g.pad;
+                arow_w[i] = q * g.st - g.pad;
+            } else {  // DGRAD: m = (n, h, w)
+                int w = (int)(mm % g.W); long tt = mm / g.W;
+                int h = (int)(tt % g.H); int n = (int)(tt / g.H);
+                arow_base[i] = n * g.P * g.Q * g.K;
+                arow_h[i] = h + g.pad;
+                arow_w[i] = w + g.pad;
+            }
+        }
+    } else {
+#pragma unroll
+        for (int i = 0; i < AV; ++i) {
+            long m = m0 + ((t + i * NT) % AVPR) * VW;
+            arow_ok[i] = m < args.M;
+            arow_base[i] = (int)m;
+            arow_h[i] = arow_w[i] = 0;
+        }
+    }
+    // B
+    int bcol_r = 0, bcol_s = 0, bcol_c = 0;
+    bool bcol_ok = true;
+    long brow_n[BV];
+    bool brow_ok[BV];
+    int bkv = 0;
+    if constexpr (B_KMAJ) {
+        bkv = (t % KVPR) * VW;
+#pragma unroll
+        for (int i = 0; i < BV; ++i) {
+            long n = n0 + (t + i * NT) / KVPR;
+            brow_ok[i] = n < args.Ncols;
+            brow_n[i] = brow_ok[i] ? n : 0;
+        }
+    } else {
+        long col = n0 + (t % BVPR) * VW;
+        bcol_ok = col < args.Ncols;
+        long cc = bcol_ok ? col : 0;
+        if constexpr (OP == OP_WGRAD) {  // col = (r, s, c)
+            bcol_c = (int)(cc % g.C); long tt = cc / g.C;
+            bcol_s = (int)(tt % g.S); bcol_r = (int)(tt / g.S);
+        } else {                          // DGRAD: col = c
+            bcol_c = (int)cc;
+        }
+#pragma unroll
+        for (int i = 0; i < BV; ++i) { brow_n[i] = 0; brow_ok[i] = true; }
+    }
+
+    float areg[AV][VW];
+    float breg[BV][VW];
+
+    auto gload = [&](int kt) {
+        const long k0 = kbeg + (long)kt * BK;
+        // ---- A ----
+#pragma unroll
+        for (int i = 0; i < AV; ++i) {
+            if constexpr (OP == OP_FWD) {
+                long kk = k0 + akv;
+                bool ok = arow_ok[i] && kk < kend;
+                int c = (int)(kk % g.C); int rs = (int)(kk / g.C);
+                int s = rs % g.S, r = rs / g.S;
+                int h = arow_h[i] + r, w = arow_w[i] + s;
+                ok = ok && (unsigned)h < (unsigned)g.H && (unsigned)w < (unsigned)g.W;
+                const float* p = args.a + (ok ? (arow_base[i] + ((long)h * g.W + w) * g.C + c) : 0);
+                load_vec<VW>(p, ok, areg[i]);
+            } else if constexpr (OP == OP_DGRAD) {
+                long kk = k0 + akv;
+                bool ok = arow_ok[i] && kk < kend;
+                int k = (int)(kk % g.K); int rs = (int)(kk / g.K);
+                int s = rs % g.S, r = rs / g.S;
+                int tp = arow_h[i] - r, tq = arow_w[i] - s;
+                int p = tp / g.st, q = tq / g.st;
+                ok = ok && tp >= 0 && tq >= 0 && p * g.st == tp && q * g.st == tq &&
+                     p < g.P && q < g.Q;
+                const float* ptr = args.a + (ok ? (arow_base[i] + ((long)p * g.Q + q) * g.K + k) : 0);
+                load_vec<VW>(ptr, ok, areg[i]);
+            } else {  // WGRAD: A[kk = m'][m = k-out] = dy[m'][k]
+                long kk = k0 + (t + i * NT) / AVPR;
+                bool ok = arow_ok[i] && kk < kend;
+                const float* ptr = args.b + (ok ? (kk * g.K + arow_base[i]) : 0);
+                load_vec<VW>(ptr, ok, areg[i]);
+            }
+        }
+        // ---- B ----
+#pragma unroll
+        for (int i = 0; i < BV; ++i) {
+            if constexpr (OP == OP_FWD) {
+                long kk = k0 + bkv;
+                bool ok = brow_ok[i] && kk < kend;
+                const float* ptr = args.b + (ok ? (brow_n[i] * args.Kred + kk) : 0);
+                load_vec<VW>(ptr, ok, breg[i]);
+            } else if constexpr (OP == OP_DGRAD) {  // B[kk = (r,s,k)][c] = w[k][r][s][c]
+                long kk = k0 + (t + i * NT) / BVPR;
+                bool ok = bcol_ok && kk < kend;
+                int k = (int)(kk % g.K); int rs = (int)(kk / g.K);
+                int s = rs % g.S, r = rs / g.S;
+                const float* ptr = args.b + (ok ? ((((long)k * g.R + r) * g.S + s) * g.C + bcol_c) : 0);
+                load_vec<VW>(ptr, ok, breg[i]);
+            } else {  // WGRAD: B[kk = (n,p,q)][j = (r,s,c)] = x[n, p*st-pad+r, q*st-pad+s, c]
+                long kk = k0 + (t + i * NT) / BVPR;
+                bool ok = bcol_ok && kk < kend;
+                long kc = ok ? kk : 0;
+                int q = (int)(kc % g.Q); long tt = kc / g.Q;
+                int p = (int)(tt % g.P); int n = (int)(tt / g.P);
+                int h = p * g.st - g.pad + bcol_r, w = q * g.st - g.pad + bcol_s;
+                ok = ok && (unsigned)h < (unsigned)g.H && (unsigned)w < (unsigned)g.W;
+                const float* ptr = args.a + (ok ? ((((long)n * g.H + h) * g.W + w) * g.C + bcol_c) : 0);
+                load_vec<VW>(ptr, ok, breg[i]);
+            }
+        }
+    };
+
+    auto sstore = [&](int buf) {
+        float* As = smem + buf * BK * (LDA + LDB);
+        float* Bs = As + BK * LDA;
+#pragma unroll
+        for (int i = 0; i < AV; ++i) {
+            if constexpr (A_KMAJ) {
+                int row = (t + i * NT) / KVPR;
+#pragma unroll
+                for (int j = 0; j < VW; ++j) As[(akv + j) * LDA + row] = cvt<BF>(areg[i][j]);
+            } else {
+                int kr = (t + i * NT) / AVPR;
+                int col = ((t + i * NT) % AVPR) * VW;
+#pragma unroll
+                for (int j = 0; j < VW; ++j) As[kr * LDA + col + j] = cvt<BF>(areg[i][j]);
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < BV; ++i) {
+            if constexpr (B_KMAJ) {
+                int row = (t + i * NT) / KVPR;
+#pragma unroll
+                for (int j = 0; j < VW; ++j) Bs[(bkv + j) * LDB + row] = cvt<BF>(breg[i][j]);
+            } else {
+                int kr = (t + i * NT) / BVPR;
+                int col = ((t + i * NT) % BVPR) * VW;
+#pragma unroll
+                for (int j = 0; j < VW; ++j) Bs[kr * LDB + col + j] = cvt<BF>(breg[i][j]);
+            }
+        }
+    };
+
+    floatx16 acc[2][2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+
+    if (ktiles > 0) {
+        gload(0);
+        sstore(0);
+    }
+    __syncthreads();
+    const int lr = lane & 31;
+    const int lk = lane >> 5;
+    for (int kt = 0; kt < ktiles; ++kt) {
+        const int buf = kt & 1;
+        if (kt + 1 < ktiles) gload(kt + 1);
+        const float* As = smem + buf * BK * (LDA + LDB);
+        const float* Bs = As + BK * LDA;
+#pragma unroll
+        for (int kk = 0; kk < BK; kk += 2) {
+            const float* ar = As + (kk + lk) * LDA + wm + lr;
+            const float* br = Bs + (kk + lk) * LDB + wn + lr;
+            float a0 = ar[0], a1 = ar[32];
+            float b0 = br[0], b1 = br[32];
+            acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0, b0, acc[0][0], 0, 0, 0);
+            acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0, b1, acc[0][1], 0, 0, 0);
+            acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1, b0, acc[1][0], 0, 0, 0);
+            acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1, b1, acc[1][1], 0, 0, 0);
+        }
+        if (kt + 1 < ktiles) sstore(buf ^ 1);
+        __syncthreads();
+    }
+
+    // ---- epilogue ----
+    // acc[i][j][v] holds out[m0 + wm + 32i + 8(v/4) + 4(lane/32) + v%4][n0 + wn + 32j + lane%32]
+    const bool partial = args.splits > 1;
+    float* out = args.out + (partial ? (long)z * args.M * args.Ncols : 0);
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+        const long col = n0 + wn + 32 * j + lr;
+        if (col >= args.Ncols) continue;
+        float bv = 0.f;
+        if (!partial && (args.epi & EPI_BIAS)) bv = args.bias[col];
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const long row = m0 + wm + 32 * i + 8 * (v >> 2) + 4 * lk + (v & 3);
+                if (row >= args.M) continue;
+                float val = acc[i][j][v];
+                float* dst = out + row * args.Ncols + col;
+                if (!partial) {
+                    val += bv;
+                    if (args.epi & EPI_RELU) val = fmaxf(val, 0.f);
+                    if (args.epi & EPI_ACCUM) val += *dst;
+                }
+                *dst = val;
+            }
+        }
+    }
+}
+
+template <int OP, int BM, int BN, int VW, bool BF>
+hipError_t launch_cfg(const KArgs& a, hipStream_t s) {
+    dim3 grid(a.tiles_m * a.tiles_n, a.splits);
+    hipLaunchKernelGGL((igemm_kernel<OP, BM, BN, VW, BF>), grid, dim3(NT), 0, s, a);
+    return hipGetLastError();
+}
+
+template <int OP, int VW, bool BF>
+hipError_t launch_op(int cfg, const KArgs& a, hipStream_t s) {
+    switch (cfg) {
+        case 0: return launch_cfg<OP, 128, 128, VW, BF>(a, s);
+        case 1: return launch_cfg<OP, 256, 64, VW, BF>(a, s);
+        default: return launch_cfg<OP, 64, 256, VW, BF>(a, s);
+    }
+}
+
+void tile_shape(int cfg, int& bm, int& bn) {
+    bm = cfg == 0 ? 128 : (cfg == 1 ? 256 : 64);
+    bn = cfg == 0 ? 128 : (cfg == 1 ? 64 : 256);
+}
+
+int choose_cfg(long M, long N) {
+    if (N <= 64 && M > 64) return 1;
+    if (M <= 64 && N > 64) return 2;
+    return 0;
+}
+
+__global__ void splitk_reduce_kernel(const float* __restrict__ ws, int splits, long M, long Ncols,
+                                     float* __restrict__ out, const float* __restrict__ bias,
+                                     int epi) {
+    const long total = M * Ncols;
+    const long stride = (long)gridDim.x * blockDim.x;
+    for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += stride) {
+        float acc = 0.f;
+        for (int z = 0; z < splits; ++z) acc += ws[(long)z * total + i];
+        if (epi & EPI_BIAS) acc += bias[i % Ncols];
+        if (epi & EPI_RELU) acc = fmaxf(acc, 0.f);
+        if (epi & EPI_ACCUM) acc += out[i];
+        out[i] = acc;
+    }
+}
+
+}  // namespace
+
+GemmPlan plan_gemm(int op, const ConvGeo& g, int bf16, int num_cus) {
+    GemmPlan p{};
+    p.op = op;
+    p.bf16 = bf16;
+    if (op == OP_FWD) {
+        p.M = (long)g.N * g.P * g.Q; p.Ncols = g.K; p.Kred = (long)g.R * g.S * g.C;
+    } else if (op == OP_DGRAD) {
+        p.M = (long)g.N * g.H * g.W; p.Ncols = g.C; p.Kred = (long)g.R * g.S * g.K;
+    } else {
+        p.M = g.K; p.Ncols = (long)g.R * g.S * g.C; p.Kred = (long)g.N * g.P * g.Q;
+    }
+    int cfg = choose_cfg(p.M, p.Ncols);
+    int bm, bn;
+    tile_shape(cfg, bm, bn);
+    long tiles = ((p.M + bm - 1) / bm) * ((p.Ncols + bn - 1) / bn);
+    long ktiles = (p.Kred + BK - 1) / BK;
+    // split the reduction when the output alone cannot fill the chip
+    long target = 4L * num_cus;
+    long splits = 1;
+    if (tiles < target) {
+        splits = (target + tiles - 1) / tiles;
+        long max_splits = ktiles / 8;        // keep >= 8 reduction tiles per split
+        if (splits > max_splits) splits = max_splits;
+        if (splits < 1) splits = 1;
+    }
+    long chunk_tiles = (ktiles + splits - 1) / splits;
+    p.kchunk = (int)(chunk_tiles * BK);
+    p.splits = (int)((ktiles + chunk_tiles - 1) / chunk_tiles);
+    p.ws_floats = p.splits > 1 ? (size_t)p.splits * p.M * p.Ncols : 0;
+    return p;
+}
+
+hipError_t launch_gemm(const GemmPlan& plan, const ConvGeo& g, const float* a, const float* b,
+                       float* out, const float* bias, int epi, float* ws, hipStream_t s) {
+    KArgs k{};
+    k.g = g;
+    k.a = a;
+    k.b = b;
+    k.bias = bias;
+    k.M = plan.M;
+    k.Ncols = plan.Ncols;
+    k.Kred = plan.Kred;
+    k.kchunk = plan.kchunk;
+    k.splits = plan.splits;
+    k.epi = epi;
+    int cfg = choose_cfg(plan.M, plan.Ncols);
+    int bm, bn;
+    tile_shape(cfg, bm, bn);
+    k.tiles_m = (int)((plan.M + bm - 1) / bm);
+    k.tiles_n = (int)((plan.Ncols + bn - 1) / bn);
+    k.out = plan.splits > 1 ? ws : out;
+    // vector width 4 needs the contiguous axes to be multiples of 4
+    bool v4;
+    if (plan.op == OP_FWD) v4 = (g.C % 4 == 0);
+    else v4 = (g.C % 4 == 0) && (g.K % 4 == 0);
+    v4 = v4 && ((((uintptr_t)a) | ((uintptr_t)b)) & 15) == 0;
+    hipError_t e;
+    const bool bf = plan.bf16 != 0;
+#define HP_DISPATCH(OPC)                                                       \
+    if (v4) e = bf ? launch_op<OPC, 4, true>(cfg, k, s) : launch_op<OPC, 4, false>(cfg, k, s); \
+    else e = bf ? launch_op<OPC, 1, true>(cfg, k, s) : launch_op<OPC, 1, false>(cfg, k, s);
+    if (plan.op == OP_FWD) { HP_DISPATCH(OP_FWD) }
+    else if (plan.op == OP_DGRAD) { HP_DISPATCH(OP_DGRAD) }
+    else { HP_DISPATCH(OP_WGRAD) }
+#undef HP_DISPATCH
+    if (e != hipSuccess || plan.splits == 1) return e;
+    return launch_splitk_reduce(ws, plan.splits, plan.M, plan.Ncols, out, bias, epi, s);
+}
+
+hipError_t launch_splitk_reduce(const float* ws, int splits, long M, long Ncols, float* out,
+                                const float* bias, int epi, hipStream_t s) {
+    long total = M * Ncols;
+    int blocks = (int)std::min<long>((total + 255) / 256, 4096);
+    hipLaunchKernelGGL(splitk_reduce_kernel, dim3(blocks), dim3(256), 0, s, ws, splits, M, Ncols,
+                       out, bias, epi);
+    return hipGetLastError();
+}
+
+}  // namespace hp

@@ -1,0 +1,100 @@
+// Internal launch interface of the gfx950 kernels (not part of the C ABI).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <cstddef>
+#include <cstdint>
+
+namespace hp {
+
+// Geometry of one convolution (FC layers are 1x1 convolutions on a 1x1 map).
+struct ConvGeo {
+    int N, H, W, C;   // input  [N][H][W][C]
+    int K, R, S;      // weight [K][R][S][C]
+    int P, Q;         // output [N][P][Q][K]
+    int st, pad;
+};
+
+enum GemmOp { OP_FWD = 0, OP_DGRAD = 1, OP_WGRAD = 2 };
+
+// Implicit-GEMM contraction on MFMA.
+//   OP_FWD:   out[N*P*Q][K]   = conv(x, w) (+ bias) (relu)
+//   OP_DGRAD: out[N*H*W][C]   = dgrad(dy, w)        (accumulate adds into out)
+//   OP_WGRAD: out[K][R*S*C]   = wgrad(x, dy)
+// `a` is x (FWD, WGRAD) or dy (DGRAD); `b` is w (FWD, DGRAD) or dy (WGRAD).
+struct GemmPlan {
+    int op;
+    int bf16;          // round operands to bf16 (RNE) when staging
+    int splits;        // split-K factor (1 = direct epilogue)
+    int kchunk;        // reduction length per split (multiple of the K tile)
+    size_t ws_floats;  // workspace needed (splits * M * Ncols when splits > 1)
+    long M, Ncols, Kred;
+};
+
+GemmPlan plan_gemm(int op, const ConvGeo& g, int bf16, int num_cus);
+
+// epilogue flags
+enum { EPI_BIAS = 1, EPI_RELU = 2, EPI_ACCUM = 4 };
+
+hipError_t launch_gemm(const GemmPlan& plan, const ConvGeo& g, const float* a,
+                       const float* b, float* out, const float* bias, int epi,
+                       float* ws, hipStream_t s);
+
+// ---- element-wise / reduction kernels (elementwise.hip) -------------------
+// y = max(x, 0)
+hipError_t launch_relu_fwd(const float* x, float* y, size_t n, hipStream_t s);
+// dx = dy * (y > 0); with accumulate, dx += ...
+hipError_t launch_relu_bwd(const float* y, const float* dy, float* dx, size_t n,
+                           int accumulate, hipStream_t s);
+// out = a + b (relu optional)
+hipError_t launch_add_fwd(const float* a, const float* b, float* y, size_t n, int relu,
+                          hipStream_t s);
+// out = v (accumulate = 0) or out += v
+hipError_t launch_copy_or_acc(const float* v, float* out, size_t n, int accumulate,
+                              hipStream_t s);
+hipError_t launch_maxpool_fwd(const float* x, float* y, int N, int H, int W, int C, int R,
+                              int S, int st, int pad, int P, int Q, hipStream_t s);
+hipError_t launch_maxpool_bwd(const float* x, const float* dy, float* dx, int N, int H, int W,
+                              int C, int R, int S, int st, int pad, int P, int Q,
+                              int accumulate, hipStream_t s);
+hipError_t launch_gap_fwd(const float* x, float* y, int N, int HW, int C, hipStream_t s);
+hipError_t launch_gap_bwd(const float* dy, float* dx, int N, int HW, int C, int accumulate,
+                          hipStream_t s);
+
+// Per-channel column reductions over M rows of an [M][C] matrix, deterministic:
+// partial sums over row blocks, then a fixed-order finalisation.
+size_t colsum_ws_floats(long M, int C);
+// out[c] = sum_m v[m][c]  (out may be a device pointer into a gradient vector)
+hipError_t launch_colsum(const float* v, long M, int C, float* out, float* ws, hipStream_t s);
+
+// Batch-norm (training mode).  Statistics: mean[c], invstd[c] = 1/sqrt(var+eps)
+// with the biased variance; apply: y = gamma*(x-mean)*invstd + beta (relu opt.).
+size_t bn_ws_floats(long M, int C);
+hipError_t launch_bn_fwd(const float* x, long M, int C, const float* gamma, const float* beta,
+                         float eps, float* y, float* mean, float* invstd, int relu, float* ws,
+                         hipStream_t s);
+// Backward.  If relu_y != NULL the incoming gradient is first masked by
+// relu_y > 0 (BN followed by ReLU).  Writes dgamma, dbeta and, unless dx is NULL,
+// dx (accumulate optional).
+hipError_t launch_bn_bwd(const float* x, const float* dy, const float* relu_y, long M, int C,
+                         const float* gamma, const float* mean, const float* invstd, float* dx,
+                         float* dgamma, float* dbeta, int accumulate, float* ws, hipStream_t s);
+
+// Softmax cross-entropy: loss (one float) = mean_n (lse(z_n) - z_n[label]);
+// dz = (softmax(z) - onehot) / B.
+hipError_t launch_softmax_ce(const float* z, const int32_t* labels, int B, int K, float* loss,
+                             float* dz, float* ws, hipStream_t s);
+
+// split-K finalisation: out = sum_z ws[z] (+bias[col]) (relu) (accumulate)
+hipError_t launch_splitk_reduce(const float* ws, int splits, long M, long Ncols, float* out,
+                                const float* bias, int epi, hipStream_t s);
+
+// ---- WSP kernels (wsp.hip) ------------------------------------------------
+// u = (-lr)*g; dst = newest + u; ut = first ? u : ut + u   (no FMA contraction)
+hipError_t launch_wsp_local_update(const float* g, const float* newest, float* dst, float* ut,
+                                   size_t n, float lr, int first, hipStream_t s);
+// wg = wg + ut
+hipError_t launch_wsp_push(float* wg, const float* ut, size_t n, hipStream_t s);
+// dst = src
+hipError_t launch_wsp_copy(const float* src, float* dst, size_t n, hipStream_t s);
+
+}  // namespace hp

@@ -93,3 +93,21 @@ def labels(key: int, n: int, classes: int) -> np.ndarray:
     lab = np.floor(u * classes).astype(np.int64)
     np.minimum(lab, classes - 1, out=lab)
     return lab.astype(np.int32)
+
+
+def initial_weights(segments, seed: int) -> np.ndarray:
+    """Initial flat weight vector from a list of parameter segments.
+
+    ``segments`` lists (kind, count, fan_in) in flat-vector order, kind one of
+    "w" (He-normal: N(0, 2/fan_in)), "b" / "beta" (zeros), "gamma" (ones).
+    Segment i of kind "w" draws from stream (seed, 0, i, T_W0)."""
+    parts = []
+    for i, (kind, count, fan_in) in enumerate(segments):
+        if kind == "w":
+            std = float(np.sqrt(2.0 / fan_in))
+            parts.append(normal(stream_key(seed, 0, i, T_W0), count, std))
+        elif kind == "gamma":
+            parts.append(np.ones(count, np.float32))
+        else:
+            parts.append(np.zeros(count, np.float32))
+    return np.concatenate(parts) if parts else np.zeros(0, np.float32)

@@ -1,0 +1,145 @@
+"""Per-operator parity of the HIP kernels against the oracle, through the C ABI.
+
+Each case is a small stage holding the operator under test, run once forward
+and backward on the GPU and in the oracle on the same seeded inputs.  Shapes
+span several MFMA tiles with ragged tails, strides 1 and 2, paddings 0, 1 and
+3, channel counts that are and are not multiples of 4, and split reductions.
+"""
+import numpy as np
+import pytest
+
+from gpu_common import BF16_TOL, FP32_TOL, assert_close, dev  # noqa: F401
+from stage_harness import make_inputs, oracle_weights, run_gpu, run_oracle, single
+
+pytestmark = pytest.mark.gpu
+
+CONV = [
+    # N, H, W, C, K, R, stride, pad, bias
+    (2, 9, 9, 8, 16, 3, 1, 1, True),
+    (2, 13, 11, 5, 7, 3, 2, 1, False),     # C % 4 != 0: scalar staging
+    (3, 8, 8, 3, 8, 3, 1, 1, True),        # an image-input first layer
+    (2, 10, 10, 16, 32, 1, 1, 0, False),
+    (2, 9, 9, 12, 20, 1, 2, 0, False),     # projection shortcut shape
+    (1, 15, 15, 3, 8, 7, 2, 3, False),     # ResNet stem shape
+    (4, 20, 18, 64, 136, 3, 1, 1, True),   # several 128x128 tiles, ragged N
+    (2, 30, 30, 32, 64, 3, 1, 1, True),    # 256x64 tile configuration
+    (16, 4, 4, 256, 40, 3, 1, 1, False),   # long reduction, split-K in wgrad
+]
+
+
+def conv_net(c):
+    N, H, W, C, K, R, st, pad, bias = c
+    return single(lambda n: n.conv(-1, C, K, R, st, pad, bias=bias), H, W, C), N
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+@pytest.mark.parametrize("case", CONV, ids=[str(c[:8]) for c in CONV])
+def test_conv(dev, case, dtype):  # noqa: F811
+    net, B = conv_net(case)
+    w = oracle_weights(net, 11)
+    if case[-1]:
+        w[-case[4]:] = np.linspace(-1, 1, case[4])      # non-zero bias
+    x, _, dy = make_inputs(net, B, 12)
+    g = run_gpu(net, B, w, x, None, dy, True, dtype)
+    r = run_oracle(net, w, x, None, dy, True, bf16=(dtype == "bf16"))
+    tol = FP32_TOL if dtype == "fp32" else BF16_TOL
+    assert_close(g["y"], r["y"], tol, "forward")
+    assert_close(g["grad"], r["grad"], tol, "weight gradient")
+    assert_close(g["dx"], r["dx"], tol, "data gradient")
+
+
+FC = [(4, 1, 1, 37, 50), (32, 2, 3, 16, 96), (5, 3, 3, 64, 260)]
+
+
+@pytest.mark.parametrize("case", FC)
+def test_fc(dev, case):  # noqa: F811
+    B, H, W, C, OUT = case
+    net = single(lambda n: n.fc(-1, H * W * C, OUT), H, W, C)
+    w = oracle_weights(net, 21)
+    w[-OUT:] = np.linspace(-0.5, 0.5, OUT)
+    x, _, dy = make_inputs(net, B, 22)
+    g = run_gpu(net, B, w, x, None, dy, True)
+    r = run_oracle(net, w, x, None, dy, True)
+    assert_close(g["y"], r["y"], FP32_TOL, "forward")
+    assert_close(g["grad"], r["grad"], FP32_TOL, "weight gradient")
+    assert_close(g["dx"], r["dx"], FP32_TOL, "data gradient")
+
+
+POOL = [(2, 8, 8, 4, 2, 2, 0), (2, 9, 7, 6, 3, 2, 1), (1, 11, 11, 64, 3, 2, 1)]
+
+
+@pytest.mark.parametrize("case", POOL)
+def test_maxpool_and_unfused_relu(dev, case):  # noqa: F811
+    B, H, W, C, R, st, pad = case
+
+    def build(n):
+        a = n.maxpool(-1, R, st, pad)
+        n.relu(a)
+    net = single(build, H, W, C)
+    x, _, dy = make_inputs(net, B, 31)
+    g = run_gpu(net, B, np.zeros(0, np.float32), x, None, dy, True)
+    r = run_oracle(net, np.zeros(0), x, None, dy, True)
+    # max-pool and ReLU select values: the results are exact
+    np.testing.assert_array_equal(g["y"], r["y"].astype(np.float32))
+    assert_close(g["dx"], r["dx"], 1e-6, "data gradient")
+
+
+def test_maxpool_ties_route_to_first(dev):  # noqa: F811
+    net = single(lambda n: n.maxpool(-1, 2, 2, 0), 4, 4, 2)
+    x = np.zeros((1, 4, 4, 2), np.float32)
+    dy = np.arange(1, 9, dtype=np.float32).reshape(1, 2, 2, 2)
+    g = run_gpu(net, 1, np.zeros(0, np.float32), x, None, dy, True)
+    r = run_oracle(net, np.zeros(0), x, None, dy, True)
+    np.testing.assert_array_equal(g["dx"], r["dx"].astype(np.float32))
+
+
+@pytest.mark.parametrize("relu", [False, True])
+@pytest.mark.parametrize("shape", [(4, 6, 6, 8), (2, 33, 33, 64), (32, 7, 7, 130)])
+def test_batchnorm(dev, shape, relu):  # noqa: F811
+    B, H, W, C = shape
+
+    def build(n):
+        a = n.bn(-1, C)
+        if relu:
+            n.relu(a)
+    net = single(build, H, W, C)
+    w = oracle_weights(net, 41, scale_bn=True)
+    x, _, dy = make_inputs(net, B, 42)
+    x = 0.5 + 2.0 * x                              # non-zero mean, non-unit variance
+    g = run_gpu(net, B, w, x, None, dy, True)
+    r = run_oracle(net, w, x, None, dy, True)
+    assert_close(g["y"], r["y"], FP32_TOL, "forward")
+    assert_close(g["grad"], r["grad"], FP32_TOL, "gamma/beta gradient")
+    assert_close(g["dx"], r["dx"], FP32_TOL, "data gradient")
+
+
+def test_residual_add_fans_out_to_the_input(dev):  # noqa: F811
+    # y = relu(bn(conv(x)) + x): the input gradient sums the branch and the skip
+    def build(n):
+        a = n.bn(n.conv(-1, 16, 16, 3, 1, 1), 16)
+        n.relu(n.addn(a, -1))
+    net = single(build, 10, 10, 16)
+    w = oracle_weights(net, 51, scale_bn=True)
+    x, _, dy = make_inputs(net, 3, 52)
+    g = run_gpu(net, 3, w, x, None, dy, True)
+    r = run_oracle(net, w, x, None, dy, True)
+    assert_close(g["y"], r["y"], FP32_TOL, "forward")
+    assert_close(g["grad"], r["grad"], FP32_TOL, "weight gradient")
+    assert_close(g["dx"], r["dx"], FP32_TOL, "data gradient")
+
+
+@pytest.mark.parametrize("classes", [10, 1000])
+def test_gap_fc_softmax_ce(dev, classes):  # noqa: F811
+    def build(n):
+        a = n.gap(-1)
+        a = n.fc(a, 48, classes)
+        n.ce(a, classes)
+    net = single(build, 5, 5, 48)
+    w = oracle_weights(net, 61)
+    x, lab, _ = make_inputs(net, 8, 62)
+    g = run_gpu(net, 8, w, x, lab, None, True)
+    r = run_oracle(net, w, x, lab, None, True)
+    assert abs(g["loss"] - r["loss"]) <= FP32_TOL * abs(r["loss"])
+    assert_close(g["y"], r["y"], FP32_TOL, "logits")
+    assert_close(g["grad"], r["grad"], FP32_TOL, "weight gradient")
+    assert_close(g["dx"], r["dx"], FP32_TOL, "data gradient")

@@ -1,0 +1,77 @@
+"""Whole-stage parity (forward + backward of every layer of a stage) on
+reduced spatial sizes of the five workloads' networks, fp32 and bf16."""
+import numpy as np
+import pytest
+
+from oracle import nets as onets
+from gpu_common import BF16_TOL, FP32_TOL, assert_close, dev  # noqa: F401
+from stage_harness import make_inputs, oracle_weights, run_gpu, run_oracle
+
+pytestmark = pytest.mark.gpu
+
+SMALL = {
+    # name: (net, batch, need_dx)
+    "tiny": (lambda: onets.tiny(), 4, True),
+    "vgg19_s1@32": (lambda: onets.vgg19_s1(32, 32), 2, False),
+    "vgg19@32": (lambda: onets.vgg19(32, 32, classes=10, fc_width=64), 2, False),
+    "resnet_mid@16": (lambda: onets.resnet152_mid(16, 16, groups=[(128, 2, 2), (256, 2, 2)]), 2, True),
+    "resnet@64": (lambda: onets.resnet152(64, 64, classes=10,
+                                          groups=[(64, 1, 1), (128, 2, 2), (256, 1, 2), (512, 1, 2)]),
+                  2, False),
+}
+
+
+def _check(name, dtype):
+    mk, B, need_dx = SMALL[name]
+    net = mk()
+    w = oracle_weights(net, 71, scale_bn=True)
+    x, lab, dy = make_inputs(net, B, 72, dy_std=1e-3)
+    g = run_gpu(net, B, w, x, lab, dy, need_dx, dtype)
+    r = run_oracle(net, w, x, lab, dy, need_dx, bf16=(dtype == "bf16"))
+    tol = FP32_TOL if dtype == "fp32" else BF16_TOL
+    if net.has_loss:
+        assert abs(g["loss"] - r["loss"]) <= tol * abs(r["loss"])
+    assert_close(g["y"], r["y"], tol, f"{name} output")
+    assert_close(g["grad"], r["grad"], tol, f"{name} weight gradient")
+    if need_dx:
+        assert_close(g["dx"], r["dx"], tol, f"{name} input gradient")
+
+
+@pytest.mark.parametrize("name", list(SMALL))
+def test_stage_fp32(dev, name):  # noqa: F811
+    _check(name, "fp32")
+
+
+@pytest.mark.parametrize("name", ["tiny", "resnet_mid@16", "resnet@64"])
+def test_stage_bf16(dev, name):  # noqa: F811
+    _check(name, "bf16")
+
+
+def test_stage_protocol_errors(dev):  # noqa: F811
+    import torch
+    from paper_2005_14038_amd import hetpipe as hp
+    from stage_harness import to_layers
+    net = onets.tiny()
+    st = hp.Stage(to_layers(net), 2, 16, 16, 3)
+    w = torch.zeros(st.P, device=dev)
+    g = torch.zeros(st.P, device=dev)
+    with pytest.raises(hp.HPError) as e:            # backward without forward
+        st.backward(w, None, None, g)
+    assert e.value.code == hp.HP_ERR_STATE
+    x = torch.zeros(2, 16, 16, 3, device=dev)
+    lab = torch.zeros(2, dtype=torch.int32, device=dev)
+    loss = torch.zeros(1, device=dev)
+    st.forward(w, x, None, lab, loss)
+    w2 = torch.zeros(st.P, device=dev)
+    with pytest.raises(hp.HPError) as e:            # different weights than the forward
+        st.backward(w2, None, None, g)
+    assert e.value.code == hp.HP_ERR_STATE
+    with pytest.raises(hp.HPError) as e:            # loss stage without labels
+        st.forward(w, x, None, None, None)
+    assert e.value.code == hp.HP_ERR_ARG
+    st.close()
+    bad = to_layers(net)
+    bad[3]["C"] = 999                                # FC fan-in mismatch
+    with pytest.raises(hp.HPError) as e:
+        hp.Stage(bad, 2, 16, 16, 3)
+    assert e.value.code == hp.HP_ERR_ARG

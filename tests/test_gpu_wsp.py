@@ -1,0 +1,139 @@
+"""WSP update on the GPU vs the oracle: bit-exact.
+
+The stage is replaced by gradients that are inputs (seeded arrays) or by the
+toy gradient g = w - a of f(w) = 1/2 |w - a|^2 computed from the weights the
+library hands out, so every value entering the WSP kernels is identical on
+both sides.  The local update, wave accumulation, push and pull perform the
+same IEEE fp32 operations in the same order as the oracle, so the event log,
+every ring slot, u~ and w_g must match bit for bit.
+"""
+import numpy as np
+import pytest
+import torch
+
+import seeded_inputs as si
+from oracle import wsp as owsp
+from paper_2005_14038_amd import hetpipe
+from paper_2005_14038_amd.driver import Deadlock, WSPDriver
+
+from gpu_common import dev, to_dev  # noqa: F401
+
+pytestmark = pytest.mark.gpu
+
+CASES = [
+    # P, N, s_local, D, waves, periods, lr, toy
+    (11642, 2, 3, 0, 3, [1, 1], 0.01, False),          # Tiny-CNN-sized, 2 VWs, D = 0
+    (1001, 4, 3, 1, 5, [1, 1, 1, 2], 0.01, False),      # 4 VWs, D = 1, a straggler
+    (37, 3, 0, 2, 6, [2, 1, 3], 0.5, True),             # wave length 1, scalar tail
+    (4099, 2, 4, 0, 3, [1, 3], 0.1, True),              # toy gradient reads the ring
+    (2_325_568, 1, 3, 0, 3, [1], 0.01, False),          # VGG-19 stage-1 parameter count
+]
+
+
+def grads_table(P, N, Q, seed=99):
+    return {(n, q): si.normal(si.stream_key(seed, n, q, si.T_Y), P)
+            for n in range(N) for q in range(1, Q + 1)}
+
+
+@pytest.mark.parametrize("case", CASES, ids=[f"P{c[0]}_N{c[1]}_W{c[2]+1}_D{c[3]}" for c in CASES])
+def test_wsp_bit_exact(dev, case):  # noqa: F811
+    P, N, s_local, D, waves, periods, lr, toy = case
+    W = s_local + 1
+    Q = waves * W
+    w0 = si.normal(si.stream_key(7, 0, 0, si.T_W0), P, 0.1)
+    if toy:
+        table = grads_table(P, N, Q)           # targets a[n, q]
+        ofn = lambda n, q, w: w - table[(n, q)]
+    else:
+        table = grads_table(P, N, Q)
+        ofn = lambda n, q, w: table[(n, q)]
+    ref = owsp.WSP(w0, N, s_local, D, lr, ofn, periods=periods)
+    ref.run(waves)
+
+    dtab = {k: to_dev(v, dev) for k, v in table.items()}
+
+    def gfn(n, q, wptr, grad):
+        if toy:
+            wt = torch.empty(P, dtype=torch.float32, device=dev)
+            hetpipe.copy_device(wptr, wt)
+            grad[:P].copy_(wt - dtab[(n, q)])
+        else:
+            grad[:P].copy_(dtab[(n, q)])
+
+    drv = WSPDriver(None, to_dev(w0, dev), N, s_local, D, lr, None, periods=periods,
+                    grad_fn=gfn, P=P)
+    drv.run(waves)
+    torch.cuda.synchronize()
+    assert drv.events == ref.events
+    wg = hetpipe.read_vector(drv.ps.weights_ptr(), P)
+    assert np.array_equal(wg.view(np.uint32), ref.wg.view(np.uint32))
+    for n in range(N):
+        ring, stride, ut = drv.vws[n].buffers()
+        for s in range(W):
+            got = hetpipe.read_vector(ring + 4 * s * stride, P)
+            assert np.array_equal(got.view(np.uint32), ref.ring[n][s].view(np.uint32)), (n, s)
+        got = hetpipe.read_vector(ut, P)
+        assert np.array_equal(got.view(np.uint32), ref.ut[n].view(np.uint32)), n
+        st = drv.vws[n].state()
+        assert st["p"] == ref.p[n] and st["c"] == ref.c[n] and st["g"] == ref.g[n]
+    assert drv.ps.clock() == ref.cg
+    drv.close()
+
+
+def test_wsp_protocol_errors(dev):  # noqa: F811
+    P = 64
+    w0 = to_dev(np.zeros(P, np.float32), dev)
+    g = torch.ones(P, dtype=torch.float32, device=dev)
+    ps = hetpipe.ParameterServer(P, w0, 2, 0)
+    v0 = hetpipe.VirtualWorker(ps, 0, 1)
+    v1 = hetpipe.VirtualWorker(ps, 1, 1)
+    with pytest.raises(hetpipe.HPError) as e:          # duplicate id
+        hetpipe.VirtualWorker(ps, 1, 1)
+    assert e.value.code == hetpipe.HP_ERR_STATE
+    with pytest.raises(hetpipe.HPError) as e:          # update without a started minibatch
+        v0.local_update(g, 0.1)
+    assert e.value.code == hetpipe.HP_ERR_STATE
+    with pytest.raises(hetpipe.HPError) as e:          # push mid-wave
+        v0.push_wave()
+    assert e.value.code == hetpipe.HP_ERR_STATE
+    for _ in range(2):                                 # complete wave 0 of VW 0
+        v0.weights()
+        v0.local_update(g, 0.1)
+    with pytest.raises(hetpipe.HPError) as e:          # next minibatch before the push
+        v0.weights()
+    assert e.value.code == hetpipe.HP_ERR_STATE
+    v0.push_wave()
+    with pytest.raises(hetpipe.HPError) as e:          # double push
+        v0.push_wave()
+    assert e.value.code == hetpipe.HP_ERR_STATE
+    assert v0.pull() is False                          # D = 0: waits for VW 1's wave 0
+    with pytest.raises(hetpipe.HPError) as e:          # weights requested while gated
+        v0.weights()
+    assert e.value.code == hetpipe.HP_ERR_STATE
+    for _ in range(2):
+        v1.weights()
+        v1.local_update(g, 0.1)
+    v1.push_wave()
+    assert ps.clock() == 1
+    assert v1.pull() is True and v0.pull() is True
+    v0.weights()
+    v1.close(); v0.close(); ps.close()
+
+
+def test_stopped_worker_is_detected_as_deadlock(dev):  # noqa: F811
+    P, N = 128, 3
+    w0 = to_dev(np.zeros(P, np.float32), dev)
+    gtab = {}
+
+    def gfn(n, q, wptr, grad):
+        grad.fill_(0.5)
+
+    drv = WSPDriver(None, w0, N, 3, 0, 0.1, None, grad_fn=gfn, P=P)
+    # VW 2 completes one wave and then stops; the others must end up blocked
+    drv.run(1)
+    drv.done[2] = 10 ** 9          # VW 2 never runs again
+    with pytest.raises(Deadlock):
+        drv.run(4)
+    assert drv.blocked[0] and drv.blocked[1]
+    drv.close()
+    del gtab
