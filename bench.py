@@ -1,0 +1,214 @@
+#!/usr/bin/env python3
+"""Stage-step throughput of the HetPipe hot path on one MI355X.
+
+One step = one minibatch of one virtual worker through the whole hot path:
+weight-version select (hp_wsp_weights), stage forward, stage backward, local
+update + wave accumulation, and at every wave end the push and the gated pull
+against the parameter server in device memory.  Inputs (a pool of seeded
+minibatches) are resident in HBM before the timed region starts.
+
+Default workload: VGG-19 stage 1 (conv1_1 .. conv3_4 with two max-pools),
+batch 32 of 224x224x3 fp32 images, upstream gradient N(0, 1e-3^2), one
+virtual worker with s_local = 3.
+
+Prints one JSON line (metric, value = images/s, roofline of the dominant
+kernel class -- the implicit-GEMM contractions -- and the CPU oracle baseline).
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_TFLOPS = {"fp32": 157.3, "bf16": 2516.6}     # MI355X dense MFMA peaks
+HBM_PEAK_GBS = 8000.0
+METRIC = "stage-step images/sec (fwd+bwd+WSP update); % of MFMA peak, HBM GB/s"
+
+
+def contraction_flops(layers, batch, H, W, C):
+    """Algorithmic FLOPs (2 per multiply-add) of one stage step's conv / FC
+    contractions: forward, weight gradient, and data gradient except for a
+    layer that reads the stage input (the image needs no gradient)."""
+    from paper_2005_14038_amd.hetpipe import HP_CONV, HP_FC
+    shape = {-1: (H, W, C)}
+    total = 0
+    for i, d in enumerate(layers):
+        h, w, c = shape[d.get("in0", i - 1)]
+        k = d["kind"]
+        if k == HP_CONV:
+            P = (h + 2 * d["pad"] - d["R"]) // d["stride"] + 1
+            Q = (w + 2 * d["pad"] - d["S"]) // d["stride"] + 1
+            macs = batch * P * Q * d["K"] * d["R"] * d["S"] * c
+            total += 2 * macs * (2 if d.get("in0", i - 1) < 0 else 3)
+            shape[i] = (P, Q, d["K"])
+        elif k == HP_FC:
+            macs = batch * d["K"] * d["C"]
+            total += 2 * macs * (2 if d.get("in0", i - 1) < 0 else 3)
+            shape[i] = (1, 1, d["K"])
+        elif k == 4:   # max-pool
+            P = (h + 2 * d["pad"] - d["R"]) // d["stride"] + 1
+            Q = (w + 2 * d["pad"] - d["S"]) // d["stride"] + 1
+            shape[i] = (P, Q, c)
+        elif k == 7:   # global average pool
+            shape[i] = (1, 1, c)
+        else:
+            shape[i] = (h, w, c)
+    return total
+
+
+def kernel_source_hash():
+    p = os.path.join(ROOT, "paper_2005_14038_amd", "csrc", "igemm.hip")
+    return hashlib.sha256(open(p, "rb").read()).hexdigest()[:16]
+
+
+def measured_traffic(workload):
+    """HBM bytes per step of the contraction kernels from the committed
+    rocprofv3 counter summary, if it was taken on the current kernel source."""
+    p = os.path.join(ROOT, "profiles", f"igemm_{workload}_traffic.json")
+    if not os.path.exists(p):
+        return None
+    d = json.load(open(p))
+    if d.get("igemm_sha256_16") != kernel_source_hash():
+        return None
+    return d.get("bytes_per_step")
+
+
+def cpu_baseline(wl, layers, out_shape, images):
+    """The oracle (plain C loops, fp64 accumulation, OpenMP) on the first
+    `images` images of minibatch 1: forward + backward of the stage and the
+    local update."""
+    import numpy as np
+    from oracle import nets as onets
+    from oracle import stage as ostage
+    from oracle import wsp as owsp
+    from paper_2005_14038_amd import workloads
+    onet = onets.by_name(wl.net, **wl.net_kw)
+    w0 = workloads.initial_weights(wl, layers)
+    x, lab, dy = workloads.inputs(wl, out_shape, 0, 1)
+    x1 = x[:images]
+    lab1 = lab[:images] if lab is not None else None
+    dy1 = dy[:images] if dy is not None else None
+    t0 = time.perf_counter()
+    r = ostage.step(onet, w0.astype(np.float64), x1, labels=lab1, dy=dy1, bf16=(wl.dtype == "bf16"))
+    sim = owsp.WSP(w0, 1, wl.s_local, 0, wl.lr, lambda n, q, w: r["grad"].astype(np.float32))
+    sim._minibatch(0, 1)
+    dt = time.perf_counter() - t0
+    cores = int(os.environ.get("OMP_NUM_THREADS", "0")) or len(os.sched_getaffinity(0))
+    return {"value": round(images / dt, 4), "unit": "images/s", "cores": cores, "kind": "oracle",
+            "sample": f"{images} image(s) of minibatch 1 ({wl.name}): oracle stage forward + "
+                      f"backward + local update, {dt:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=4)
+    ap.add_argument("--workload", default="vgg19_s1")
+    ap.add_argument("--pool", type=int, default=2, help="distinct minibatches resident in HBM")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-images", type=int, default=4,
+                    help="images of the oracle's bounded CPU sample")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU: the multi-VW data-parallel layer is simulated on a "
+              "single MI355X (virtual workers take turns on it); --gpus must be 1.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2005_14038_amd import workloads
+    from paper_2005_14038_amd.driver import WSPDriver
+    from paper_2005_14038_amd.hetpipe import Stage
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    wl = workloads.WORKLOADS[args.workload]
+    b = wl.builder()
+    layers = b.layers
+    st = Stage(layers, wl.batch, wl.H, wl.W, wl.C, dtype=wl.dtype)
+    out_shape = st.output_shape(-1)
+    w0 = torch.from_numpy(workloads.initial_weights(wl, layers)).to(dev)
+
+    pool = {}
+    for n in range(wl.N):
+        for j in range(args.pool):
+            x, lab, dy = workloads.inputs(wl, out_shape, n, j + 1)
+            pool[(n, j)] = tuple(torch.from_numpy(a).to(dev) if a is not None else None
+                                 for a in (x, lab, dy))
+
+    def data(n, q):
+        return pool[(n, (q - 1) % args.pool)]
+
+    drv = WSPDriver(st, w0, wl.N, wl.s_local, wl.D, wl.lr, data, periods=wl.periods)
+    order = []
+
+    def next_vw():
+        cand = [n for n in range(wl.N) if not drv.blocked[n]]
+        return min(cand, key=lambda m: (drv.t[m], m))
+
+    for _ in range(args.warmup):
+        drv.minibatch(next_vw())
+    torch.cuda.synchronize()
+    st.read_timing()                      # discard
+    st.set_timing(True)
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    start.record()
+    for _ in range(args.steps):
+        n = next_vw()
+        order.append(n)
+        drv.minibatch(n)
+    stop.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ev_ms = start.elapsed_time(stop)
+    ms, launches = st.read_timing()
+    st.set_timing(False)
+
+    ms_step = max(wall, ev_ms / 1e3) * 1e3 / args.steps
+    value = wl.batch * args.steps / (max(wall, ev_ms / 1e3))
+    flops_step = contraction_flops(layers, wl.batch, wl.H, wl.W, wl.C)
+    gemm_ms_step = ms["contraction"] / args.steps
+    achieved = flops_step / (gemm_ms_step * 1e-3) / 1e12
+    peak = PEAK_TFLOPS[wl.dtype]
+    traffic = measured_traffic(args.workload)
+    out = {
+        "metric": METRIC,
+        "value": round(value, 3),
+        "unit": "images/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32" if wl.dtype == "fp32" else "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"{wl.name}: batch {wl.batch} x {wl.H}x{wl.W}x{wl.C}, "
+                               f"{wl.N} virtual worker(s), s_local {wl.s_local}, D {wl.D}",
+                   "global_batch": wl.batch, "parallelism": "single GPU, simulated VWs"},
+        "roofline": {"bound": "mfma", "achieved": round(achieved, 3), "peak": peak,
+                     "unit": "TFLOP/s", "frac": round(achieved / peak, 4), "traffic": traffic,
+                     "kernel": "implicit-GEMM conv/FC contractions (all launches of a step)",
+                     "flop_per_step": flops_step, "ms_per_step": round(gemm_ms_step, 4),
+                     "launches_per_step": launches["contraction"] / args.steps},
+        "other_kernels_ms_per_step": round(ms["other"] / args.steps, 4),
+    }
+    drv.close()
+    st.close()
+    torch.cuda.synchronize()
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(wl, layers, out_shape, args.cpu_images)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

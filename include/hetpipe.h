@@ -102,6 +102,15 @@ int hp_stage_output_shape(const hp_stage *st, int layer, int dims[3]);
 /* Bytes of device memory the stage holds. */
 int hp_stage_device_bytes(const hp_stage *st, size_t *bytes);
 
+/* Device timing of the stage's own kernels, for profiling.  While enabled,
+ * every kernel the stage enqueues is bracketed by HIP events on the stage's
+ * stream.  hp_stage_read_timing synchronises the stream, returns the summed
+ * device time in milliseconds and the launch counts of two classes --
+ * [0] contractions (implicit-GEMM conv / FC kernels and their split-K
+ * reductions), [1] every other stage kernel -- and resets the sums. */
+int hp_stage_set_timing(hp_stage *st, int enable);
+int hp_stage_read_timing(hp_stage *st, double ms[2], int64_t launches[2]);
+
 /* Forward pass of one minibatch (HetPipe Sec. 3: the layers of the stage in
  * order) at weights `w` (flat fp32, length P).  `x` is the stage input
  * [batch][H][W][C].  If the stage ends in HP_SOFTMAX_CE, `labels` (int32

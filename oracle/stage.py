@@ -13,7 +13,8 @@ backward pass).
 Precision: everything is float64.  In bf16 mode every operand of a contraction
 (conv / FC weights, their input activations, and the upstream gradients fed to
 dgrad and wgrad) is rounded to bfloat16 first (``bf16.round_bf16``); BN, ReLU,
-pooling, the residual add and the loss stay in full precision.
+pooling, the residual add, the loss and the bias gradient (a plain sum of the
+upstream gradient) stay in full precision.
 """
 from __future__ import annotations
 
@@ -126,21 +127,22 @@ def backward(net, params_flat, x, vals, saved, dy=None, need_dx=False, bf16=Fals
         wants_dx = nd["in"] >= 0 or need_dx
         if k == "conv":
             w = prm[(i, "w")]
-            dw, db = ops.conv_wgrad(rnd(a), rnd(g), nd["R"], nd["S"], nd["stride"],
-                                    nd["pad"], nd["bias"])
+            dw, _ = ops.conv_wgrad(rnd(a), rnd(g), nd["R"], nd["S"], nd["stride"],
+                                   nd["pad"], False)
             grads[(i, "w")] = dw
             if nd["bias"]:
-                grads[(i, "b")] = db
+                # the bias gradient is a plain sum of dy, not a contraction: no rounding
+                grads[(i, "b")] = g.reshape(-1, nd["K"]).sum(axis=0)
             if wants_dx:
                 send(nd["in"], ops.conv_dgrad(rnd(g), rnd(w), nd["stride"], nd["pad"],
                                               a.shape[1], a.shape[2]))
         elif k == "fc":
             w = prm[(i, "w")]
             a2 = a.reshape(a.shape[0], -1)
-            dw, db = ops.fc_wgrad(rnd(a2), rnd(g), nd["bias"])
+            dw, _ = ops.fc_wgrad(rnd(a2), rnd(g), False)
             grads[(i, "w")] = dw
             if nd["bias"]:
-                grads[(i, "b")] = db
+                grads[(i, "b")] = g.sum(axis=0)
             if wants_dx:
                 send(nd["in"], ops.fc_dgrad(rnd(g), rnd(w)).reshape(a.shape))
         elif k == "relu":

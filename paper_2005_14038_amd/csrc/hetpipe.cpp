@@ -71,7 +71,41 @@ size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
 }  // namespace
 
+struct StageTimer {
+    bool on = false;
+    struct Rec { hipEvent_t a, b; int cat; };
+    std::vector<Rec> recs;          // recorded, not yet read
+    std::vector<hipEvent_t> pool;   // free events
+    hipEvent_t take() {
+        if (!pool.empty()) { hipEvent_t e = pool.back(); pool.pop_back(); return e; }
+        hipEvent_t e = nullptr;
+        if (hipEventCreate(&e) != hipSuccess) return nullptr;
+        return e;
+    }
+    int cur = -1;
+    hipEvent_t cur_a = nullptr;
+    void begin(int cat, hipStream_t s) {
+        if (!on) return;
+        cur_a = take();
+        cur = cat;
+        if (cur_a) (void)hipEventRecord(cur_a, s);
+    }
+    void end(hipStream_t s) {
+        if (!on || !cur_a) return;
+        hipEvent_t b = take();
+        if (!b) return;
+        (void)hipEventRecord(b, s);
+        recs.push_back({cur_a, b, cur});
+        cur_a = nullptr;
+    }
+    ~StageTimer() {
+        for (auto& r : recs) { (void)hipEventDestroy(r.a); (void)hipEventDestroy(r.b); }
+        for (auto e : pool) (void)hipEventDestroy(e);
+    }
+};
+
 struct hp_stage {
+    StageTimer timer;
     std::vector<Node> nodes;
     int batch = 0, H = 0, W = 0, C = 0;
     int dtype = HP_FP32;
@@ -355,6 +389,29 @@ extern "C" int hp_stage_device_bytes(const hp_stage* st, size_t* bytes) {
     return HP_OK;
 }
 
+extern "C" int hp_stage_set_timing(hp_stage* st, int enable) {
+    if (!st) return fail(HP_ERR_ARG, "hp_stage_set_timing: NULL stage");
+    st->timer.on = enable != 0;
+    return HP_OK;
+}
+
+extern "C" int hp_stage_read_timing(hp_stage* st, double ms[2], int64_t launches[2]) {
+    if (!st || !ms || !launches) return fail(HP_ERR_ARG, "hp_stage_read_timing: NULL argument");
+    HP_HIP(hipStreamSynchronize(st->stream));
+    ms[0] = ms[1] = 0.0;
+    launches[0] = launches[1] = 0;
+    for (auto& r : st->timer.recs) {
+        float t = 0.f;
+        HP_HIP(hipEventElapsedTime(&t, r.a, r.b));
+        ms[r.cat] += t;
+        launches[r.cat] += 1;
+        st->timer.pool.push_back(r.a);
+        st->timer.pool.push_back(r.b);
+    }
+    st->timer.recs.clear();
+    return HP_OK;
+}
+
 extern "C" int hp_stage_forward(hp_stage* st, const float* w, const float* x, float* y,
                                 const int32_t* labels, float* loss) {
     if (!st || !x || (!w && st->P)) return fail(HP_ERR_ARG, "hp_stage_forward: NULL argument");
@@ -370,6 +427,8 @@ extern "C" int hp_stage_forward(hp_stage* st, const float* w, const float* x, fl
         const hp_layer& L = nd.L;
         const float* in = L.in0 < 0 ? x : st->nodes[L.in0].y;
         hipError_t e = hipSuccess;
+        StageTimer& tm = st->timer;
+        tm.begin(L.kind == HP_CONV || L.kind == HP_FC ? 0 : 1, s);
         switch (L.kind) {
             case HP_CONV:
             case HP_FC: {
@@ -407,6 +466,7 @@ extern "C" int hp_stage_forward(hp_stage* st, const float* w, const float* x, fl
                 break;
             }
         }
+        tm.end(s);
         int rc = launch_ok(e, "forward", (int)i);
         if (rc) return rc;
     }
@@ -467,15 +527,26 @@ extern "C" int hp_stage_backward(hp_stage* st, const float* w, const float* dy, 
         hipError_t e = hipSuccess;
         float* d;
         int acc;
+        const bool gemm_node = L.kind == HP_CONV || L.kind == HP_FC;
+        if (!gemm_node) st->timer.begin(1, s);
         switch (L.kind) {
             case HP_CONV:
             case HP_FC: {
+                StageTimer& tm = st->timer;
+                tm.begin(0, s);
                 e = launch_gemm(nd.wgrad, nd.geo, in, gin, grad + nd.w_off, nullptr, 0, st->ws, s);
-                if (e == hipSuccess && L.bias)
+                tm.end(s);
+                if (e == hipSuccess && L.bias) {
+                    tm.begin(1, s);
                     e = launch_colsum(gin, (long)B * nd.H * nd.W, nd.C, grad + nd.b_off, st->ws, s);
-                if (e == hipSuccess && dest(L.in0, &d, &acc))
+                    tm.end(s);
+                }
+                if (e == hipSuccess && dest(L.in0, &d, &acc)) {
+                    tm.begin(0, s);
                     e = launch_gemm(nd.dgrad, nd.geo, gin, w + nd.w_off, d, nullptr,
                                     acc ? EPI_ACCUM : 0, st->ws, s);
+                    tm.end(s);
+                }
                 break;
             }
             case HP_RELU: {
@@ -514,6 +585,7 @@ extern "C" int hp_stage_backward(hp_stage* st, const float* w, const float* dy, 
                     e = launch_gap_bwd(gin, d, B, nd.inH * nd.inW, nd.C, acc, s);
                 break;
         }
+        if (!gemm_node) st->timer.end(s);
         int rc = launch_ok(e, "backward", i);
         if (rc) return rc;
     }

@@ -3,11 +3,14 @@
 // All three stream flat fp32 parameter vectors once, so they are HBM-bound:
 // float4 accesses, a grid of a few workgroups per CU striding over the vector,
 // and a scalar tail for lengths that are not multiples of 4.  The arithmetic
-// is fixed to one IEEE fp32 operation at a time (explicit round-to-nearest
-// intrinsics, no fused multiply-add), so the result is bit-identical to any
+// is fixed to one IEEE fp32 operation at a time (contraction into fused
+// multiply-add is switched off for this file), so the result is bit-identical to any
 // other implementation that performs the same operations in the same order:
 //   u = (-lr) * g;   new = newest + u;   u~ = u  or  u~ + u;   w_g = w_g + u~.
 #include "kernels.h"
+
+// One rounding per operation: never fuse a multiply and an add into an FMA here.
+#pragma clang fp contract(off)
 
 namespace hp {
 namespace {
@@ -20,8 +23,8 @@ inline int wsp_blocks(size_t n4) {
     return (int)(b ? b : 1);
 }
 
-__device__ __forceinline__ float mul_rn(float a, float b) { return __fmul_rn(a, b); }
-__device__ __forceinline__ float add_rn(float a, float b) { return __fadd_rn(a, b); }
+__device__ __forceinline__ float mul_rn(float a, float b) { return a * b; }
+__device__ __forceinline__ float add_rn(float a, float b) { return a + b; }
 
 template <bool FIRST>
 __global__ void local_update_kernel(const float* __restrict__ g, const float* newest,

@@ -23,7 +23,8 @@ HP_FP32, HP_BF16 = 0, 1
 
 EXPORTS = [
     "hp_stage_create", "hp_stage_destroy", "hp_stage_param_count", "hp_stage_param_layout",
-    "hp_stage_output_shape", "hp_stage_device_bytes", "hp_stage_forward", "hp_stage_backward",
+    "hp_stage_output_shape", "hp_stage_device_bytes", "hp_stage_set_timing",
+    "hp_stage_read_timing", "hp_stage_forward", "hp_stage_backward",
     "hp_ps_create", "hp_ps_destroy", "hp_ps_weights", "hp_ps_clock",
     "hp_vw_create", "hp_vw_destroy", "hp_wsp_weights", "hp_wsp_local_update",
     "hp_wsp_push_wave", "hp_wsp_pull", "hp_wsp_state", "hp_wsp_version", "hp_wsp_buffers",
@@ -71,6 +72,9 @@ def lib():
     L.hp_stage_param_layout.argtypes = [_vp, i32, ctypes.POINTER(sz), ctypes.POINTER(sz)]
     L.hp_stage_output_shape.argtypes = [_vp, i32, ctypes.POINTER(ctypes.c_int * 3)]
     L.hp_stage_device_bytes.argtypes = [_vp, ctypes.POINTER(sz)]
+    L.hp_stage_set_timing.argtypes = [_vp, i32]
+    L.hp_stage_read_timing.argtypes = [_vp, ctypes.POINTER(ctypes.c_double * 2),
+                                       ctypes.POINTER(ctypes.c_int64 * 2)]
     L.hp_stage_forward.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp]
     L.hp_stage_backward.argtypes = [_vp, _vp, _vp, _vp, _vp]
     L.hp_ps_create.argtypes = [sz, _vp, i32, i32, _vp, _pp]
@@ -174,6 +178,17 @@ class Stage:
         n = ctypes.c_size_t()
         _check(self._L.hp_stage_device_bytes(self.h, ctypes.byref(n)))
         return n.value
+
+    def set_timing(self, on=True):
+        _check(self._L.hp_stage_set_timing(self.h, 1 if on else 0))
+
+    def read_timing(self):
+        """({'contraction': ms, 'other': ms}, {'contraction': n, 'other': n}); resets."""
+        ms = (ctypes.c_double * 2)()
+        n = (ctypes.c_int64 * 2)()
+        _check(self._L.hp_stage_read_timing(self.h, ctypes.byref(ms), ctypes.byref(n)))
+        return ({"contraction": ms[0], "other": ms[1]},
+                {"contraction": int(n[0]), "other": int(n[1])})
 
     def forward(self, w, x, y=None, labels=None, loss=None):
         _check(self._L.hp_stage_forward(self.h, _ptr(w), _ptr(x), _ptr(y), _ptr(labels),
