@@ -84,7 +84,8 @@ __global__ void maxpool_fwd_kernel(const float* __restrict__ x, float* __restric
 // whose first maximum it is (the window's argmax is recomputed from x).
 __global__ void maxpool_bwd_kernel(const float* __restrict__ x, const float* __restrict__ dy,
                                    float* __restrict__ dx, int N, int H, int W, int C, int R,
-                                   int S, int st, int pad, int P, int Q, int acc) {
+                                   int S, int st, int pad, int P, int Q, int acc,
+                                   const float* __restrict__ mask) {
     const size_t total = (size_t)N * H * W * C;
     for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
          i += (size_t)gridDim.x * blockDim.x) {
@@ -120,7 +121,41 @@ __global__ void maxpool_bwd_kernel(const float* __restrict__ x, const float* __r
                 if (best == r * S + s) sum += dy[(((size_t)n * P + p) * Q + q) * C + c];
             }
         }
+        if (mask && !(mask[i] > 0.f)) sum = 0.f;
         dx[i] = acc ? dx[i] + sum : sum;
+    }
+}
+
+// max-pool backward for non-overlapping windows (window = stride, no padding,
+// windows tile the input exactly): one thread per output element writes its
+// whole window -- dy at the first maximum, zero elsewhere.
+__global__ void maxpool_bwd_tiled_kernel(const float* __restrict__ x, const float* __restrict__ dy,
+                                         float* __restrict__ dx, int N, int H, int W, int C, int R,
+                                         int P, int Q, int acc, const float* __restrict__ mask) {
+    const size_t total = (size_t)N * P * Q * C;
+    for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
+         i += (size_t)gridDim.x * blockDim.x) {
+        int c = (int)(i % C);
+        size_t t = i / C;
+        int q = (int)(t % Q); t /= Q;
+        int p = (int)(t % P);
+        int n = (int)(t / P);
+        const size_t base = (((size_t)n * H + p * R) * W + q * R) * C + c;
+        int best = 0;
+        float m = x[base];
+        for (int r = 0; r < R; ++r)
+            for (int s = 0; s < R; ++s) {
+                float v = x[base + ((size_t)r * W + s) * C];
+                if (v > m) { m = v; best = r * R + s; }
+            }
+        const float g = dy[i];
+        for (int r = 0; r < R; ++r)
+            for (int s = 0; s < R; ++s) {
+                size_t j = base + ((size_t)r * W + s) * C;
+                float v = (r * R + s == best) ? g : 0.f;
+                if (mask && !(mask[j] > 0.f)) v = 0.f;
+                dx[j] = acc ? dx[j] + v : v;
+            }
     }
 }
 
@@ -208,32 +243,30 @@ __global__ void colsum_partial_kernel(const float* __restrict__ v, const float* 
     }
 }
 
-__global__ void colsum_final_kernel(const float* __restrict__ part, int nb, int C,
-                                    float* __restrict__ out) {
-    int c = blockIdx.x * blockDim.x + threadIdx.x;
-    if (c >= C) return;
-    float s = 0.f;
-    for (int b = 0; b < nb; ++b) s += part[(size_t)b * C + c];
-    out[c] = s;
-}
+// Final reduction of the row-block partials: workgroup = 64 channels x 16
+// lanes; lane l sums partial rows l, l+16, ...; the 16 lane sums are combined
+// in LDS in a fixed order.  mode 0: out = sum; 1: out = sum / M (mean);
+// 2: out = 1 / sqrt(sum / M + eps) (inverse standard deviation).
+constexpr int CF_LANES = 16;
 
-// mean[c] = sum / M
-__global__ void bn_mean_kernel(const float* __restrict__ part, int nb, int C, long M,
-                               float* __restrict__ mean) {
-    int c = blockIdx.x * blockDim.x + threadIdx.x;
-    if (c >= C) return;
+__global__ void colsum_final_kernel(const float* __restrict__ part, int nb, int C, long M,
+                                    float eps, int mode, float* __restrict__ out) {
+    __shared__ float red[CF_LANES][CS_CH];
+    const int cl = threadIdx.x % CS_CH;
+    const int rl = threadIdx.x / CS_CH;
+    const int c = blockIdx.x * CS_CH + cl;
     float s = 0.f;
-    for (int b = 0; b < nb; ++b) s += part[(size_t)b * C + c];
-    mean[c] = s / (float)M;
-}
-
-__global__ void bn_invstd_kernel(const float* __restrict__ part, int nb, int C, long M, float eps,
-                                 float* __restrict__ invstd) {
-    int c = blockIdx.x * blockDim.x + threadIdx.x;
-    if (c >= C) return;
-    float s = 0.f;
-    for (int b = 0; b < nb; ++b) s += part[(size_t)b * C + c];
-    invstd[c] = 1.f / sqrtf(s / (float)M + eps);
+    if (c < C)
+        for (int b = rl; b < nb; b += CF_LANES) s += part[(size_t)b * C + c];
+    red[rl][cl] = s;
+    __syncthreads();
+    if (rl == 0 && c < C) {
+        float t = 0.f;
+        for (int l = 0; l < CF_LANES; ++l) t += red[l][cl];
+        if (mode == 1) t = t / (float)M;
+        else if (mode == 2) t = 1.f / sqrtf(t / (float)M + eps);
+        out[c] = t;
+    }
 }
 
 __global__ void bn_apply_kernel(const float* __restrict__ x, long M, int C,
@@ -354,10 +387,16 @@ hipError_t launch_maxpool_fwd(const float* x, float* y, int N, int H, int W, int
 
 hipError_t launch_maxpool_bwd(const float* x, const float* dy, float* dx, int N, int H, int W,
                               int C, int R, int S, int st, int pad, int P, int Q, int accumulate,
-                              hipStream_t s) {
+                              const float* mask, hipStream_t s) {
+    if (R == S && R == st && pad == 0 && P * st == H && Q * st == W) {
+        size_t n = (size_t)N * P * Q * C;
+        hipLaunchKernelGGL(maxpool_bwd_tiled_kernel, dim3(ew_blocks(n)), dim3(EW_THREADS), 0, s, x,
+                           dy, dx, N, H, W, C, R, P, Q, accumulate, mask);
+        return hipGetLastError();
+    }
     size_t n = (size_t)N * H * W * C;
     hipLaunchKernelGGL(maxpool_bwd_kernel, dim3(ew_blocks(n)), dim3(EW_THREADS), 0, s, x, dy, dx,
-                       N, H, W, C, R, S, st, pad, P, Q, accumulate);
+                       N, H, W, C, R, S, st, pad, P, Q, accumulate, mask);
     return hipGetLastError();
 }
 
@@ -382,7 +421,8 @@ hipError_t launch_colsum(const float* v, long M, int C, float* out, float* ws, h
     dim3 grid((C + CS_CH - 1) / CS_CH, nb);
     hipLaunchKernelGGL(colsum_partial_kernel<0>, grid, dim3(256), 0, s, v, nullptr, nullptr,
                        nullptr, nullptr, M, C, ws, nullptr);
-    hipLaunchKernelGGL(colsum_final_kernel, dim3((C + 255) / 256), dim3(256), 0, s, ws, nb, C, out);
+    hipLaunchKernelGGL(colsum_final_kernel, dim3((C + CS_CH - 1) / CS_CH), dim3(CS_CH * CF_LANES), 0,
+                       s, ws, nb, C, M, 0.f, 0, out);
     return hipGetLastError();
 }
 
@@ -395,11 +435,12 @@ hipError_t launch_bn_fwd(const float* x, long M, int C, const float* gamma, cons
     dim3 grid((C + CS_CH - 1) / CS_CH, nb);
     hipLaunchKernelGGL(colsum_partial_kernel<0>, grid, dim3(256), 0, s, x, nullptr, nullptr,
                        nullptr, nullptr, M, C, ws, nullptr);
-    hipLaunchKernelGGL(bn_mean_kernel, dim3((C + 255) / 256), dim3(256), 0, s, ws, nb, C, M, mean);
+    hipLaunchKernelGGL(colsum_final_kernel, dim3((C + CS_CH - 1) / CS_CH), dim3(CS_CH * CF_LANES), 0,
+                       s, ws, nb, C, M, 0.f, 1, mean);
     hipLaunchKernelGGL(colsum_partial_kernel<1>, grid, dim3(256), 0, s, x, nullptr, nullptr, mean,
                        nullptr, M, C, ws, nullptr);
-    hipLaunchKernelGGL(bn_invstd_kernel, dim3((C + 255) / 256), dim3(256), 0, s, ws, nb, C, M, eps,
-                       invstd);
+    hipLaunchKernelGGL(colsum_final_kernel, dim3((C + CS_CH - 1) / CS_CH), dim3(CS_CH * CF_LANES), 0,
+                       s, ws, nb, C, M, eps, 2, invstd);
     size_t n = (size_t)M * C;
     hipLaunchKernelGGL(bn_apply_kernel, dim3(ew_blocks(n)), dim3(EW_THREADS), 0, s, x, M, C, gamma,
                        beta, mean, invstd, y, relu);
@@ -415,10 +456,10 @@ hipError_t launch_bn_bwd(const float* x, const float* dy, const float* relu_y, l
     dim3 grid((C + CS_CH - 1) / CS_CH, nb);
     hipLaunchKernelGGL(colsum_partial_kernel<2>, grid, dim3(256), 0, s, dy, x, relu_y, mean,
                        invstd, M, C, p0, p1);
-    hipLaunchKernelGGL(colsum_final_kernel, dim3((C + 255) / 256), dim3(256), 0, s, p0, nb, C,
-                       dbeta);
-    hipLaunchKernelGGL(colsum_final_kernel, dim3((C + 255) / 256), dim3(256), 0, s, p1, nb, C,
-                       dgamma);
+    hipLaunchKernelGGL(colsum_final_kernel, dim3((C + CS_CH - 1) / CS_CH), dim3(CS_CH * CF_LANES), 0,
+                       s, p0, nb, C, M, 0.f, 0, dbeta);
+    hipLaunchKernelGGL(colsum_final_kernel, dim3((C + CS_CH - 1) / CS_CH), dim3(CS_CH * CF_LANES), 0,
+                       s, p1, nb, C, M, 0.f, 0, dgamma);
     if (!dx) return hipGetLastError();      // parameter gradients only
     size_t n = (size_t)M * C;
     hipLaunchKernelGGL(bn_bwd_apply_kernel, dim3(ew_blocks(n)), dim3(EW_THREADS), 0, s, x, dy,

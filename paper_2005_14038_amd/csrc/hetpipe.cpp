@@ -20,7 +20,7 @@
 #include <string>
 #include <vector>
 
-#include "../../include/hetpipe.h"
+#include "hetpipe.h"
 #include "kernels.h"
 
 using namespace hp;
@@ -59,6 +59,9 @@ struct Node {
     float* g = nullptr;                 // gradient of the output
     bool g_written = false;
     const float* g_alias = nullptr;     // gradient handed over without a copy (ReLU -> BN)
+    int mask_into = -1;                 // data gradient goes to this producer, ReLU-masked
+    bool bias_in_wgrad = false;         // bias gradient computed by the weight-gradient GEMM
+    bool bwd_by_consumer = false;       // (ReLU) its backward is fused into its consumer
     size_t p_off = 0, p_cnt = 0;        // all parameters of the node
     size_t w_off = 0, b_off = 0;        // conv/fc weight, bias; bn gamma, beta
     ConvGeo geo{};
@@ -223,12 +226,15 @@ int build_stage(hp_stage* st, const hp_layer* layers, int n_layers) {
                 nd.p_cnt = off - nd.p_off;
                 nd.fwd = plan_gemm(OP_FWD, nd.geo, st->dtype, cus);
                 nd.dgrad = plan_gemm(OP_DGRAD, nd.geo, st->dtype, cus);
-                nd.wgrad = plan_gemm(OP_WGRAD, nd.geo, st->dtype, cus);
-                st->ws_floats = std::max({st->ws_floats, nd.fwd.ws_floats, nd.dgrad.ws_floats,
-                                          nd.wgrad.ws_floats});
-                if (L.bias)
+                // fp32: the bias gradient rides along as a column of ones in the weight
+                // gradient; bf16 would round dy there, so it is a separate fp32 sum
+                nd.bias_in_wgrad = L.bias && st->dtype == HP_FP32;
+                nd.wgrad = plan_gemm(OP_WGRAD, nd.geo, st->dtype, cus, nd.bias_in_wgrad ? 1 : 0);
+                if (L.bias && !nd.bias_in_wgrad)
                     st->ws_floats = std::max(st->ws_floats,
                                              colsum_ws_floats((long)B * P * Q, L.K));
+                st->ws_floats = std::max({st->ws_floats, nd.fwd.ws_floats, nd.dgrad.ws_floats,
+                                          nd.wgrad.ws_floats});
                 break;
             }
             case HP_RELU:
@@ -295,6 +301,18 @@ int build_stage(hp_stage* st, const hp_layer* layers, int n_layers) {
             pr.fuses_relu = true;
             nd.relu_fused = true;
         }
+    }
+    // ReLU backward fused into the consumer's data-gradient write: a conv, FC or
+    // max-pool reading a fused ReLU (producer conv / FC / add) that it alone reads
+    for (int i = 0; i < n_layers; ++i) {
+        Node& nd = st->nodes[i];
+        int k = nd.L.kind;
+        if ((k != HP_CONV && k != HP_FC && k != HP_MAXPOOL) || nd.L.in0 < 0) continue;
+        Node& r = st->nodes[nd.L.in0];
+        if (!r.relu_fused || r.consumers != 1) continue;
+        if (st->nodes[r.L.in0].L.kind == HP_BN) continue;
+        nd.mask_into = r.L.in0;
+        r.bwd_by_consumer = true;
     }
     // device buffers
     for (int i = 0; i < n_layers; ++i) {
@@ -432,9 +450,10 @@ extern "C" int hp_stage_forward(hp_stage* st, const float* w, const float* x, fl
         switch (L.kind) {
             case HP_CONV:
             case HP_FC: {
-                int epi = (L.bias ? EPI_BIAS : 0) | (nd.fuses_relu ? EPI_RELU : 0);
-                e = launch_gemm(nd.fwd, nd.geo, in, w + nd.w_off, nd.y,
-                                L.bias ? w + nd.b_off : nullptr, epi, st->ws, s);
+                Epilogue ep;
+                ep.flags = (L.bias ? EPI_BIAS : 0) | (nd.fuses_relu ? EPI_RELU : 0);
+                ep.bias = L.bias ? w + nd.b_off : nullptr;
+                e = launch_gemm(nd.fwd, nd.geo, in, w + nd.w_off, nd.y, ep, st->ws, s);
                 break;
             }
             case HP_RELU:
@@ -534,24 +553,34 @@ extern "C" int hp_stage_backward(hp_stage* st, const float* w, const float* dy, 
             case HP_FC: {
                 StageTimer& tm = st->timer;
                 tm.begin(0, s);
-                e = launch_gemm(nd.wgrad, nd.geo, in, gin, grad + nd.w_off, nullptr, 0, st->ws, s);
+                Epilogue wep;                     // bias gradient = appended column
+                wep.bias_out = nd.bias_in_wgrad ? grad + nd.b_off : nullptr;
+                e = launch_gemm(nd.wgrad, nd.geo, in, gin, grad + nd.w_off, wep, st->ws, s);
                 tm.end(s);
-                if (e == hipSuccess && L.bias) {
+                if (e == hipSuccess && L.bias && !nd.bias_in_wgrad) {
                     tm.begin(1, s);
                     e = launch_colsum(gin, (long)B * nd.H * nd.W, nd.C, grad + nd.b_off, st->ws, s);
                     tm.end(s);
                 }
-                if (e == hipSuccess && dest(L.in0, &d, &acc)) {
+                const int tgt = nd.mask_into >= 0 ? nd.mask_into : L.in0;
+                if (e == hipSuccess && dest(tgt, &d, &acc)) {
+                    Epilogue dep;
+                    dep.flags = acc ? EPI_ACCUM : 0;
+                    if (nd.mask_into >= 0) {
+                        dep.flags |= EPI_MASK;
+                        dep.mask = st->nodes[L.in0].y;
+                    }
                     tm.begin(0, s);
-                    e = launch_gemm(nd.dgrad, nd.geo, gin, w + nd.w_off, d, nullptr,
-                                    acc ? EPI_ACCUM : 0, st->ws, s);
+                    e = launch_gemm(nd.dgrad, nd.geo, gin, w + nd.w_off, d, dep, st->ws, s);
                     tm.end(s);
                 }
                 break;
             }
             case HP_RELU: {
                 const bool into_bn = nd.relu_fused && st->nodes[L.in0].L.kind == HP_BN;
-                if (into_bn) {
+                if (nd.bwd_by_consumer) {
+                    // already applied by the consumer's data-gradient write
+                } else if (into_bn) {
                     // the BN backward applies the ReLU mask itself: hand it this gradient
                     Node& pr = st->nodes[L.in0];
                     pr.g_alias = gin;
@@ -561,11 +590,14 @@ extern "C" int hp_stage_backward(hp_stage* st, const float* w, const float* dy, 
                 }
                 break;
             }
-            case HP_MAXPOOL:
-                if (dest(L.in0, &d, &acc))
+            case HP_MAXPOOL: {
+                const int tgt = nd.mask_into >= 0 ? nd.mask_into : L.in0;
+                const float* mask = nd.mask_into >= 0 ? st->nodes[L.in0].y : nullptr;
+                if (dest(tgt, &d, &acc))
                     e = launch_maxpool_bwd(in, gin, d, B, nd.inH, nd.inW, nd.inC, L.R, L.S,
-                                           L.stride, L.pad, nd.H, nd.W, acc, s);
+                                           L.stride, L.pad, nd.H, nd.W, acc, mask, s);
                 break;
+            }
             case HP_BN: {
                 // with a fused ReLU, nd.y holds the ReLU output and serves as the mask
                 bool want = dest(L.in0, &d, &acc);

@@ -28,9 +28,21 @@ typedef float floatx16 __attribute__((ext_vector_type(16)));
 
 namespace {
 
-constexpr int NT = 256;   // threads per workgroup
-constexpr int BK = 16;    // reduction tile
 constexpr int PAD = 4;    // LDS row padding (floats)
+
+// Tile configurations: workgroup tile BM x BN, reduction tile BK, wave tile
+// WM x WN (a grid of (WM/32) x (WN/32) MFMA 32x32 tiles per wave); the
+// workgroup has (BM/WM) * (BN/WN) waves.
+struct TileCfg { int bm, bn, bk, wm, wn; };
+constexpr TileCfg kCfgs[] = {
+    {128, 128, 16, 64, 64},    // 0: general
+    {256, 64, 16, 64, 64},     // 1: narrow N (64 output channels)
+    {64, 256, 16, 64, 64},     // 2: narrow M (weight gradients of 64-channel layers, FC)
+    {256, 128, 16, 128, 64},   // 3: large M, 4 waves of 128x64
+    {128, 256, 16, 64, 128},   // 4: large N, 4 waves of 64x128
+    {128, 128, 32, 64, 64},    // 5: general, deeper reduction tile
+};
+constexpr int kNumCfgs = sizeof(kCfgs) / sizeof(kCfgs[0]);
 
 struct KArgs {
     ConvGeo g;
@@ -38,12 +50,35 @@ struct KArgs {
     const float* b;
     float* out;
     const float* bias;
+    const float* mask;
+    float* bias_out;
     long M, Ncols, Kred;
     int kchunk;
     int tiles_m, tiles_n;
     int splits;
     int epi;
 };
+
+// Destination of output element (row, col): the bias-gradient column of a
+// weight gradient goes to bias_out[row]; everything else is row-major with
+// the weight part's row length.
+__device__ __forceinline__ float* out_ptr(float* out, float* bias_out, long row, long col,
+                                          long Ncols, int epi) {
+    if (epi & EPI_BIASCOL) {
+        if (col == Ncols - 1) return bias_out + row;
+        return out + row * (Ncols - 1) + col;
+    }
+    return out + row * Ncols + col;
+}
+
+__device__ __forceinline__ float epilogue(float v, long row, long col, long Ncols, int epi,
+                                          const float* bias, const float* mask, const float* prev) {
+    if (epi & EPI_BIAS) v += bias[col];
+    if (epi & EPI_RELU) v = fmaxf(v, 0.f);
+    if ((epi & EPI_MASK) && !(mask[row * Ncols + col] > 0.f)) v = 0.f;
+    if (epi & EPI_ACCUM) v += *prev;
+    return v;
+}
 
 __device__ __forceinline__ float round_bf16(float x) {
     unsigned u = __float_as_uint(x);
@@ -75,20 +110,21 @@ __device__ __forceinline__ void load_vec(const float* p, bool ok, float* v) {
     }
 }
 
-template <int OP, int BM, int BN, int VW, bool BF>
-__global__ void __launch_bounds__(NT, 2) igemm_kernel(KArgs args) {
+template <int OP, int BM, int BN, int BK, int WM, int WN, int VW, bool BF>
+__global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_kernel(KArgs args) {
+    constexpr int NT = 64 * (BM / WM) * (BN / WN);
+    constexpr int TM = WM / 32, TN = WN / 32;  // MFMA tiles per wave
     constexpr int LDA = BM + PAD;
     constexpr int LDB = BN + PAD;
-    constexpr int WAVES_N = BN / 64;           // wave grid: (BM/64) x (BN/64) = 4
-    static_assert((BM / 64) * (BN / 64) == 4, "4 waves of 64x64");
+    constexpr int WAVES_N = BN / WN;
     __shared__ float smem[2 * BK * (LDA + LDB)];
 
     const ConvGeo& g = args.g;
     const int t = threadIdx.x;
     const int lane = t & 63;
     const int wave = t >> 6;
-    const int wm = (wave / WAVES_N) * 64;
-    const int wn = (wave % WAVES_N) * 64;
+    const int wm = (wave / WAVES_N) * WM;
+    const int wn = (wave % WAVES_N) * WN;
 
     // XCD-aware tile order: consecutive workgroup ids are dealt round-robin to
     // the 8 XCDs; give each XCD a contiguous run of tiles (n fastest) so tiles
@@ -159,6 +195,7 @@ __global__ void __launch_bounds__(NT, 2) igemm_kernel(KArgs args) {
     // B
     int bcol_r = 0, bcol_s = 0, bcol_c = 0;
     bool bcol_ok = true;
+    bool bcol_ones = false;
     long brow_n[BV];
     bool brow_ok[BV];
     int bkv = 0;
@@ -173,6 +210,10 @@ __global__ void __launch_bounds__(NT, 2) igemm_kernel(KArgs args) {
     } else {
         long col = n0 + (t % BVPR) * VW;
         bcol_ok = col < args.Ncols;
+        if (OP == OP_WGRAD && (args.epi & EPI_BIASCOL) && col == args.Ncols - 1) {
+            bcol_ones = true;      // the appended column of ones (bias gradient)
+            bcol_ok = false;
+        }
         long cc = bcol_ok ? col : 0;
         if constexpr (OP == OP_WGRAD) {  // col = (r, s, c)
             bcol_c = (int)(cc % g.C); long tt = cc / g.C;
@@ -187,63 +228,93 @@ __global__ void __launch_bounds__(NT, 2) igemm_kernel(KArgs args) {
     float areg[AV][VW];
     float breg[BV][VW];
 
+    // Staging of one reduction tile [k0, k0 + BK).  The decomposition of k0 into
+    // (filter tap, channel) or (image, output row, output column) is uniform
+    // across the workgroup (scalar unit); each thread then steps from it by its
+    // own small offset instead of dividing per element.
     auto gload = [&](int kt) {
-        const long k0 = kbeg + (long)kt * BK;
-        // ---- A ----
+        const int k0 = (int)(kbeg + (long)kt * BK);
+        const int kend_i = (int)kend;
+        if constexpr (OP == OP_FWD || OP == OP_DGRAD) {
+            const int CC = (OP == OP_FWD) ? g.C : g.K;       // contiguous axis of a tap
+            const int rs0 = k0 / CC;
+            const int c0 = k0 - rs0 * CC;
+            const int r0 = rs0 / g.S;
+            const int s0 = rs0 - r0 * g.S;
+            // ---- A: k-major gathered rows ----
+            {
+                int c = c0 + akv, r = r0, sx = s0;
+                while (c >= CC) { c -= CC; if (++sx == g.S) { sx = 0; ++r; } }
+                const bool kin = k0 + akv < kend_i;
 #pragma unroll
-        for (int i = 0; i < AV; ++i) {
-            if constexpr (OP == OP_FWD) {
-                long kk = k0 + akv;
-                bool ok = arow_ok[i] && kk < kend;
-                int c = (int)(kk % g.C); int rs = (int)(kk / g.C);
-                int s = rs % g.S, r = rs / g.S;
-                int h = arow_h[i] + r, w = arow_w[i] + s;
-                ok = ok && (unsigned)h < (unsigned)g.H && (unsigned)w < (unsigned)g.W;
-                const float* p = args.a + (ok ? (arow_base[i] + ((long)h * g.W + w) * g.C + c) : 0);
-                load_vec<VW>(p, ok, areg[i]);
-            } else if constexpr (OP == OP_DGRAD) {
-                long kk = k0 + akv;
-                bool ok = arow_ok[i] && kk < kend;
-                int k = (int)(kk % g.K); int rs = (int)(kk / g.K);
-                int s = rs % g.S, r = rs / g.S;
-                int tp = arow_h[i] - r, tq = arow_w[i] - s;
-                int p = tp / g.st, q = tq / g.st;
-                ok = ok && tp >= 0 && tq >= 0 && p * g.st == tp && q * g.st == tq &&
-                     p < g.P && q < g.Q;
-                const float* ptr = args.a + (ok ? (arow_base[i] + ((long)p * g.Q + q) * g.K + k) : 0);
-                load_vec<VW>(ptr, ok, areg[i]);
-            } else {  // WGRAD: A[kk = m'][m = k-out] = dy[m'][k]
-                long kk = k0 + (t + i * NT) / AVPR;
-                bool ok = arow_ok[i] && kk < kend;
-                const float* ptr = args.b + (ok ? (kk * g.K + arow_base[i]) : 0);
+                for (int i = 0; i < AV; ++i) {
+                    if constexpr (OP == OP_FWD) {
+                        int h = arow_h[i] + r, w = arow_w[i] + sx;
+                        bool ok = arow_ok[i] && kin && (unsigned)h < (unsigned)g.H &&
+                                  (unsigned)w < (unsigned)g.W;
+                        const float* ptr =
+                            args.a + (ok ? (arow_base[i] + ((long)h * g.W + w) * g.C + c) : 0);
+                        load_vec<VW>(ptr, ok, areg[i]);
+                    } else {
+                        int tp = arow_h[i] - r, tq = arow_w[i] - sx;
+                        int p = tp / g.st, q = tq / g.st;
+                        bool ok = arow_ok[i] && kin && tp >= 0 && tq >= 0 && p * g.st == tp &&
+                                  q * g.st == tq && p < g.P && q < g.Q;
+                        const float* ptr =
+                            args.a + (ok ? (arow_base[i] + ((long)p * g.Q + q) * g.K + c) : 0);
+                        load_vec<VW>(ptr, ok, areg[i]);
+                    }
+                }
+            }
+            // ---- B ----
+#pragma unroll
+            for (int i = 0; i < BV; ++i) {
+                if constexpr (OP == OP_FWD) {
+                    const int kk = k0 + bkv;
+                    bool ok = brow_ok[i] && kk < kend_i;
+                    const float* ptr = args.b + (ok ? (brow_n[i] * args.Kred + kk) : 0);
+                    load_vec<VW>(ptr, ok, breg[i]);
+                } else {   // B[kk = (r,s,k)][c] = w[k][r][s][c]
+                    const int kr = (t + i * NT) / BVPR;
+                    int k = c0 + kr, r = r0, sx = s0;
+                    while (k >= CC) { k -= CC; if (++sx == g.S) { sx = 0; ++r; } }
+                    bool ok = bcol_ok && k0 + kr < kend_i;
+                    const float* ptr =
+                        args.b + (ok ? ((((long)k * g.R + r) * g.S + sx) * g.C + bcol_c) : 0);
+                    load_vec<VW>(ptr, ok, breg[i]);
+                }
+            }
+        } else {
+            // ---- A: dy rows, m-major: A[kk = m'][m = k-out] = dy[m'][k] ----
+#pragma unroll
+            for (int i = 0; i < AV; ++i) {
+                const int kk = k0 + (t + i * NT) / AVPR;
+                bool ok = arow_ok[i] && kk < kend_i;
+                const float* ptr = args.b + (ok ? ((long)kk * g.K + arow_base[i]) : 0);
                 load_vec<VW>(ptr, ok, areg[i]);
             }
-        }
-        // ---- B ----
+            // ---- B: B[kk = (n,p,q)][j = (r,s,c)] = x[n, p*st-pad+r, q*st-pad+s, c] ----
+            const int q0 = k0 % g.Q;
+            const int t0 = k0 / g.Q;
+            const int p0 = t0 % g.P;
+            const int n0i = t0 / g.P;
 #pragma unroll
-        for (int i = 0; i < BV; ++i) {
-            if constexpr (OP == OP_FWD) {
-                long kk = k0 + bkv;
-                bool ok = brow_ok[i] && kk < kend;
-                const float* ptr = args.b + (ok ? (brow_n[i] * args.Kred + kk) : 0);
-                load_vec<VW>(ptr, ok, breg[i]);
-            } else if constexpr (OP == OP_DGRAD) {  // B[kk = (r,s,k)][c] = w[k][r][s][c]
-                long kk = k0 + (t + i * NT) / BVPR;
-                bool ok = bcol_ok && kk < kend;
-                int k = (int)(kk % g.K); int rs = (int)(kk / g.K);
-                int s = rs % g.S, r = rs / g.S;
-                const float* ptr = args.b + (ok ? ((((long)k * g.R + r) * g.S + s) * g.C + bcol_c) : 0);
-                load_vec<VW>(ptr, ok, breg[i]);
-            } else {  // WGRAD: B[kk = (n,p,q)][j = (r,s,c)] = x[n, p*st-pad+r, q*st-pad+s, c]
-                long kk = k0 + (t + i * NT) / BVPR;
-                bool ok = bcol_ok && kk < kend;
-                long kc = ok ? kk : 0;
-                int q = (int)(kc % g.Q); long tt = kc / g.Q;
-                int p = (int)(tt % g.P); int n = (int)(tt / g.P);
+            for (int i = 0; i < BV; ++i) {
+                const int kr = (t + i * NT) / BVPR;
+                int q = q0 + kr, p = p0, n = n0i;
+                while (q >= g.Q) { q -= g.Q; if (++p == g.P) { p = 0; ++n; } }
+                const bool kin = k0 + kr < kend_i;
                 int h = p * g.st - g.pad + bcol_r, w = q * g.st - g.pad + bcol_s;
-                ok = ok && (unsigned)h < (unsigned)g.H && (unsigned)w < (unsigned)g.W;
-                const float* ptr = args.a + (ok ? ((((long)n * g.H + h) * g.W + w) * g.C + bcol_c) : 0);
+                bool ok = bcol_ok && kin && (unsigned)h < (unsigned)g.H &&
+                          (unsigned)w < (unsigned)g.W;
+                const float* ptr =
+                    args.a + (ok ? ((((long)n * g.H + h) * g.W + w) * g.C + bcol_c) : 0);
                 load_vec<VW>(ptr, ok, breg[i]);
+                if (bcol_ones) {
+                    breg[i][0] = kin ? 1.f : 0.f;
+#pragma unroll
+                    for (int j = 1; j < VW; ++j) breg[i][j] = 0.f;
+                }
             }
         }
     };
@@ -279,11 +350,11 @@ __global__ void __launch_bounds__(NT, 2) igemm_kernel(KArgs args) {
         }
     };
 
-    floatx16 acc[2][2];
+    floatx16 acc[TM][TN];
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < TM; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
+        for (int j = 0; j < TN; ++j)
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
@@ -303,12 +374,16 @@ __global__ void __launch_bounds__(NT, 2) igemm_kernel(KArgs args) {
         for (int kk = 0; kk < BK; kk += 2) {
             const float* ar = As + (kk + lk) * LDA + wm + lr;
             const float* br = Bs + (kk + lk) * LDB + wn + lr;
-            float a0 = ar[0], a1 = ar[32];
-            float b0 = br[0], b1 = br[32];
-            acc[0][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0, b0, acc[0][0], 0, 0, 0);
-            acc[0][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a0, b1, acc[0][1], 0, 0, 0);
-            acc[1][0] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1, b0, acc[1][0], 0, 0, 0);
-            acc[1][1] = __builtin_amdgcn_mfma_f32_32x32x2f32(a1, b1, acc[1][1], 0, 0, 0);
+            float av[TM], bv[TN];
+#pragma unroll
+            for (int i = 0; i < TM; ++i) av[i] = ar[32 * i];
+#pragma unroll
+            for (int j = 0; j < TN; ++j) bv[j] = br[32 * j];
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[i], bv[j], acc[i][j], 0, 0, 0);
         }
         if (kt + 1 < ktiles) sstore(buf ^ 1);
         __syncthreads();
@@ -317,90 +392,101 @@ __global__ void __launch_bounds__(NT, 2) igemm_kernel(KArgs args) {
     // ---- epilogue ----
     // acc[i][j][v] holds out[m0 + wm + 32i + 8(v/4) + 4(lane/32) + v%4][n0 + wn + 32j + lane%32]
     const bool partial = args.splits > 1;
-    float* out = args.out + (partial ? (long)z * args.M * args.Ncols : 0);
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
+    for (int j = 0; j < TN; ++j) {
         const long col = n0 + wn + 32 * j + lr;
         if (col >= args.Ncols) continue;
-        float bv = 0.f;
-        if (!partial && (args.epi & EPI_BIAS)) bv = args.bias[col];
 #pragma unroll
-        for (int i = 0; i < 2; ++i) {
+        for (int i = 0; i < TM; ++i) {
 #pragma unroll
             for (int v = 0; v < 16; ++v) {
                 const long row = m0 + wm + 32 * i + 8 * (v >> 2) + 4 * lk + (v & 3);
                 if (row >= args.M) continue;
                 float val = acc[i][j][v];
-                float* dst = out + row * args.Ncols + col;
-                if (!partial) {
-                    val += bv;
-                    if (args.epi & EPI_RELU) val = fmaxf(val, 0.f);
-                    if (args.epi & EPI_ACCUM) val += *dst;
+                if (partial) {
+                    args.out[((long)z * args.M + row) * args.Ncols + col] = val;
+                } else {
+                    float* dst = out_ptr(args.out, args.bias_out, row, col, args.Ncols, args.epi);
+                    *dst = epilogue(val, row, col, args.Ncols, args.epi, args.bias, args.mask, dst);
                 }
-                *dst = val;
             }
         }
     }
 }
 
-template <int OP, int BM, int BN, int VW, bool BF>
+template <int OP, int CFG, int VW, bool BF>
 hipError_t launch_cfg(const KArgs& a, hipStream_t s) {
+    constexpr TileCfg c = kCfgs[CFG];
+    constexpr int NT = 64 * (c.bm / c.wm) * (c.bn / c.wn);
     dim3 grid(a.tiles_m * a.tiles_n, a.splits);
-    hipLaunchKernelGGL((igemm_kernel<OP, BM, BN, VW, BF>), grid, dim3(NT), 0, s, a);
+    hipLaunchKernelGGL((igemm_kernel<OP, c.bm, c.bn, c.bk, c.wm, c.wn, VW, BF>), grid, dim3(NT), 0,
+                       s, a);
     return hipGetLastError();
 }
 
+// Vector width 1 (channel counts not divisible by 4) only occurs for the first
+// layer of an image stage; it is instantiated for the three basic shapes.
 template <int OP, int VW, bool BF>
 hipError_t launch_op(int cfg, const KArgs& a, hipStream_t s) {
-    switch (cfg) {
-        case 0: return launch_cfg<OP, 128, 128, VW, BF>(a, s);
-        case 1: return launch_cfg<OP, 256, 64, VW, BF>(a, s);
-        default: return launch_cfg<OP, 64, 256, VW, BF>(a, s);
+    if constexpr (VW == 1) {
+        switch (cfg) {
+            case 1: return launch_cfg<OP, 1, VW, BF>(a, s);
+            case 2: return launch_cfg<OP, 2, VW, BF>(a, s);
+            default: return launch_cfg<OP, 0, VW, BF>(a, s);
+        }
+    } else {
+        switch (cfg) {
+            case 1: return launch_cfg<OP, 1, VW, BF>(a, s);
+            case 2: return launch_cfg<OP, 2, VW, BF>(a, s);
+            case 3: return launch_cfg<OP, 3, VW, BF>(a, s);
+            case 4: return launch_cfg<OP, 4, VW, BF>(a, s);
+            case 5: return launch_cfg<OP, 5, VW, BF>(a, s);
+            default: return launch_cfg<OP, 0, VW, BF>(a, s);
+        }
     }
 }
 
-void tile_shape(int cfg, int& bm, int& bn) {
-    bm = cfg == 0 ? 128 : (cfg == 1 ? 256 : 64);
-    bn = cfg == 0 ? 128 : (cfg == 1 ? 64 : 256);
-}
-
-int choose_cfg(long M, long N) {
-    if (N <= 64 && M > 64) return 1;
-    if (M <= 64 && N > 64) return 2;
-    return 0;
+// Tile configuration for a contraction of M x N (x Kred).
+int choose_cfg(long M, long N, bool v4) {
+    int c = 0;
+    if (N <= 64 && M > 64) c = 1;
+    else if (M <= 64 && N > 64) c = 2;
+    if (!v4 && c > 2) c = 0;
+    return c;
 }
 
 __global__ void splitk_reduce_kernel(const float* __restrict__ ws, int splits, long M, long Ncols,
-                                     float* __restrict__ out, const float* __restrict__ bias,
-                                     int epi) {
+                                     float* out, const float* __restrict__ bias,
+                                     const float* __restrict__ mask, float* bias_out, int epi) {
     const long total = M * Ncols;
     const long stride = (long)gridDim.x * blockDim.x;
     for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += stride) {
         float acc = 0.f;
         for (int z = 0; z < splits; ++z) acc += ws[(long)z * total + i];
-        if (epi & EPI_BIAS) acc += bias[i % Ncols];
-        if (epi & EPI_RELU) acc = fmaxf(acc, 0.f);
-        if (epi & EPI_ACCUM) acc += out[i];
-        out[i] = acc;
+        const long row = i / Ncols, col = i % Ncols;
+        float* dst = out_ptr(out, bias_out, row, col, Ncols, epi);
+        *dst = epilogue(acc, row, col, Ncols, epi, bias, mask, dst);
     }
 }
 
 }  // namespace
 
-GemmPlan plan_gemm(int op, const ConvGeo& g, int bf16, int num_cus) {
+GemmPlan plan_gemm(int op, const ConvGeo& g, int bf16, int num_cus, int bias_col) {
     GemmPlan p{};
     p.op = op;
     p.bf16 = bf16;
+    p.bias_col = (op == OP_WGRAD) ? bias_col : 0;
     if (op == OP_FWD) {
         p.M = (long)g.N * g.P * g.Q; p.Ncols = g.K; p.Kred = (long)g.R * g.S * g.C;
     } else if (op == OP_DGRAD) {
         p.M = (long)g.N * g.H * g.W; p.Ncols = g.C; p.Kred = (long)g.R * g.S * g.K;
     } else {
-        p.M = g.K; p.Ncols = (long)g.R * g.S * g.C; p.Kred = (long)g.N * g.P * g.Q;
+        p.M = g.K; p.Ncols = (long)g.R * g.S * g.C + (p.bias_col ? 1 : 0);
+        p.Kred = (long)g.N * g.P * g.Q;
     }
-    int cfg = choose_cfg(p.M, p.Ncols);
-    int bm, bn;
-    tile_shape(cfg, bm, bn);
+    const bool v4 = (op == OP_FWD) ? (g.C % 4 == 0) : (g.C % 4 == 0 && g.K % 4 == 0);
+    p.cfg = choose_cfg(p.M, p.Ncols, v4);
+    const int bm = kCfgs[p.cfg].bm, bn = kCfgs[p.cfg].bn, BK = kCfgs[p.cfg].bk;
     long tiles = ((p.M + bm - 1) / bm) * ((p.Ncols + bn - 1) / bn);
     long ktiles = (p.Kred + BK - 1) / BK;
     // split the reduction when the output alone cannot fill the chip
@@ -420,29 +506,31 @@ GemmPlan plan_gemm(int op, const ConvGeo& g, int bf16, int num_cus) {
 }
 
 hipError_t launch_gemm(const GemmPlan& plan, const ConvGeo& g, const float* a, const float* b,
-                       float* out, const float* bias, int epi, float* ws, hipStream_t s) {
+                       float* out, const Epilogue& ep, float* ws, hipStream_t s) {
     KArgs k{};
     k.g = g;
     k.a = a;
     k.b = b;
-    k.bias = bias;
+    k.bias = ep.bias;
+    k.mask = ep.mask;
+    k.bias_out = ep.bias_out;
+    const int epi = ep.flags | (plan.bias_col ? EPI_BIASCOL : 0);
     k.M = plan.M;
     k.Ncols = plan.Ncols;
     k.Kred = plan.Kred;
     k.kchunk = plan.kchunk;
     k.splits = plan.splits;
     k.epi = epi;
-    int cfg = choose_cfg(plan.M, plan.Ncols);
-    int bm, bn;
-    tile_shape(cfg, bm, bn);
-    k.tiles_m = (int)((plan.M + bm - 1) / bm);
-    k.tiles_n = (int)((plan.Ncols + bn - 1) / bn);
+    int cfg = plan.cfg;
     k.out = plan.splits > 1 ? ws : out;
     // vector width 4 needs the contiguous axes to be multiples of 4
     bool v4;
     if (plan.op == OP_FWD) v4 = (g.C % 4 == 0);
     else v4 = (g.C % 4 == 0) && (g.K % 4 == 0);
     v4 = v4 && ((((uintptr_t)a) | ((uintptr_t)b)) & 15) == 0;
+    if (!v4 && cfg > 2) cfg = 0;     // (unaligned operands: scalar staging, basic tile)
+    k.tiles_m = (int)((plan.M + kCfgs[cfg].bm - 1) / kCfgs[cfg].bm);
+    k.tiles_n = (int)((plan.Ncols + kCfgs[cfg].bn - 1) / kCfgs[cfg].bn);
     hipError_t e;
     const bool bf = plan.bf16 != 0;
 #define HP_DISPATCH(OPC)                                                       \
@@ -453,15 +541,17 @@ hipError_t launch_gemm(const GemmPlan& plan, const ConvGeo& g, const float* a, c
     else { HP_DISPATCH(OP_WGRAD) }
 #undef HP_DISPATCH
     if (e != hipSuccess || plan.splits == 1) return e;
-    return launch_splitk_reduce(ws, plan.splits, plan.M, plan.Ncols, out, bias, epi, s);
+    Epilogue e2 = ep;
+    e2.flags = epi;
+    return launch_splitk_reduce(ws, plan.splits, plan.M, plan.Ncols, out, e2, s);
 }
 
 hipError_t launch_splitk_reduce(const float* ws, int splits, long M, long Ncols, float* out,
-                                const float* bias, int epi, hipStream_t s) {
+                                const Epilogue& ep, hipStream_t s) {
     long total = M * Ncols;
     int blocks = (int)std::min<long>((total + 255) / 256, 4096);
     hipLaunchKernelGGL(splitk_reduce_kernel, dim3(blocks), dim3(256), 0, s, ws, splits, M, Ncols,
-                       out, bias, epi);
+                       out, ep.bias, ep.mask, ep.bias_out, ep.flags);
     return hipGetLastError();
 }
 

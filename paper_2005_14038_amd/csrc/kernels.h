@@ -25,19 +25,36 @@ struct GemmPlan {
     int op;
     int bf16;          // round operands to bf16 (RNE) when staging
     int splits;        // split-K factor (1 = direct epilogue)
+    int bias_col;      // OP_WGRAD: Ncols includes the bias-gradient column
+    int cfg;           // tile configuration
     int kchunk;        // reduction length per split (multiple of the K tile)
     size_t ws_floats;  // workspace needed (splits * M * Ncols when splits > 1)
     long M, Ncols, Kred;
 };
 
-GemmPlan plan_gemm(int op, const ConvGeo& g, int bf16, int num_cus);
+// bias_col (OP_WGRAD only): append a column of ones to the gathered input so
+// that the last output column is sum_m dy[m][k], the bias gradient.
+GemmPlan plan_gemm(int op, const ConvGeo& g, int bf16, int num_cus, int bias_col = 0);
 
 // epilogue flags
-enum { EPI_BIAS = 1, EPI_RELU = 2, EPI_ACCUM = 4 };
+enum {
+    EPI_BIAS = 1,     // out += bias[col]
+    EPI_RELU = 2,     // out = max(out, 0)
+    EPI_ACCUM = 4,    // out += previous out
+    EPI_MASK = 8,     // out = mask[row][col] > 0 ? out : 0   (ReLU backward fused)
+    EPI_BIASCOL = 16  // last column (see plan_gemm bias_col) goes to bias_out[row]
+};
+
+struct Epilogue {
+    int flags = 0;
+    const float* bias = nullptr;
+    const float* mask = nullptr;
+    float* bias_out = nullptr;
+};
 
 hipError_t launch_gemm(const GemmPlan& plan, const ConvGeo& g, const float* a,
-                       const float* b, float* out, const float* bias, int epi,
-                       float* ws, hipStream_t s);
+                       const float* b, float* out, const Epilogue& ep, float* ws,
+                       hipStream_t s);
 
 // ---- element-wise / reduction kernels (elementwise.hip) -------------------
 // y = max(x, 0)
@@ -53,9 +70,11 @@ hipError_t launch_copy_or_acc(const float* v, float* out, size_t n, int accumula
                               hipStream_t s);
 hipError_t launch_maxpool_fwd(const float* x, float* y, int N, int H, int W, int C, int R,
                               int S, int st, int pad, int P, int Q, hipStream_t s);
+// mask (optional, layout of dx): the pooled input is a ReLU output; dx is
+// zeroed where mask <= 0 (ReLU backward fused)
 hipError_t launch_maxpool_bwd(const float* x, const float* dy, float* dx, int N, int H, int W,
                               int C, int R, int S, int st, int pad, int P, int Q,
-                              int accumulate, hipStream_t s);
+                              int accumulate, const float* mask, hipStream_t s);
 hipError_t launch_gap_fwd(const float* x, float* y, int N, int HW, int C, hipStream_t s);
 hipError_t launch_gap_bwd(const float* dy, float* dx, int N, int HW, int C, int accumulate,
                           hipStream_t s);
@@ -84,9 +103,9 @@ hipError_t launch_bn_bwd(const float* x, const float* dy, const float* relu_y, l
 hipError_t launch_softmax_ce(const float* z, const int32_t* labels, int B, int K, float* loss,
                              float* dz, float* ws, hipStream_t s);
 
-// split-K finalisation: out = sum_z ws[z] (+bias[col]) (relu) (accumulate)
+// split-K finalisation: out = epilogue(sum_z ws[z]) with the flags of `ep`
 hipError_t launch_splitk_reduce(const float* ws, int splits, long M, long Ncols, float* out,
-                                const float* bias, int epi, hipStream_t s);
+                                const Epilogue& ep, hipStream_t s);
 
 // ---- WSP kernels (wsp.hip) ------------------------------------------------
 // u = (-lr)*g; dst = newest + u; ut = first ? u : ut + u   (no FMA contraction)
