@@ -28,7 +28,12 @@ typedef float floatx16 __attribute__((ext_vector_type(16)));
 
 namespace {
 
-constexpr int PAD = 4;    // LDS row padding (floats)
+// LDS row padding (floats).  Operands staged from k-major rows are written
+// transposed, one float per store: a row length of 2 mod 32 spreads a wave's
+// stores over distinct banks.  Operands staged as whole float4 rows need a
+// row length that keeps 16-byte alignment.
+constexpr int PAD_T = 2;
+constexpr int PAD_V = 4;
 
 // Tile configurations: workgroup tile BM x BN, reduction tile BK, wave tile
 // WM x WN (a grid of (WM/32) x (WN/32) MFMA 32x32 tiles per wave); the
@@ -53,9 +58,11 @@ struct KArgs {
     const float* mask;
     float* bias_out;
     long M, Ncols, Kred;
-    int kchunk;
     int tiles_m, tiles_n;
-    int splits;
+    int tfull;        // tiles computed whole, one per workgroup (the first tfull ids)
+    int splits;       // every remaining tile is cut into `splits` reduction chunks
+    int kchunk;       // reduction length of a chunk (multiple of the K tile)
+    float* ws;        // partial tiles of the cut tiles: [tile - tfull][split][BM * BN]
     int epi;
 };
 
@@ -114,8 +121,10 @@ template <int OP, int BM, int BN, int BK, int WM, int WN, int VW, bool BF>
 __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_kernel(KArgs args) {
     constexpr int NT = 64 * (BM / WM) * (BN / WN);
     constexpr int TM = WM / 32, TN = WN / 32;  // MFMA tiles per wave
-    constexpr int LDA = BM + PAD;
-    constexpr int LDB = BN + PAD;
+    constexpr bool A_KMAJ = (OP != OP_WGRAD);
+    constexpr bool B_KMAJ = (OP == OP_FWD);
+    constexpr int LDA = BM + (A_KMAJ ? PAD_T : PAD_V);
+    constexpr int LDB = BN + (B_KMAJ ? PAD_T : PAD_V);
     constexpr int WAVES_N = BN / WN;
     __shared__ float smem[2 * BK * (LDA + LDB)];
 
@@ -126,19 +135,30 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_kernel(KA
     const int wm = (wave / WAVES_N) * WM;
     const int wn = (wave % WAVES_N) * WN;
 
-    // XCD-aware tile order: consecutive workgroup ids are dealt round-robin to
-    // the 8 XCDs; give each XCD a contiguous run of tiles (n fastest) so tiles
-    // that share A rows share that XCD's L2.
-    const int ntiles = args.tiles_m * args.tiles_n;
+    // Work assignment.  The first `tfull` workgroups each compute one whole
+    // output tile (whole rounds of the resident workgroups); the rest cut each
+    // remaining tile's reduction into `splits` chunks, so that the last round
+    // is as full as the others, and leave partial tiles for
+    // igemm_splitk_reduce_kernel.  XCD-aware: consecutive workgroup ids are
+    // dealt round-robin to the 8 XCDs; each XCD gets a contiguous run of whole
+    // tiles (n fastest), so tiles sharing A rows share that XCD's L2.
     int bid = blockIdx.x;
-    if ((ntiles & 7) == 0) bid = (bid & 7) * (ntiles >> 3) + (bid >> 3);
-    const int tm = bid / args.tiles_n;
-    const int tn = bid % args.tiles_n;
+    int tile, z = 0;
+    const bool partial = bid >= args.tfull;
+    if (!partial) {
+        if ((args.tfull & 7) == 0) bid = (bid & 7) * (args.tfull >> 3) + (bid >> 3);
+        tile = bid;
+    } else {
+        const int r = bid - args.tfull;
+        tile = args.tfull + r / args.splits;
+        z = r - (tile - args.tfull) * args.splits;
+    }
+    const int tm = tile / args.tiles_n;
+    const int tn = tile % args.tiles_n;
     const long m0 = (long)tm * BM;
     const long n0 = (long)tn * BN;
-    const int z = blockIdx.y;
-    const long kbeg = (long)z * args.kchunk;
-    const long kend = min(kbeg + (long)args.kchunk, args.Kred);
+    const long kbeg = partial ? (long)z * args.kchunk : 0;
+    const long kend = partial ? min(kbeg + (long)args.kchunk, args.Kred) : args.Kred;
     const int ktiles = (int)((kend - kbeg + BK - 1) / BK);
 
     // ---- per-thread staging coordinates ----
@@ -146,8 +166,6 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_kernel(KA
     // ("k-major"); OP_WGRAD reads dy rows (reduction index = row) with m = k
     // contiguous ("m-major").  B: OP_FWD reads weight rows (k-major);
     // OP_DGRAD / OP_WGRAD read rows indexed by the reduction with n contiguous.
-    constexpr bool A_KMAJ = (OP != OP_WGRAD);
-    constexpr bool B_KMAJ = (OP == OP_FWD);
     constexpr int AV = A_KMAJ ? (BM * BK / VW / NT) : (BM * BK / VW / NT);
     constexpr int BV = (BN * BK / VW / NT);
     static_assert(AV >= 1 && BV >= 1, "tile too small");
@@ -257,9 +275,15 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_kernel(KA
                         load_vec<VW>(ptr, ok, areg[i]);
                     } else {
                         int tp = arow_h[i] - r, tq = arow_w[i] - sx;
-                        int p = tp / g.st, q = tq / g.st;
-                        bool ok = arow_ok[i] && kin && tp >= 0 && tq >= 0 && p * g.st == tp &&
-                                  q * g.st == tq && p < g.P && q < g.Q;
+                        int p = tp, q = tq;
+                        bool on_grid = true;
+                        if (g.st != 1) {            // (uniform branch) strided: exact taps only
+                            p = tp / g.st;
+                            q = tq / g.st;
+                            on_grid = p * g.st == tp && q * g.st == tq;
+                        }
+                        bool ok = arow_ok[i] && kin && tp >= 0 && tq >= 0 && on_grid &&
+                                  p < g.P && q < g.Q;
                         const float* ptr =
                             args.a + (ok ? (arow_base[i] + ((long)p * g.Q + q) * g.K + c) : 0);
                         load_vec<VW>(ptr, ok, areg[i]);
@@ -391,20 +415,23 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_kernel(KA
 
     // ---- epilogue ----
     // acc[i][j][v] holds out[m0 + wm + 32i + 8(v/4) + 4(lane/32) + v%4][n0 + wn + 32j + lane%32]
-    const bool partial = args.splits > 1;
+    float* pslot = partial ? args.ws + ((long)(tile - args.tfull) * args.splits + z) * (BM * BN)
+                           : nullptr;
 #pragma unroll
     for (int j = 0; j < TN; ++j) {
-        const long col = n0 + wn + 32 * j + lr;
+        const int lcol = wn + 32 * j + lr;
+        const long col = n0 + lcol;
         if (col >= args.Ncols) continue;
 #pragma unroll
         for (int i = 0; i < TM; ++i) {
 #pragma unroll
             for (int v = 0; v < 16; ++v) {
-                const long row = m0 + wm + 32 * i + 8 * (v >> 2) + 4 * lk + (v & 3);
+                const int lrow = wm + 32 * i + 8 * (v >> 2) + 4 * lk + (v & 3);
+                const long row = m0 + lrow;
                 if (row >= args.M) continue;
                 float val = acc[i][j][v];
                 if (partial) {
-                    args.out[((long)z * args.M + row) * args.Ncols + col] = val;
+                    pslot[lrow * BN + lcol] = val;
                 } else {
                     float* dst = out_ptr(args.out, args.bias_out, row, col, args.Ncols, args.epi);
                     *dst = epilogue(val, row, col, args.Ncols, args.epi, args.bias, args.mask, dst);
@@ -414,36 +441,100 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_kernel(KA
     }
 }
 
+// Reduction of the cut tiles: workgroup = 64 elements of one tile x 16 split
+// lanes; lane l adds splits l, l+16, ...; the lane sums are combined in a
+// fixed order (deterministic), then the epilogue runs.
+constexpr int SK_EL = 64, SK_LANES = 16;
+
+__global__ void __launch_bounds__(SK_EL * SK_LANES)
+igemm_splitk_reduce_kernel(KArgs args, int BM, int BN) {
+    __shared__ float red[SK_LANES][SK_EL];
+    const int el = threadIdx.x % SK_EL;
+    const int ln = threadIdx.x / SK_EL;
+    const int chunks = (BM * BN) / SK_EL;
+    const int rt = blockIdx.x / chunks;                 // index among the cut tiles
+    const int e = (blockIdx.x - rt * chunks) * SK_EL + el;
+    const int tile = args.tfull + rt;
+    const long row = (long)(tile / args.tiles_n) * BM + e / BN;
+    const long col = (long)(tile % args.tiles_n) * BN + e % BN;
+    float s = 0.f;
+    const float* src = args.ws + (long)rt * args.splits * (BM * BN) + e;
+    for (int z = ln; z < args.splits; z += SK_LANES) s += src[(long)z * (BM * BN)];
+    red[ln][el] = s;
+    __syncthreads();
+    if (ln == 0 && row < args.M && col < args.Ncols) {
+        float acc = 0.f;
+        for (int l = 0; l < SK_LANES; ++l) acc += red[l][el];
+        float* dst = out_ptr(args.out, args.bias_out, row, col, args.Ncols, args.epi);
+        *dst = epilogue(acc, row, col, args.Ncols, args.epi, args.bias, args.mask, dst);
+    }
+}
+
+// The same reduction for few splits: one thread per element of the cut tiles
+// (grid-stride), adding the splits in order.
+__global__ void __launch_bounds__(256) igemm_cut_reduce_kernel(KArgs args, int BM, int BN) {
+    const long tile_elems = (long)BM * BN;
+    const long total = (long)(args.tiles_m * args.tiles_n - args.tfull) * tile_elems;
+    for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < total;
+         i += (long)gridDim.x * blockDim.x) {
+        const int rt = (int)(i / tile_elems);
+        const int e = (int)(i - rt * tile_elems);
+        const int tile = args.tfull + rt;
+        const long row = (long)(tile / args.tiles_n) * BM + e / BN;
+        const long col = (long)(tile % args.tiles_n) * BN + e % BN;
+        if (row >= args.M || col >= args.Ncols) continue;
+        const float* src = args.ws + (long)rt * args.splits * tile_elems + e;
+        float acc = 0.f;
+        for (int z = 0; z < args.splits; ++z) acc += src[z * tile_elems];
+        float* dst = out_ptr(args.out, args.bias_out, row, col, args.Ncols, args.epi);
+        *dst = epilogue(acc, row, col, args.Ncols, args.epi, args.bias, args.mask, dst);
+    }
+}
+
+struct KernelRef {
+    const void* fn;
+    int nt;
+};
+
 template <int OP, int CFG, int VW, bool BF>
-hipError_t launch_cfg(const KArgs& a, hipStream_t s) {
+KernelRef kref() {
     constexpr TileCfg c = kCfgs[CFG];
-    constexpr int NT = 64 * (c.bm / c.wm) * (c.bn / c.wn);
-    dim3 grid(a.tiles_m * a.tiles_n, a.splits);
-    hipLaunchKernelGGL((igemm_kernel<OP, c.bm, c.bn, c.bk, c.wm, c.wn, VW, BF>), grid, dim3(NT), 0,
-                       s, a);
-    return hipGetLastError();
+    return {reinterpret_cast<const void*>(&igemm_kernel<OP, c.bm, c.bn, c.bk, c.wm, c.wn, VW, BF>),
+            64 * (c.bm / c.wm) * (c.bn / c.wn)};
 }
 
 // Vector width 1 (channel counts not divisible by 4) only occurs for the first
 // layer of an image stage; it is instantiated for the three basic shapes.
 template <int OP, int VW, bool BF>
-hipError_t launch_op(int cfg, const KArgs& a, hipStream_t s) {
+KernelRef kref_cfg(int cfg) {
     if constexpr (VW == 1) {
         switch (cfg) {
-            case 1: return launch_cfg<OP, 1, VW, BF>(a, s);
-            case 2: return launch_cfg<OP, 2, VW, BF>(a, s);
-            default: return launch_cfg<OP, 0, VW, BF>(a, s);
+            case 1: return kref<OP, 1, VW, BF>();
+            case 2: return kref<OP, 2, VW, BF>();
+            default: return kref<OP, 0, VW, BF>();
         }
     } else {
         switch (cfg) {
-            case 1: return launch_cfg<OP, 1, VW, BF>(a, s);
-            case 2: return launch_cfg<OP, 2, VW, BF>(a, s);
-            case 3: return launch_cfg<OP, 3, VW, BF>(a, s);
-            case 4: return launch_cfg<OP, 4, VW, BF>(a, s);
-            case 5: return launch_cfg<OP, 5, VW, BF>(a, s);
-            default: return launch_cfg<OP, 0, VW, BF>(a, s);
+            case 1: return kref<OP, 1, VW, BF>();
+            case 2: return kref<OP, 2, VW, BF>();
+            case 3: return kref<OP, 3, VW, BF>();
+            case 4: return kref<OP, 4, VW, BF>();
+            case 5: return kref<OP, 5, VW, BF>();
+            default: return kref<OP, 0, VW, BF>();
         }
     }
+}
+
+template <int OP>
+KernelRef kref_op(int cfg, bool v4, bool bf) {
+    if (v4) return bf ? kref_cfg<OP, 4, true>(cfg) : kref_cfg<OP, 4, false>(cfg);
+    return bf ? kref_cfg<OP, 1, true>(cfg) : kref_cfg<OP, 1, false>(cfg);
+}
+
+KernelRef kernel_for(int op, int cfg, bool v4, bool bf) {
+    if (op == OP_FWD) return kref_op<OP_FWD>(cfg, v4, bf);
+    if (op == OP_DGRAD) return kref_op<OP_DGRAD>(cfg, v4, bf);
+    return kref_op<OP_WGRAD>(cfg, v4, bf);
 }
 
 // Tile configuration for a contraction of M x N (x Kred).
@@ -453,20 +544,6 @@ int choose_cfg(long M, long N, bool v4) {
     else if (M <= 64 && N > 64) c = 2;
     if (!v4 && c > 2) c = 0;
     return c;
-}
-
-__global__ void splitk_reduce_kernel(const float* __restrict__ ws, int splits, long M, long Ncols,
-                                     float* out, const float* __restrict__ bias,
-                                     const float* __restrict__ mask, float* bias_out, int epi) {
-    const long total = M * Ncols;
-    const long stride = (long)gridDim.x * blockDim.x;
-    for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < total; i += stride) {
-        float acc = 0.f;
-        for (int z = 0; z < splits; ++z) acc += ws[(long)z * total + i];
-        const long row = i / Ncols, col = i % Ncols;
-        float* dst = out_ptr(out, bias_out, row, col, Ncols, epi);
-        *dst = epilogue(acc, row, col, Ncols, epi, bias, mask, dst);
-    }
 }
 
 }  // namespace
@@ -486,22 +563,38 @@ GemmPlan plan_gemm(int op, const ConvGeo& g, int bf16, int num_cus, int bias_col
     }
     const bool v4 = (op == OP_FWD) ? (g.C % 4 == 0) : (g.C % 4 == 0 && g.K % 4 == 0);
     p.cfg = choose_cfg(p.M, p.Ncols, v4);
-    const int bm = kCfgs[p.cfg].bm, bn = kCfgs[p.cfg].bn, BK = kCfgs[p.cfg].bk;
-    long tiles = ((p.M + bm - 1) / bm) * ((p.Ncols + bn - 1) / bn);
-    long ktiles = (p.Kred + BK - 1) / BK;
-    // split the reduction when the output alone cannot fill the chip
-    long target = 4L * num_cus;
-    long splits = 1;
-    if (tiles < target) {
-        splits = (target + tiles - 1) / tiles;
-        long max_splits = ktiles / 8;        // keep >= 8 reduction tiles per split
-        if (splits > max_splits) splits = max_splits;
-        if (splits < 1) splits = 1;
+    const TileCfg& c = kCfgs[p.cfg];
+    const long tiles = ((p.M + c.bm - 1) / c.bm) * ((p.Ncols + c.bn - 1) / c.bn);
+    const long ktiles = (p.Kred + c.bk - 1) / c.bk;
+    // workgroups resident at once
+    KernelRef kr = kernel_for(op, p.cfg, v4, bf16 != 0);
+    int occ = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, kr.fn, kr.nt, 0) != hipSuccess || occ < 1)
+        occ = 1;
+    const long slots = (long)num_cus * occ;
+    long tfull = tiles, splits = 1;
+    if (tiles >= slots) {
+        // whole rounds of whole tiles; cut the tiles of a partial last round
+        // into s chunks when that shortens it: time ~ ceil(rem*s/slots)/s
+        const long rounds = tiles / slots, rem = tiles - rounds * slots;
+        double best = 1.0;
+        for (long s = 2; rem && s <= 16 && s * 4 <= ktiles; ++s) {
+            double t = (double)((rem * s + slots - 1) / slots) / s + 0.01 * s;
+            if (t < best) { best = t; splits = s; }
+        }
+        if (splits > 1) tfull = rounds * slots;
+    } else {
+        // too few tiles: cut every tile so that one round is filled
+        splits = std::min<long>(slots / tiles, ktiles / 8);
+        if (splits >= 2) tfull = 0;
+        else splits = 1;
     }
     long chunk_tiles = (ktiles + splits - 1) / splits;
-    p.kchunk = (int)(chunk_tiles * BK);
     p.splits = (int)((ktiles + chunk_tiles - 1) / chunk_tiles);
-    p.ws_floats = p.splits > 1 ? (size_t)p.splits * p.M * p.Ncols : 0;
+    p.kchunk = (int)(chunk_tiles * c.bk);
+    p.tfull = (int)(p.splits > 1 ? tfull : tiles);
+    p.nwg = (int)(p.tfull + (tiles - p.tfull) * p.splits);
+    p.ws_floats = (size_t)(tiles - p.tfull) * p.splits * c.bm * c.bn;
     return p;
 }
 
@@ -511,47 +604,39 @@ hipError_t launch_gemm(const GemmPlan& plan, const ConvGeo& g, const float* a, c
     k.g = g;
     k.a = a;
     k.b = b;
+    k.out = out;
     k.bias = ep.bias;
     k.mask = ep.mask;
     k.bias_out = ep.bias_out;
-    const int epi = ep.flags | (plan.bias_col ? EPI_BIASCOL : 0);
+    k.epi = ep.flags | (plan.bias_col ? EPI_BIASCOL : 0);
     k.M = plan.M;
     k.Ncols = plan.Ncols;
     k.Kred = plan.Kred;
-    k.kchunk = plan.kchunk;
+    k.tfull = plan.tfull;
     k.splits = plan.splits;
-    k.epi = epi;
-    int cfg = plan.cfg;
-    k.out = plan.splits > 1 ? ws : out;
-    // vector width 4 needs the contiguous axes to be multiples of 4
-    bool v4;
-    if (plan.op == OP_FWD) v4 = (g.C % 4 == 0);
-    else v4 = (g.C % 4 == 0) && (g.K % 4 == 0);
+    k.kchunk = plan.kchunk;
+    k.ws = ws;
+    const TileCfg& c = kCfgs[plan.cfg];
+    k.tiles_m = (int)((plan.M + c.bm - 1) / c.bm);
+    k.tiles_n = (int)((plan.Ncols + c.bn - 1) / c.bn);
+    // vector width 4 needs the contiguous axes to be multiples of 4 and the
+    // operand bases 16-byte aligned
+    bool v4 = (plan.op == OP_FWD) ? (g.C % 4 == 0) : (g.C % 4 == 0 && g.K % 4 == 0);
     v4 = v4 && ((((uintptr_t)a) | ((uintptr_t)b)) & 15) == 0;
-    if (!v4 && cfg > 2) cfg = 0;     // (unaligned operands: scalar staging, basic tile)
-    k.tiles_m = (int)((plan.M + kCfgs[cfg].bm - 1) / kCfgs[cfg].bm);
-    k.tiles_n = (int)((plan.Ncols + kCfgs[cfg].bn - 1) / kCfgs[cfg].bn);
-    hipError_t e;
-    const bool bf = plan.bf16 != 0;
-#define HP_DISPATCH(OPC)                                                       \
-    if (v4) e = bf ? launch_op<OPC, 4, true>(cfg, k, s) : launch_op<OPC, 4, false>(cfg, k, s); \
-    else e = bf ? launch_op<OPC, 1, true>(cfg, k, s) : launch_op<OPC, 1, false>(cfg, k, s);
-    if (plan.op == OP_FWD) { HP_DISPATCH(OP_FWD) }
-    else if (plan.op == OP_DGRAD) { HP_DISPATCH(OP_DGRAD) }
-    else { HP_DISPATCH(OP_WGRAD) }
-#undef HP_DISPATCH
-    if (e != hipSuccess || plan.splits == 1) return e;
-    Epilogue e2 = ep;
-    e2.flags = epi;
-    return launch_splitk_reduce(ws, plan.splits, plan.M, plan.Ncols, out, e2, s);
-}
-
-hipError_t launch_splitk_reduce(const float* ws, int splits, long M, long Ncols, float* out,
-                                const Epilogue& ep, hipStream_t s) {
-    long total = M * Ncols;
-    int blocks = (int)std::min<long>((total + 255) / 256, 4096);
-    hipLaunchKernelGGL(splitk_reduce_kernel, dim3(blocks), dim3(256), 0, s, ws, splits, M, Ncols,
-                       out, ep.bias, ep.mask, ep.bias_out, ep.flags);
+    if (!v4 && plan.cfg > 2) return hipErrorInvalidValue;   // planned for aligned operands
+    KernelRef kr = kernel_for(plan.op, plan.cfg, v4, plan.bf16 != 0);
+    void* kargs[] = {&k};
+    hipError_t e = hipLaunchKernel(kr.fn, dim3(plan.nwg), dim3(kr.nt), kargs, 0, s);
+    const int cut = k.tiles_m * k.tiles_n - plan.tfull;
+    if (e != hipSuccess || cut == 0) return e;
+    if (plan.splits <= SK_LANES) {
+        const long total = (long)cut * c.bm * c.bn;
+        const int blocks = (int)std::min<long>((total + 255) / 256, 8192);
+        hipLaunchKernelGGL(igemm_cut_reduce_kernel, dim3(blocks), dim3(256), 0, s, k, c.bm, c.bn);
+    } else {
+        hipLaunchKernelGGL(igemm_splitk_reduce_kernel, dim3(cut * (c.bm * c.bn / SK_EL)),
+                           dim3(SK_EL * SK_LANES), 0, s, k, c.bm, c.bn);
+    }
     return hipGetLastError();
 }
 

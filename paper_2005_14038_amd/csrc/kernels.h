@@ -24,11 +24,13 @@ enum GemmOp { OP_FWD = 0, OP_DGRAD = 1, OP_WGRAD = 2 };
 struct GemmPlan {
     int op;
     int bf16;          // round operands to bf16 (RNE) when staging
-    int splits;        // split-K factor (1 = direct epilogue)
     int bias_col;      // OP_WGRAD: Ncols includes the bias-gradient column
     int cfg;           // tile configuration
-    int kchunk;        // reduction length per split (multiple of the K tile)
-    size_t ws_floats;  // workspace needed (splits * M * Ncols when splits > 1)
+    int tfull;         // tiles computed whole (one workgroup each)
+    int splits;        // the other tiles are cut into `splits` reduction chunks
+    int kchunk;        // reduction length of a chunk (multiple of the K tile)
+    int nwg;           // workgroups launched
+    size_t ws_floats;  // workspace for the partial tiles of the cut tiles
     long M, Ncols, Kred;
 };
 
@@ -103,9 +105,6 @@ hipError_t launch_bn_bwd(const float* x, const float* dy, const float* relu_y, l
 hipError_t launch_softmax_ce(const float* z, const int32_t* labels, int B, int K, float* loss,
                              float* dz, float* ws, hipStream_t s);
 
-// split-K finalisation: out = epilogue(sum_z ws[z]) with the flags of `ep`
-hipError_t launch_splitk_reduce(const float* ws, int splits, long M, long Ncols, float* out,
-                                const Epilogue& ep, hipStream_t s);
 
 // ---- WSP kernels (wsp.hip) ------------------------------------------------
 // u = (-lr)*g; dst = newest + u; ut = first ? u : ut + u   (no FMA contraction)
