@@ -228,8 +228,9 @@ int build_stage(hp_stage* st, const hp_layer* layers, int n_layers) {
                 nd.dgrad = plan_gemm(OP_DGRAD, nd.geo, st->dtype, cus);
                 // fp32: the bias gradient rides along as a column of ones in the weight
                 // gradient; bf16 would round dy there, so it is a separate fp32 sum
-                nd.bias_in_wgrad = L.bias && st->dtype == HP_FP32;
-                nd.wgrad = plan_gemm(OP_WGRAD, nd.geo, st->dtype, cus, nd.bias_in_wgrad ? 1 : 0);
+                nd.wgrad = plan_gemm(OP_WGRAD, nd.geo, st->dtype, cus,
+                                     (L.bias && st->dtype == HP_FP32) ? 1 : 0);
+                nd.bias_in_wgrad = nd.wgrad.bias_col != 0;
                 if (L.bias && !nd.bias_in_wgrad)
                     st->ws_floats = std::max(st->ws_floats,
                                              colsum_ws_floats((long)B * P * Q, L.K));

@@ -41,13 +41,11 @@ constexpr int PAD_V = 4;
 struct TileCfg { int bm, bn, bk, wm, wn; };
 constexpr TileCfg kCfgs[] = {
     {128, 128, 16, 64, 64},    // 0: general
-    {256, 64, 16, 64, 64},     // 1: narrow N (64 output channels)
-    {64, 256, 16, 64, 64},     // 2: narrow M (weight gradients of 64-channel layers, FC)
-    {256, 128, 16, 128, 64},   // 3: large M, 4 waves of 128x64
-    {128, 256, 16, 64, 128},   // 4: large N, 4 waves of 64x128
-    {128, 128, 32, 64, 64},    // 5: general, deeper reduction tile
+    {256, 64, 16, 64, 64},     // 1: narrow N (at most 64 output columns)
+    {64, 256, 16, 64, 64},     // 2: narrow M, N a multiple of 256 or large
+    {64, 128, 16, 64, 64},     // 3: narrow M otherwise (2 waves)
+    {64, 64, 16, 32, 32},      // 4: small M and N (4 waves of 32x32)
 };
-constexpr int kNumCfgs = sizeof(kCfgs) / sizeof(kCfgs[0]);
 
 struct KArgs {
     ConvGeo g;
@@ -503,25 +501,16 @@ KernelRef kref() {
             64 * (c.bm / c.wm) * (c.bn / c.wn)};
 }
 
-// Vector width 1 (channel counts not divisible by 4) only occurs for the first
-// layer of an image stage; it is instantiated for the three basic shapes.
+// Every configuration is instantiated with vector width 4 (channel counts
+// divisible by 4, aligned operands) and 1 (everything else).
 template <int OP, int VW, bool BF>
 KernelRef kref_cfg(int cfg) {
-    if constexpr (VW == 1) {
-        switch (cfg) {
-            case 1: return kref<OP, 1, VW, BF>();
-            case 2: return kref<OP, 2, VW, BF>();
-            default: return kref<OP, 0, VW, BF>();
-        }
-    } else {
-        switch (cfg) {
-            case 1: return kref<OP, 1, VW, BF>();
-            case 2: return kref<OP, 2, VW, BF>();
-            case 3: return kref<OP, 3, VW, BF>();
-            case 4: return kref<OP, 4, VW, BF>();
-            case 5: return kref<OP, 5, VW, BF>();
-            default: return kref<OP, 0, VW, BF>();
-        }
+    switch (cfg) {
+        case 1: return kref<OP, 1, VW, BF>();
+        case 2: return kref<OP, 2, VW, BF>();
+        case 3: return kref<OP, 3, VW, BF>();
+        case 4: return kref<OP, 4, VW, BF>();
+        default: return kref<OP, 0, VW, BF>();
     }
 }
 
@@ -537,13 +526,13 @@ KernelRef kernel_for(int op, int cfg, bool v4, bool bf) {
     return kref_op<OP_WGRAD>(cfg, v4, bf);
 }
 
-// Tile configuration for a contraction of M x N (x Kred).
-int choose_cfg(long M, long N, bool v4) {
-    int c = 0;
-    if (N <= 64 && M > 64) c = 1;
-    else if (M <= 64 && N > 64) c = 2;
-    if (!v4 && c > 2) c = 0;
-    return c;
+// Tile configuration for a contraction of M x N (x Kred): the 128x128 tile
+// unless one side is at most 64, where a tile of that width wastes less.
+int choose_cfg(long M, long N) {
+    if (M <= 64 && N <= 64) return 4;
+    if (N <= 64) return 1;
+    if (M <= 64) return (N % 256 == 0 || N >= 1024) ? 2 : 3;
+    return 0;
 }
 
 }  // namespace
@@ -562,7 +551,18 @@ GemmPlan plan_gemm(int op, const ConvGeo& g, int bf16, int num_cus, int bias_col
         p.Kred = (long)g.N * g.P * g.Q;
     }
     const bool v4 = (op == OP_FWD) ? (g.C % 4 == 0) : (g.C % 4 == 0 && g.K % 4 == 0);
-    p.cfg = choose_cfg(p.M, p.Ncols, v4);
+    p.cfg = choose_cfg(p.M, p.Ncols);
+    if (p.bias_col) {
+        // the bias-gradient column rides along only when it needs no extra tile
+        const long wn = p.Ncols - 1;
+        const int c0 = choose_cfg(p.M, wn);
+        const long bn = kCfgs[c0].bn;
+        if (c0 != p.cfg || (p.Ncols + bn - 1) / bn != (wn + bn - 1) / bn) {
+            p.bias_col = 0;
+            p.Ncols = wn;
+            p.cfg = c0;
+        }
+    }
     const TileCfg& c = kCfgs[p.cfg];
     const long tiles = ((p.M + c.bm - 1) / c.bm) * ((p.Ncols + c.bn - 1) / c.bn);
     const long ktiles = (p.Kred + c.bk - 1) / c.bk;
@@ -623,7 +623,6 @@ hipError_t launch_gemm(const GemmPlan& plan, const ConvGeo& g, const float* a, c
     // operand bases 16-byte aligned
     bool v4 = (plan.op == OP_FWD) ? (g.C % 4 == 0) : (g.C % 4 == 0 && g.K % 4 == 0);
     v4 = v4 && ((((uintptr_t)a) | ((uintptr_t)b)) & 15) == 0;
-    if (!v4 && plan.cfg > 2) return hipErrorInvalidValue;   // planned for aligned operands
     KernelRef kr = kernel_for(plan.op, plan.cfg, v4, plan.bf16 != 0);
     void* kargs[] = {&k};
     hipError_t e = hipLaunchKernel(kr.fn, dim3(plan.nwg), dim3(kr.nt), kargs, 0, s);

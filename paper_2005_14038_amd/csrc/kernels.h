@@ -35,7 +35,8 @@ struct GemmPlan {
 };
 
 // bias_col (OP_WGRAD only): append a column of ones to the gathered input so
-// that the last output column is sum_m dy[m][k], the bias gradient.
+// that the last output column is sum_m dy[m][k], the bias gradient.  The plan
+// keeps it only when it costs no extra tile; plan.bias_col says whether it did.
 GemmPlan plan_gemm(int op, const ConvGeo& g, int bf16, int num_cus, int bias_col = 0);
 
 // epilogue flags
