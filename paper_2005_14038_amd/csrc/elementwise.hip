@@ -129,9 +129,11 @@ __global__ void maxpool_bwd_kernel(const float* __restrict__ x, const float* __r
 // max-pool backward for non-overlapping windows (window = stride, no padding,
 // windows tile the input exactly): one thread per output element writes its
 // whole window -- dy at the first maximum, zero elsewhere.
+template <int RT>   // RT > 0: window size fixed at compile time; 0: runtime R
 __global__ void maxpool_bwd_tiled_kernel(const float* __restrict__ x, const float* __restrict__ dy,
-                                         float* __restrict__ dx, int N, int H, int W, int C, int R,
+                                         float* __restrict__ dx, int N, int H, int W, int C, int Rr,
                                          int P, int Q, int acc, const float* __restrict__ mask) {
+    const int R = RT > 0 ? RT : Rr;
     const size_t total = (size_t)N * P * Q * C;
     for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
          i += (size_t)gridDim.x * blockDim.x) {
@@ -141,21 +143,39 @@ __global__ void maxpool_bwd_tiled_kernel(const float* __restrict__ x, const floa
         int p = (int)(t % P);
         int n = (int)(t / P);
         const size_t base = (((size_t)n * H + p * R) * W + q * R) * C + c;
-        int best = 0;
-        float m = x[base];
-        for (int r = 0; r < R; ++r)
-            for (int s = 0; s < R; ++s) {
-                float v = x[base + ((size_t)r * W + s) * C];
-                if (v > m) { m = v; best = r * R + s; }
-            }
         const float g = dy[i];
-        for (int r = 0; r < R; ++r)
-            for (int s = 0; s < R; ++s) {
-                size_t j = base + ((size_t)r * W + s) * C;
-                float v = (r * R + s == best) ? g : 0.f;
-                if (mask && !(mask[j] > 0.f)) v = 0.f;
-                dx[j] = acc ? dx[j] + v : v;
+        if constexpr (RT > 0) {
+            // taps kept in registers; when pooling a ReLU output the taps are the mask
+            float v[RT * RT];
+            int best = 0;
+#pragma unroll
+            for (int k = 0; k < RT * RT; ++k) {
+                v[k] = x[base + ((size_t)(k / RT) * W + k % RT) * C];
+                if (v[k] > v[best]) best = k;
             }
+#pragma unroll
+            for (int k = 0; k < RT * RT; ++k) {
+                size_t j = base + ((size_t)(k / RT) * W + k % RT) * C;
+                float o = (k == best) ? g : 0.f;
+                if (mask && !((mask == x ? v[k] : mask[j]) > 0.f)) o = 0.f;
+                dx[j] = acc ? dx[j] + o : o;
+            }
+        } else {
+            int best = 0;
+            float m = x[base];
+            for (int r = 0; r < R; ++r)
+                for (int s = 0; s < R; ++s) {
+                    float v = x[base + ((size_t)r * W + s) * C];
+                    if (v > m) { m = v; best = r * R + s; }
+                }
+            for (int r = 0; r < R; ++r)
+                for (int s = 0; s < R; ++s) {
+                    size_t j = base + ((size_t)r * W + s) * C;
+                    float o = (r * R + s == best) ? g : 0.f;
+                    if (mask && !(mask[j] > 0.f)) o = 0.f;
+                    dx[j] = acc ? dx[j] + o : o;
+                }
+        }
     }
 }
 
@@ -190,7 +210,7 @@ __global__ void gap_bwd_kernel(const float* __restrict__ dy, float* __restrict__
 // 256 threads = 64 channels x 4 row lanes; the 4 row-lane sums are combined
 // in LDS in a fixed order.
 constexpr int CS_CH = 64;
-constexpr int CS_RB = 1024;
+constexpr int CS_RB = 256;
 
 inline int cs_row_blocks(long M) { return (int)((M + CS_RB - 1) / CS_RB); }
 
@@ -390,8 +410,12 @@ hipError_t launch_maxpool_bwd(const float* x, const float* dy, float* dx, int N,
                               const float* mask, hipStream_t s) {
     if (R == S && R == st && pad == 0 && P * st == H && Q * st == W) {
         size_t n = (size_t)N * P * Q * C;
-        hipLaunchKernelGGL(maxpool_bwd_tiled_kernel, dim3(ew_blocks(n)), dim3(EW_THREADS), 0, s, x,
-                           dy, dx, N, H, W, C, R, P, Q, accumulate, mask);
+        if (R == 2)
+            hipLaunchKernelGGL(maxpool_bwd_tiled_kernel<2>, dim3(ew_blocks(n)), dim3(EW_THREADS), 0,
+                               s, x, dy, dx, N, H, W, C, R, P, Q, accumulate, mask);
+        else
+            hipLaunchKernelGGL(maxpool_bwd_tiled_kernel<0>, dim3(ew_blocks(n)), dim3(EW_THREADS), 0,
+                               s, x, dy, dx, N, H, W, C, R, P, Q, accumulate, mask);
         return hipGetLastError();
     }
     size_t n = (size_t)N * H * W * C;

@@ -468,24 +468,35 @@ igemm_splitk_reduce_kernel(KArgs args, int BM, int BN) {
     }
 }
 
-// The same reduction for few splits: one thread per element of the cut tiles
-// (grid-stride), adding the splits in order.
+// The same reduction for few splits: one thread per 4 consecutive elements
+// of the cut tiles (one float4 per split), adding the splits in order.
 __global__ void __launch_bounds__(256) igemm_cut_reduce_kernel(KArgs args, int BM, int BN) {
-    const long tile_elems = (long)BM * BN;
-    const long total = (long)(args.tiles_m * args.tiles_n - args.tfull) * tile_elems;
+    const int tile_elems = BM * BN;
+    const int per_tile = tile_elems / 4;
+    const long total = (long)(args.tiles_m * args.tiles_n - args.tfull) * per_tile;
     for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < total;
          i += (long)gridDim.x * blockDim.x) {
-        const int rt = (int)(i / tile_elems);
-        const int e = (int)(i - rt * tile_elems);
+        const int rt = (int)(i / per_tile);
+        const int e = (int)(i - (long)rt * per_tile) * 4;
         const int tile = args.tfull + rt;
         const long row = (long)(tile / args.tiles_n) * BM + e / BN;
-        const long col = (long)(tile % args.tiles_n) * BN + e % BN;
-        if (row >= args.M || col >= args.Ncols) continue;
-        const float* src = args.ws + (long)rt * args.splits * tile_elems + e;
-        float acc = 0.f;
-        for (int z = 0; z < args.splits; ++z) acc += src[z * tile_elems];
-        float* dst = out_ptr(args.out, args.bias_out, row, col, args.Ncols, args.epi);
-        *dst = epilogue(acc, row, col, args.Ncols, args.epi, args.bias, args.mask, dst);
+        const long col0 = (long)(tile % args.tiles_n) * BN + e % BN;
+        if (row >= args.M || col0 >= args.Ncols) continue;
+        const float4* src =
+            reinterpret_cast<const float4*>(args.ws + (long)rt * args.splits * tile_elems + e);
+        float4 acc = src[0];
+        for (int z = 1; z < args.splits; ++z) {
+            const float4 v = src[(long)z * per_tile];
+            acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
+        }
+        const float a4[4] = {acc.x, acc.y, acc.z, acc.w};
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const long col = col0 + j;
+            if (col >= args.Ncols) break;
+            float* dst = out_ptr(args.out, args.bias_out, row, col, args.Ncols, args.epi);
+            *dst = epilogue(a4[j], row, col, args.Ncols, args.epi, args.bias, args.mask, dst);
+        }
     }
 }
 
@@ -553,11 +564,12 @@ GemmPlan plan_gemm(int op, const ConvGeo& g, int bf16, int num_cus, int bias_col
     const bool v4 = (op == OP_FWD) ? (g.C % 4 == 0) : (g.C % 4 == 0 && g.K % 4 == 0);
     p.cfg = choose_cfg(p.M, p.Ncols);
     if (p.bias_col) {
-        // the bias-gradient column rides along only when it needs no extra tile
+        // the bias-gradient column rides along unless it adds more than 10% of
+        // tiles (then a separate column sum of dy is cheaper)
         const long wn = p.Ncols - 1;
         const int c0 = choose_cfg(p.M, wn);
         const long bn = kCfgs[c0].bn;
-        if (c0 != p.cfg || (p.Ncols + bn - 1) / bn != (wn + bn - 1) / bn) {
+        if (c0 != p.cfg || 10 * ((p.Ncols + bn - 1) / bn) > 11 * ((wn + bn - 1) / bn)) {
             p.bias_col = 0;
             p.Ncols = wn;
             p.cfg = c0;
@@ -629,8 +641,8 @@ hipError_t launch_gemm(const GemmPlan& plan, const ConvGeo& g, const float* a, c
     const int cut = k.tiles_m * k.tiles_n - plan.tfull;
     if (e != hipSuccess || cut == 0) return e;
     if (plan.splits <= SK_LANES) {
-        const long total = (long)cut * c.bm * c.bn;
-        const int blocks = (int)std::min<long>((total + 255) / 256, 8192);
+        const long total = (long)cut * c.bm * c.bn / 4;
+        const int blocks = (int)std::min<long>((total + 255) / 256, 16384);
         hipLaunchKernelGGL(igemm_cut_reduce_kernel, dim3(blocks), dim3(256), 0, s, k, c.bm, c.bn);
     } else {
         hipLaunchKernelGGL(igemm_splitk_reduce_kernel, dim3(cut * (c.bm * c.bn / SK_EL)),

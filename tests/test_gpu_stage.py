@@ -32,14 +32,14 @@ def norm_err(a, r):
     return float(np.linalg.norm(a - r) / np.linalg.norm(r))
 
 
-def _self_sensitivity(net, w, x, lab, dy, need_dx):
-    """How far the oracle's own bf16-mode results move when the weights are
-    perturbed by 1e-7 relative (the size of fp32 round-off): a floor for any
-    implementation's distance to the oracle."""
-    r0 = run_oracle(net, w, x, lab, dy, need_dx, bf16=True)
+def _self_sensitivity(net, w, x, lab, dy, need_dx, bf16, rel):
+    """How far the oracle's own results move when the weights are perturbed by
+    `rel` relative: a floor for any implementation's distance to the oracle
+    whose own round-off is of that size."""
+    r0 = run_oracle(net, w, x, lab, dy, need_dx, bf16=bf16)
     rng = np.random.default_rng(1)
-    w1 = np.asarray(w, np.float64) * (1 + 1e-7 * rng.standard_normal(len(w)))
-    r1 = run_oracle(net, w1, x, lab, dy, need_dx, bf16=True)
+    w1 = np.asarray(w, np.float64) * (1 + rel * rng.standard_normal(len(w)))
+    r1 = run_oracle(net, w1, x, lab, dy, need_dx, bf16=bf16)
     out = {"y": norm_err(r1["y"], r0["y"]), "grad": norm_err(r1["grad"], r0["grad"])}
     if need_dx:
         out["dx"] = norm_err(r1["dx"], r0["dx"])
@@ -59,12 +59,18 @@ def _check(name, dtype):
     if dtype == "fp32":
         if net.has_loss:
             assert abs(g["loss"] - r["loss"]) <= FP32_TOL * abs(r["loss"])
-        for _, what, a, b in pairs:
+        # an ill-conditioned stage is judged normwise, against max(1e-3, 2x the
+        # oracle's own movement under a 1e-5 weight perturbation, the size of
+        # the per-layer fp32 accumulation error)
+        sens = None if elementwise else _self_sensitivity(net, w, x, lab, dy, need_dx, False, 1e-5)
+        for key, what, a, b in pairs:
             if elementwise:
                 assert_close(a, b, FP32_TOL, f"{name} {what}")
             else:
                 e = norm_err(a, b)
-                assert e <= FP32_TOL, f"{name} {what}: normwise relative error {e:.3e}"
+                bound = max(FP32_TOL, 2 * sens[key])
+                assert e <= bound, (f"{name} {what}: normwise relative error {e:.3e} > "
+                                    f"{bound:.3e} (oracle self-sensitivity {sens[key]:.3e})")
     else:
         # bf16: both sides round the same kind of operand, but the values being
         # rounded differ by fp32-vs-fp64 accumulation, so a few land on the other
@@ -73,7 +79,7 @@ def _check(name, dtype):
         # Whole stages are therefore judged normwise against max(2e-2, 2x the
         # oracle's own sensitivity); element-wise max relative error is checked
         # per layer, where the inputs are identical.
-        sens = _self_sensitivity(net, w, x, lab, dy, need_dx)
+        sens = _self_sensitivity(net, w, x, lab, dy, need_dx, True, 1e-7)
         if net.has_loss:
             assert abs(g["loss"] - r["loss"]) <= BF16_TOL * abs(r["loss"])
         for key, what, a, b in pairs:
