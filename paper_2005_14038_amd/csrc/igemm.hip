@@ -1,7 +1,7 @@
 // Implicit-GEMM convolution / FC contractions on CDNA4 MFMA (gfx950).
 //
-// One kernel template covers the three contractions of a convolution layer
-// (an FC layer is a 1x1 convolution on a 1x1 map):
+// One kernel template per precision covers the three contractions of a
+// convolution layer (an FC layer is a 1x1 convolution on a 1x1 map):
 //
 //   forward  out[m = (n,p,q)][k]     = sum_{(r,s,c)} x[n, p*st-pad+r, q*st-pad+s, c] w[k,r,s,c]
 //   dgrad    out[m = (n,h,w)][c]     = sum_{(r,s,k)} dy[n, (h+pad-r)/st, (w+pad-s)/st, k] w[k,r,s,c]
@@ -9,17 +9,20 @@
 //   wgrad    out[k][j = (r,s,c)]     = sum_{(n,p,q)} dy[n,p,q,k] x[n, p*st-pad+r, q*st-pad+s, c]
 //
 // The operands are gathered straight from the NHWC activations and the KRSC
-// weights ("implicit" im2col: nothing is materialised), staged through LDS in
-// [BK][BM] / [BK][BN] tiles (the GEMM's row index contiguous), double
-// buffered, and fed to v_mfma_f32_32x32x2_f32.  256 threads = 4 wave64s, each
-// owning a 64x64 block of the output as 2x2 MFMA 32x32 tiles.
+// weights ("implicit" im2col: nothing is materialised), staged through LDS,
+// double buffered, and fed to the matrix cores; each wave64 owns a WM x WN
+// block of the output as a grid of MFMA 32x32 tiles.
+//
+//   fp32: v_mfma_f32_32x32x2_f32; LDS tiles [BK][rows] (row index contiguous).
+//   bf16: every operand is rounded to bfloat16 (RNE) as it is staged; LDS
+//         tiles [rows][32 k] of bf16 (reduction index contiguous) feed
+//         v_mfma_f32_32x32x16_bf16.  Products of bf16 values are exact in fp32
+//         and the accumulation stays fp32.
 //
 // Long reductions (weight gradients reduce over N*P*Q, FC layers over their
-// fan-in) are split over blockIdx.y; each split writes a partial tile to a
+// fan-in) are cut into chunks; each chunk writes a partial tile to a
 // workspace and a second kernel adds the partials in a fixed order, so results
-// are deterministic.  In bf16 mode every operand is rounded to bfloat16 (RNE)
-// when it is staged; products of bf16 values are exact in fp32 and the
-// accumulation stays fp32.
+// are deterministic.
 #include "kernels.h"
 
 namespace hp {
@@ -91,10 +94,79 @@ __device__ __forceinline__ float round_bf16(float x) {
     return __uint_as_float(u);
 }
 
-template <bool BF>
-__device__ __forceinline__ float cvt(float x) {
-    if constexpr (BF) return round_bf16(x);
-    else return x;
+// Two floats rounded to bf16, packed low element first (LDS byte order).
+__device__ __forceinline__ unsigned pack_bf16(float lo, float hi) {
+    return (__float_as_uint(round_bf16(lo)) >> 16) | (__float_as_uint(round_bf16(hi)) & 0xFFFF0000u);
+}
+
+// Work assignment.  The first `tfull` workgroups each compute one whole
+// output tile (whole rounds of the resident workgroups); the rest cut each
+// remaining tile's reduction into `splits` chunks, so that the last round is
+// as full as the others, and leave partial tiles for the reduce kernels.
+// XCD-aware: consecutive workgroup ids are dealt round-robin to the 8 XCDs;
+// each XCD gets a contiguous run of whole tiles (n fastest), so tiles sharing
+// A rows share that XCD's L2.
+struct Work {
+    int tile, z;
+    bool partial;
+    long m0, n0, kbeg, kend;
+};
+
+template <int BM, int BN>
+__device__ __forceinline__ Work decode_work(const KArgs& args) {
+    Work w;
+    int bid = blockIdx.x;
+    w.z = 0;
+    w.partial = bid >= args.tfull;
+    if (!w.partial) {
+        if ((args.tfull & 7) == 0) bid = (bid & 7) * (args.tfull >> 3) + (bid >> 3);
+        w.tile = bid;
+    } else {
+        const int r = bid - args.tfull;
+        w.tile = args.tfull + r / args.splits;
+        w.z = r - (w.tile - args.tfull) * args.splits;
+    }
+    w.m0 = (long)(w.tile / args.tiles_n) * BM;
+    w.n0 = (long)(w.tile % args.tiles_n) * BN;
+    w.kbeg = w.partial ? (long)w.z * args.kchunk : 0;
+    w.kend = w.partial ? min(w.kbeg + (long)args.kchunk, args.Kred) : args.Kred;
+    return w;
+}
+
+// Writes a wave's accumulators: acc[i][j][v] holds
+// out[m0 + wm + 32i + 8(v/4) + 4(lane/32) + v%4][n0 + wn + 32j + lane%32]
+// (the output layout of the 32x32 MFMAs), through the epilogue, or raw into
+// the workspace slot of a cut tile.
+template <int BM, int BN, int TM, int TN>
+__device__ __forceinline__ void store_tile(const KArgs& args, const Work& w,
+                                           const floatx16 (&acc)[TM][TN], int wm, int wn,
+                                           int lane) {
+    const int lr = lane & 31, lk = lane >> 5;
+    float* pslot = w.partial
+                       ? args.ws + ((long)(w.tile - args.tfull) * args.splits + w.z) * (BM * BN)
+                       : nullptr;
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+        const int lcol = wn + 32 * j + lr;
+        const long col = w.n0 + lcol;
+        if (col >= args.Ncols) continue;
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const int lrow = wm + 32 * i + 8 * (v >> 2) + 4 * lk + (v & 3);
+                const long row = w.m0 + lrow;
+                if (row >= args.M) continue;
+                float val = acc[i][j][v];
+                if (w.partial) {
+                    pslot[lrow * BN + lcol] = val;
+                } else {
+                    float* dst = out_ptr(args.out, args.bias_out, row, col, args.Ncols, args.epi);
+                    *dst = epilogue(val, row, col, args.Ncols, args.epi, args.bias, args.mask, dst);
+                }
+            }
+        }
+    }
 }
 
 // ---- operand gathers -------------------------------------------------------
@@ -115,7 +187,7 @@ __device__ __forceinline__ void load_vec(const float* p, bool ok, float* v) {
     }
 }
 
-template <int OP, int BM, int BN, int BK, int WM, int WN, int VW, bool BF>
+template <int OP, int BM, int BN, int BK, int WM, int WN, int VW>
 __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_kernel(KArgs args) {
     constexpr int NT = 64 * (BM / WM) * (BN / WN);
     constexpr int TM = WM / 32, TN = WN / 32;  // MFMA tiles per wave
@@ -133,30 +205,8 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_kernel(KA
     const int wm = (wave / WAVES_N) * WM;
     const int wn = (wave % WAVES_N) * WN;
 
-    // Work assignment.  The first `tfull` workgroups each compute one whole
-    // output tile (whole rounds of the resident workgroups); the rest cut each
-    // remaining tile's reduction into `splits` chunks, so that the last round
-    // is as full as the others, and leave partial tiles for
-    // igemm_splitk_reduce_kernel.  XCD-aware: consecutive workgroup ids are
-    // dealt round-robin to the 8 XCDs; each XCD gets a contiguous run of whole
-    // tiles (n fastest), so tiles sharing A rows share that XCD's L2.
-    int bid = blockIdx.x;
-    int tile, z = 0;
-    const bool partial = bid >= args.tfull;
-    if (!partial) {
-        if ((args.tfull & 7) == 0) bid = (bid & 7) * (args.tfull >> 3) + (bid >> 3);
-        tile = bid;
-    } else {
-        const int r = bid - args.tfull;
-        tile = args.tfull + r / args.splits;
-        z = r - (tile - args.tfull) * args.splits;
-    }
-    const int tm = tile / args.tiles_n;
-    const int tn = tile % args.tiles_n;
-    const long m0 = (long)tm * BM;
-    const long n0 = (long)tn * BN;
-    const long kbeg = partial ? (long)z * args.kchunk : 0;
-    const long kend = partial ? min(kbeg + (long)args.kchunk, args.Kred) : args.Kred;
+    const Work wk = decode_work<BM, BN>(args);
+    const long m0 = wk.m0, n0 = wk.n0, kbeg = wk.kbeg, kend = wk.kend;
     const int ktiles = (int)((kend - kbeg + BK - 1) / BK);
 
     // ---- per-thread staging coordinates ----
@@ -349,12 +399,12 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_kernel(KA
             if constexpr (A_KMAJ) {
                 int row = (t + i * NT) / KVPR;
 #pragma unroll
-                for (int j = 0; j < VW; ++j) As[(akv + j) * LDA + row] = cvt<BF>(areg[i][j]);
+                for (int j = 0; j < VW; ++j) As[(akv + j) * LDA + row] = areg[i][j];
             } else {
                 int kr = (t + i * NT) / AVPR;
                 int col = ((t + i * NT) % AVPR) * VW;
 #pragma unroll
-                for (int j = 0; j < VW; ++j) As[kr * LDA + col + j] = cvt<BF>(areg[i][j]);
+                for (int j = 0; j < VW; ++j) As[kr * LDA + col + j] = areg[i][j];
             }
         }
 #pragma unroll
@@ -362,12 +412,12 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_kernel(KA
             if constexpr (B_KMAJ) {
                 int row = (t + i * NT) / KVPR;
 #pragma unroll
-                for (int j = 0; j < VW; ++j) Bs[(bkv + j) * LDB + row] = cvt<BF>(breg[i][j]);
+                for (int j = 0; j < VW; ++j) Bs[(bkv + j) * LDB + row] = breg[i][j];
             } else {
                 int kr = (t + i * NT) / BVPR;
                 int col = ((t + i * NT) % BVPR) * VW;
 #pragma unroll
-                for (int j = 0; j < VW; ++j) Bs[kr * LDB + col + j] = cvt<BF>(breg[i][j]);
+                for (int j = 0; j < VW; ++j) Bs[kr * LDB + col + j] = breg[i][j];
             }
         }
     };
@@ -411,33 +461,362 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_kernel(KA
         __syncthreads();
     }
 
-    // ---- epilogue ----
-    // acc[i][j][v] holds out[m0 + wm + 32i + 8(v/4) + 4(lane/32) + v%4][n0 + wn + 32j + lane%32]
-    float* pslot = partial ? args.ws + ((long)(tile - args.tfull) * args.splits + z) * (BM * BN)
-                           : nullptr;
+    store_tile<BM, BN, TM, TN>(args, wk, acc, wm, wn, lane);
+}
+
+// ---- bf16 kernel ------------------------------------------------------------
+// The same three contractions on v_mfma_f32_32x32x16_bf16.  Operands are
+// gathered in fp32 exactly as above, rounded to bf16 and staged row-major in
+// LDS with the reduction index contiguous: [rows][LDH] bf16, BKH = 32 k per
+// tile, rows padded to 80 bytes so that the 16-byte fragment reads of 8
+// consecutive rows cover all banks once.  A lane's MFMA operand is 8
+// consecutive k of one row (row = lane % 32, k = 8 (lane / 32) .. + 7; both
+// operands use the same k order, so the contraction is the same whatever
+// order the hardware takes the k in).
+//
+// k-major operands (gathered rows, reduction index contiguous in memory) are
+// staged in groups of 4 consecutive k of one row (one 8-byte LDS store);
+// m-major operands (reduction index = memory row) in 4 x 4 blocks, 4
+// reduction rows of 4 consecutive columns, transposed in registers.
+constexpr int BKH = 32;
+constexpr int LDH = BKH + 8;
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef unsigned uintx4 __attribute__((ext_vector_type(4)));
+typedef unsigned uintx2 __attribute__((ext_vector_type(2)));
+
+template <int OP, int BM, int BN, int WM, int WN, int VW>
+__global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_bf16_kernel(KArgs args) {
+    constexpr int NT = 64 * (BM / WM) * (BN / WN);
+    constexpr int TM = WM / 32, TN = WN / 32;
+    constexpr bool A_KMAJ = (OP != OP_WGRAD);
+    constexpr bool B_KMAJ = (OP == OP_FWD);
+    constexpr int WAVES_N = BN / WN;
+    constexpr int KG = BKH / 4;                  // 4-k groups per k-major row
+    constexpr int GA = BM * KG / NT;             // k-major groups per thread
+    constexpr int GB = BN * KG / NT;
+    constexpr int CGA = BM / 4, CGB = BN / 4;    // column groups of an m-major operand
+    constexpr int PA = (2 * BM + NT - 1) / NT;   // m-major 4x4 blocks per thread
+    constexpr int PB = (2 * BN + NT - 1) / NT;
+    constexpr int NA = A_KMAJ ? GA : 4 * PA;     // 4-vectors held per thread
+    constexpr int NB = B_KMAJ ? GB : 4 * PB;
+    constexpr int CV = VW == 4 ? 1 : 4;          // separately addressed columns of a 4-vector
+    static_assert(GA >= 1 && GB >= 1 && NT % KG == 0 && NT % CGA == 0 && NT % CGB == 0,
+                  "tile shape");
+    __shared__ __attribute__((aligned(16))) unsigned short smem[2 * (BM + BN) * LDH];
+
+    const ConvGeo& g = args.g;
+    const int t = threadIdx.x;
+    const int lane = t & 63;
+    const int wave = t >> 6;
+    const int wm = (wave / WAVES_N) * WM;
+    const int wn = (wave % WAVES_N) * WN;
+    const Work wk = decode_work<BM, BN>(args);
+    const int ktiles = (int)((wk.kend - wk.kbeg + BKH - 1) / BKH);
+    const int kg = (t % KG) * 4;                                // k-major: k offset of the group
+    const bool a_act = A_KMAJ || 2 * BM >= NT || t < 2 * BM;    // m-major: thread owns a block
+    const bool b_act = B_KMAJ || 2 * BN >= NT || t < 2 * BN;
+
+    // ---- per-thread staging coordinates ----
+    int arow_base[GA], arow_h[GA], arow_w[GA];
+    bool arow_ok[GA];
+    long acol = 0;
+    if constexpr (A_KMAJ) {
 #pragma unroll
-    for (int j = 0; j < TN; ++j) {
-        const int lcol = wn + 32 * j + lr;
-        const long col = n0 + lcol;
-        if (col >= args.Ncols) continue;
+        for (int i = 0; i < GA; ++i) {
+            const long m = wk.m0 + t / KG + i * (NT / KG);
+            arow_ok[i] = m < args.M;
+            const long mm = arow_ok[i] ? m : 0;
+            if constexpr (OP == OP_FWD) {
+                int q = (int)(mm % g.Q); long tt = mm / g.Q;
+                int p = (int)(tt % g.P); int n = (int)(tt / g.P);
+                arow_base[i] = n * g.H * g.W * g.C;
+                arow_h[i] = p * g.st - g.pad;
+                arow_w[i] = q * g.st - g.pad;
+            } else {  // DGRAD: m = (n, h, w)
+                int w = (int)(mm % g.W); long tt = mm / g.W;
+                int h = (int)(tt % g.H); int n = (int)(tt / g.H);
+                arow_base[i] = n * g.P * g.Q * g.K;
+                arow_h[i] = h + g.pad;
+                arow_w[i] = w + g.pad;
+            }
+        }
+    } else {
+        acol = wk.m0 + (t % CGA) * 4;           // WGRAD: output channels acol .. +3
+    }
+    long brow_n[GB];
+    bool brow_ok[GB];
+    long bcol = 0;
+    int bcol_r[CV], bcol_s[CV], bcol_c[CV];
+    bool bcol_ok[CV], bcol_ones[CV];
+    if constexpr (B_KMAJ) {
 #pragma unroll
-        for (int i = 0; i < TM; ++i) {
+        for (int i = 0; i < GB; ++i) {
+            const long n = wk.n0 + t / KG + i * (NT / KG);
+            brow_ok[i] = n < args.Ncols;
+            brow_n[i] = brow_ok[i] ? n : 0;
+        }
+    } else {
+        bcol = wk.n0 + (t % CGB) * 4;
 #pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                const int lrow = wm + 32 * i + 8 * (v >> 2) + 4 * lk + (v & 3);
-                const long row = m0 + lrow;
-                if (row >= args.M) continue;
-                float val = acc[i][j][v];
-                if (partial) {
-                    pslot[lrow * BN + lcol] = val;
-                } else {
-                    float* dst = out_ptr(args.out, args.bias_out, row, col, args.Ncols, args.epi);
-                    *dst = epilogue(val, row, col, args.Ncols, args.epi, args.bias, args.mask, dst);
-                }
+        for (int c = 0; c < CV; ++c) {
+            const long col = bcol + c;
+            bcol_ok[c] = col < args.Ncols;
+            bcol_ones[c] = false;
+            if (OP == OP_WGRAD && (args.epi & EPI_BIASCOL) && col == args.Ncols - 1) {
+                bcol_ones[c] = true;       // the appended column of ones (bias gradient)
+                bcol_ok[c] = false;
+            }
+            const long cc = bcol_ok[c] ? col : 0;
+            if constexpr (OP == OP_WGRAD) {      // col = (r, s, c)
+                bcol_c[c] = (int)(cc % g.C); long tt = cc / g.C;
+                bcol_s[c] = (int)(tt % g.S); bcol_r[c] = (int)(tt / g.S);
+            } else {                              // DGRAD: col = c
+                bcol_c[c] = (int)cc;
+                bcol_r[c] = bcol_s[c] = 0;
             }
         }
     }
+
+    float areg[NA][4];
+    float breg[NB][4];
+
+    // Staging of one reduction tile [k0, k0 + BKH); as in the fp32 kernel the
+    // decomposition of k0 is uniform and each thread steps from it.
+    auto gload = [&](int kt) {
+        const int k0 = (int)(wk.kbeg + (long)kt * BKH);
+        const int kend_i = (int)wk.kend;
+        if constexpr (OP == OP_FWD || OP == OP_DGRAD) {
+            const int CC = (OP == OP_FWD) ? g.C : g.K;       // contiguous axis of a tap
+            const int rs0 = k0 / CC;
+            const int c0 = k0 - rs0 * CC;
+            const int r0 = rs0 / g.S;
+            const int s0 = rs0 - r0 * g.S;
+            // ---- A: k-major gathered rows, k = k0 + kg .. + 3 ----
+            {
+                int c = c0 + kg, r = r0, sx = s0;
+                while (c >= CC) { c -= CC; if (++sx == g.S) { sx = 0; ++r; } }
+#pragma unroll
+                for (int j = 0; j < CV; ++j) {
+                    if (j > 0 && ++c == CC) { c = 0; if (++sx == g.S) { sx = 0; ++r; } }
+                    const bool kin = k0 + kg + j < kend_i;
+#pragma unroll
+                    for (int i = 0; i < GA; ++i) {
+                        bool ok;
+                        long off;
+                        if constexpr (OP == OP_FWD) {
+                            const int h = arow_h[i] + r, w = arow_w[i] + sx;
+                            ok = arow_ok[i] && kin && (unsigned)h < (unsigned)g.H &&
+                                 (unsigned)w < (unsigned)g.W;
+                            off = arow_base[i] + ((long)h * g.W + w) * g.C + c;
+                        } else {
+                            const int tp = arow_h[i] - r, tq = arow_w[i] - sx;
+                            int p = tp, q = tq;
+                            bool on_grid = true;
+                            if (g.st != 1) {        // (uniform branch) strided: exact taps only
+                                p = tp / g.st;
+                                q = tq / g.st;
+                                on_grid = p * g.st == tp && q * g.st == tq;
+                            }
+                            ok = arow_ok[i] && kin && tp >= 0 && tq >= 0 && on_grid &&
+                                 p < g.P && q < g.Q;
+                            off = arow_base[i] + ((long)p * g.Q + q) * g.K + c;
+                        }
+                        const float* ptr = args.a + (ok ? off : 0);
+                        if constexpr (VW == 4) load_vec<4>(ptr, ok, areg[i]);
+                        else areg[i][j] = ok ? *ptr : 0.f;
+                    }
+                }
+            }
+            // ---- B ----
+            if constexpr (OP == OP_FWD) {                     // weight rows, k-major
+#pragma unroll
+                for (int j = 0; j < CV; ++j) {
+                    const int kk = k0 + kg + j;
+#pragma unroll
+                    for (int i = 0; i < GB; ++i) {
+                        const bool ok = brow_ok[i] && kk < kend_i;
+                        const float* ptr = args.b + (ok ? (brow_n[i] * args.Kred + kk) : 0);
+                        if constexpr (VW == 4) load_vec<4>(ptr, ok, breg[i]);
+                        else breg[i][j] = ok ? *ptr : 0.f;
+                    }
+                }
+            } else if (b_act) {     // B[kk = (r,s,k)][c] = w[k][r][s][c], m-major blocks
+#pragma unroll
+                for (int i = 0; i < PB; ++i) {
+                    const int kq = ((t + i * NT) / CGB) * 4;
+                    int k = c0 + kq, r = r0, sx = s0;
+                    while (k >= CC) { k -= CC; if (++sx == g.S) { sx = 0; ++r; } }
+#pragma unroll
+                    for (int jr = 0; jr < 4; ++jr) {
+                        if (jr > 0 && ++k == CC) { k = 0; if (++sx == g.S) { sx = 0; ++r; } }
+                        const bool kin = k0 + kq + jr < kend_i;
+                        const long base = (((long)k * g.R + r) * g.S + sx) * g.C;
+#pragma unroll
+                        for (int c = 0; c < CV; ++c) {
+                            const bool ok = bcol_ok[c] && kin;
+                            const float* ptr = args.b + (ok ? base + bcol_c[c] : 0);
+                            if constexpr (VW == 4) load_vec<4>(ptr, ok, breg[4 * i + jr]);
+                            else breg[4 * i + jr][c] = ok ? *ptr : 0.f;
+                        }
+                    }
+                }
+            }
+        } else {
+            // ---- A: A[kk = m'][m = k-out] = dy[m'][k], m-major blocks ----
+            if (a_act) {
+#pragma unroll
+                for (int i = 0; i < PA; ++i) {
+                    const int kq = ((t + i * NT) / CGA) * 4;
+#pragma unroll
+                    for (int jr = 0; jr < 4; ++jr) {
+                        const int kk = k0 + kq + jr;
+                        const bool kin = kk < kend_i;
+                        const float* row = args.b + (long)kk * g.K + acol;
+                        if constexpr (VW == 4) {
+                            const bool ok = kin && acol < args.M;
+                            load_vec<4>(ok ? row : args.b, ok, areg[4 * i + jr]);
+                        } else {
+#pragma unroll
+                            for (int c = 0; c < 4; ++c) {
+                                const bool ok = kin && acol + c < args.M;
+                                areg[4 * i + jr][c] = ok ? row[c] : 0.f;
+                            }
+                        }
+                    }
+                }
+            }
+            // ---- B: B[kk = (n,p,q)][j = (r,s,c)] = x[n, p*st-pad+r, q*st-pad+s, c] ----
+            if (b_act) {
+                const int q0 = k0 % g.Q;
+                const int t0 = k0 / g.Q;
+                const int p0 = t0 % g.P;
+                const int n0i = t0 / g.P;
+#pragma unroll
+                for (int i = 0; i < PB; ++i) {
+                    const int kq = ((t + i * NT) / CGB) * 4;
+                    int q = q0 + kq, p = p0, n = n0i;
+                    while (q >= g.Q) { q -= g.Q; if (++p == g.P) { p = 0; ++n; } }
+#pragma unroll
+                    for (int jr = 0; jr < 4; ++jr) {
+                        if (jr > 0 && ++q == g.Q) { q = 0; if (++p == g.P) { p = 0; ++n; } }
+                        const bool kin = k0 + kq + jr < kend_i;
+#pragma unroll
+                        for (int c = 0; c < CV; ++c) {
+                            const int h = p * g.st - g.pad + bcol_r[c];
+                            const int w = q * g.st - g.pad + bcol_s[c];
+                            const bool ok = bcol_ok[c] && kin && (unsigned)h < (unsigned)g.H &&
+                                            (unsigned)w < (unsigned)g.W;
+                            const float* ptr =
+                                args.a +
+                                (ok ? ((((long)n * g.H + h) * g.W + w) * g.C + bcol_c[c]) : 0);
+                            if constexpr (VW == 4) {
+                                load_vec<4>(ptr, ok, breg[4 * i + jr]);
+                                if (bcol_ones[0]) {
+                                    breg[4 * i + jr][0] = kin ? 1.f : 0.f;
+                                    breg[4 * i + jr][1] = breg[4 * i + jr][2] =
+                                        breg[4 * i + jr][3] = 0.f;
+                                }
+                            } else {
+                                breg[4 * i + jr][c] =
+                                    bcol_ones[c] ? (kin ? 1.f : 0.f) : (ok ? *ptr : 0.f);
+                            }
+                        }
+                    }
+                }
+            }
+        }
+    };
+
+    auto sstore = [&](int buf) {
+        unsigned short* As = smem + buf * (BM + BN) * LDH;
+        unsigned short* Bs = As + BM * LDH;
+        if constexpr (A_KMAJ) {
+#pragma unroll
+            for (int i = 0; i < GA; ++i) {
+                const int row = t / KG + i * (NT / KG);
+                *reinterpret_cast<uintx2*>(As + row * LDH + kg) =
+                    uintx2{pack_bf16(areg[i][0], areg[i][1]), pack_bf16(areg[i][2], areg[i][3])};
+            }
+        } else if (a_act) {
+#pragma unroll
+            for (int i = 0; i < PA; ++i) {
+                const int kq = ((t + i * NT) / CGA) * 4;
+#pragma unroll
+                for (int c = 0; c < 4; ++c) {
+                    const int col = (t % CGA) * 4 + c;
+                    *reinterpret_cast<uintx2*>(As + col * LDH + kq) =
+                        uintx2{pack_bf16(areg[4 * i][c], areg[4 * i + 1][c]),
+                               pack_bf16(areg[4 * i + 2][c], areg[4 * i + 3][c])};
+                }
+            }
+        }
+        if constexpr (B_KMAJ) {
+#pragma unroll
+            for (int i = 0; i < GB; ++i) {
+                const int row = t / KG + i * (NT / KG);
+                *reinterpret_cast<uintx2*>(Bs + row * LDH + kg) =
+                    uintx2{pack_bf16(breg[i][0], breg[i][1]), pack_bf16(breg[i][2], breg[i][3])};
+            }
+        } else if (b_act) {
+#pragma unroll
+            for (int i = 0; i < PB; ++i) {
+                const int kq = ((t + i * NT) / CGB) * 4;
+#pragma unroll
+                for (int c = 0; c < 4; ++c) {
+                    const int col = (t % CGB) * 4 + c;
+                    *reinterpret_cast<uintx2*>(Bs + col * LDH + kq) =
+                        uintx2{pack_bf16(breg[4 * i][c], breg[4 * i + 1][c]),
+                               pack_bf16(breg[4 * i + 2][c], breg[4 * i + 3][c])};
+                }
+            }
+        }
+    };
+
+    floatx16 acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+
+    if (ktiles > 0) {
+        gload(0);
+        sstore(0);
+    }
+    __syncthreads();
+    const int lr = lane & 31;
+    const int lk = lane >> 5;
+    for (int kt = 0; kt < ktiles; ++kt) {
+        const int buf = kt & 1;
+        if (kt + 1 < ktiles) gload(kt + 1);
+        const unsigned short* As = smem + buf * (BM + BN) * LDH;
+        const unsigned short* Bs = As + BM * LDH;
+#pragma unroll
+        for (int kk = 0; kk < BKH; kk += 16) {
+            bf16x8 av[TM], bv[TN];
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+                av[i] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uintx4*>(
+                                                       As + (wm + 32 * i + lr) * LDH + kk + 8 * lk));
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+                bv[j] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uintx4*>(
+                                                       Bs + (wn + 32 * j + lr) * LDH + kk + 8 * lk));
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[i], bv[j], acc[i][j], 0,
+                                                                         0, 0);
+        }
+        if (kt + 1 < ktiles) sstore(buf ^ 1);
+        __syncthreads();
+    }
+    store_tile<BM, BN, TM, TN>(args, wk, acc, wm, wn, lane);
 }
+
 
 // Reduction of the cut tiles: workgroup = 64 elements of one tile x 16 split
 // lanes; lane l adds splits l, l+16, ...; the lane sums are combined in a
@@ -508,8 +887,13 @@ struct KernelRef {
 template <int OP, int CFG, int VW, bool BF>
 KernelRef kref() {
     constexpr TileCfg c = kCfgs[CFG];
-    return {reinterpret_cast<const void*>(&igemm_kernel<OP, c.bm, c.bn, c.bk, c.wm, c.wn, VW, BF>),
-            64 * (c.bm / c.wm) * (c.bn / c.wn)};
+    constexpr int nt = 64 * (c.bm / c.wm) * (c.bn / c.wn);
+    if constexpr (BF)
+        return {reinterpret_cast<const void*>(&igemm_bf16_kernel<OP, c.bm, c.bn, c.wm, c.wn, VW>),
+                nt};
+    else
+        return {reinterpret_cast<const void*>(&igemm_kernel<OP, c.bm, c.bn, c.bk, c.wm, c.wn, VW>),
+                nt};
 }
 
 // Every configuration is instantiated with vector width 4 (channel counts
@@ -577,7 +961,8 @@ GemmPlan plan_gemm(int op, const ConvGeo& g, int bf16, int num_cus, int bias_col
     }
     const TileCfg& c = kCfgs[p.cfg];
     const long tiles = ((p.M + c.bm - 1) / c.bm) * ((p.Ncols + c.bn - 1) / c.bn);
-    const long ktiles = (p.Kred + c.bk - 1) / c.bk;
+    const int bk = bf16 ? BKH : c.bk;
+    const long ktiles = (p.Kred + bk - 1) / bk;
     // workgroups resident at once
     KernelRef kr = kernel_for(op, p.cfg, v4, bf16 != 0);
     int occ = 0;
@@ -603,7 +988,7 @@ GemmPlan plan_gemm(int op, const ConvGeo& g, int bf16, int num_cus, int bias_col
     }
     long chunk_tiles = (ktiles + splits - 1) / splits;
     p.splits = (int)((ktiles + chunk_tiles - 1) / chunk_tiles);
-    p.kchunk = (int)(chunk_tiles * c.bk);
+    p.kchunk = (int)(chunk_tiles * bk);
     p.tfull = (int)(p.splits > 1 ? tfull : tiles);
     p.nwg = (int)(p.tfull + (tiles - p.tfull) * p.splits);
     p.ws_floats = (size_t)(tiles - p.tfull) * p.splits * c.bm * c.bn;
