@@ -9,6 +9,9 @@
 // strip of channels into a partial row of a workspace, then one thread per
 // channel adds the partials in block order.  No atomics are used, so every
 // result is bit-reproducible run to run.
+#include <algorithm>
+#include <initializer_list>
+
 #include "kernels.h"
 
 namespace hp {
@@ -206,86 +209,212 @@ __global__ void gap_bwd_kernel(const float* __restrict__ dy, float* __restrict__
 }
 
 // ---- per-channel column reductions ----------------------------------------
-// Workgroup (bx, by): channels [bx*64, bx*64+64), rows [by*RB, by*RB+RB).
-// 256 threads = 64 channels x 4 row lanes; the 4 row-lane sums are combined
-// in LDS in a fixed order.
-constexpr int CS_CH = 64;
-constexpr int CS_RB = 256;
+// Partials: workgroup (bx, by) reduces rows [by*rb, by*rb + rb) of a strip of
+// channels.  256 threads = cg channel lanes (VEC consecutive channels each,
+// one vector load per row) x 256/cg row lanes; a thread visits its rows four
+// at a time (independent loads in flight) and the row lanes are combined in
+// LDS in a fixed order.  rb is chosen so that the grid has a few hundred
+// workgroups whatever the shape (few rows x many channels or the reverse).
+//
+// MODE_SUM:     part0 = sum v
+// MODE_MOMENTS: part0 = mean of the block's rows, part1 = sum of squared
+//               deviations from it (one pass: each thread sums deviations from
+//               its first value, then the thread and block statistics are
+//               merged with the pairwise update of Chan, Golub and LeVeque)
+// MODE_BNBWD:   part0 = sum g, part1 = sum g * xhat, g = v masked by relu_y > 0
+//               when relu_y is given, xhat = (x - mean) * invstd
+enum { MODE_SUM = 0, MODE_MOMENTS = 1, MODE_BNBWD = 2 };
+constexpr int CS_THREADS = 256;
 
-inline int cs_row_blocks(long M) { return (int)((M + CS_RB - 1) / CS_RB); }
+template <int VEC>
+__device__ __forceinline__ void ldv(const float* p, float* o) {
+    if constexpr (VEC == 4) {
+        const float4 t = *reinterpret_cast<const float4*>(p);
+        o[0] = t.x; o[1] = t.y; o[2] = t.z; o[3] = t.w;
+    } else {
+        o[0] = *p;
+    }
+}
 
-// mode 0: sum v;  mode 1: sum (v - mean[c])^2;  mode 2: sum dy', sum dy'*xhat
-// (two outputs) where dy' = dy masked by relu_y > 0 if relu_y is given.
-template <int MODE>
-__global__ void colsum_partial_kernel(const float* __restrict__ v, const float* __restrict__ x,
-                                      const float* __restrict__ relu_y,
-                                      const float* __restrict__ mean,
-                                      const float* __restrict__ invstd, long M, int C,
-                                      float* __restrict__ part0, float* __restrict__ part1) {
-    __shared__ float red0[4][CS_CH];
-    __shared__ float red1[4][CS_CH];
-    const int cl = threadIdx.x % CS_CH;
-    const int rl = threadIdx.x / CS_CH;
-    const int c = blockIdx.x * CS_CH + cl;
-    const long r0 = (long)blockIdx.y * CS_RB;
-    const long r1 = min(r0 + CS_RB, M);
-    float s0 = 0.f, s1 = 0.f;
-    if (c < C) {
-        float mu = 0.f, is = 0.f;
-        if (MODE >= 1) mu = mean[c];
-        if (MODE == 2) is = invstd[c];
-        for (long r = r0 + rl; r < r1; r += 4) {
-            size_t idx = (size_t)r * C + c;
-            if (MODE == 0) {
-                s0 += v[idx];
-            } else if (MODE == 1) {
-                float d = v[idx] - mu;
-                s0 += d * d;
+// (n_a, mean_a, m2_a) <- merge with (n_b, mean_b, m2_b)
+__device__ __forceinline__ void chan_merge(float& na, float& mean_a, float& m2a, float nb,
+                                           float mean_b, float m2b) {
+    const float n = na + nb;
+    if (nb == 0.f) return;
+    if (na == 0.f) { na = nb; mean_a = mean_b; m2a = m2b; return; }
+    const float d = mean_b - mean_a;
+    const float f = nb / n;
+    mean_a = mean_a + d * f;
+    m2a = (m2a + m2b) + d * d * (na * f);
+    na = n;
+}
+
+template <int MODE, int VEC>
+__global__ void __launch_bounds__(CS_THREADS)
+colsum_partial_kernel(const float* __restrict__ v, const float* __restrict__ x,
+                      const float* __restrict__ relu_y, const float* __restrict__ mean,
+                      const float* __restrict__ invstd, long M, int C, int cg, long rb,
+                      float* __restrict__ part0, float* __restrict__ part1) {
+    __shared__ float red0[CS_THREADS * VEC];
+    __shared__ float red1[CS_THREADS * VEC];
+    __shared__ float cnt[CS_THREADS];
+    const int cl = threadIdx.x % cg;
+    const int rl = threadIdx.x / cg;
+    const int RL = CS_THREADS / cg;
+    const int c0 = (blockIdx.x * cg + cl) * VEC;
+    const bool on = c0 < C;
+    const long r0 = (long)blockIdx.y * rb;
+    const long r1 = min(r0 + rb, M);
+    float a0[VEC], a1[VEC], k[VEC], mu[VEC], is[VEC];
+#pragma unroll
+    for (int j = 0; j < VEC; ++j) a0[j] = a1[j] = k[j] = mu[j] = is[j] = 0.f;
+    int n = 0;
+    auto acc = [&](const float* t, const float* xx, const float* yy) {
+#pragma unroll
+        for (int j = 0; j < VEC; ++j) {
+            if constexpr (MODE == MODE_SUM) {
+                a0[j] += t[j];
+            } else if constexpr (MODE == MODE_MOMENTS) {
+                const float d = t[j] - k[j];
+                a0[j] += d;
+                a1[j] += d * d;
             } else {
-                float g = v[idx];
-                if (relu_y && !(relu_y[idx] > 0.f)) g = 0.f;
-                float xh = (x[idx] - mu) * is;
-                s0 += g;
-                s1 += g * xh;
+                const float g = (relu_y && !(yy[j] > 0.f)) ? 0.f : t[j];
+                const float xh = (xx[j] - mu[j]) * is[j];
+                a0[j] += g;
+                a1[j] += g * xh;
             }
         }
+    };
+    if (on) {
+        if constexpr (MODE == MODE_BNBWD) {
+            ldv<VEC>(mean + c0, mu);
+            ldv<VEC>(invstd + c0, is);
+        }
+        long r = r0 + rl;
+        if constexpr (MODE == MODE_MOMENTS) {
+            if (r < r1) ldv<VEC>(v + (size_t)r * C + c0, k);
+        }
+        for (; r + 3L * RL < r1; r += 4L * RL) {
+            float t[4][VEC], xx[4][VEC], yy[4][VEC];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+                const size_t idx = (size_t)(r + (long)u * RL) * C + c0;
+                ldv<VEC>(v + idx, t[u]);
+                if constexpr (MODE == MODE_BNBWD) {
+                    ldv<VEC>(x + idx, xx[u]);
+                    if (relu_y) ldv<VEC>(relu_y + idx, yy[u]);
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < 4; ++u) acc(t[u], xx[u], yy[u]);
+            n += 4;
+        }
+        for (; r < r1; r += RL) {
+            float t[VEC], xx[VEC], yy[VEC];
+            const size_t idx = (size_t)r * C + c0;
+            ldv<VEC>(v + idx, t);
+            if constexpr (MODE == MODE_BNBWD) {
+                ldv<VEC>(x + idx, xx);
+                if (relu_y) ldv<VEC>(relu_y + idx, yy);
+            }
+            acc(t, xx, yy);
+            n += 1;
+        }
     }
-    red0[rl][cl] = s0;
-    red1[rl][cl] = s1;
+    if constexpr (MODE == MODE_MOMENTS) {
+        // thread statistics: mean = shift + mean deviation
+        const float fn = (float)n;
+#pragma unroll
+        for (int j = 0; j < VEC; ++j) {
+            if (n > 0) {
+                const float md = a0[j] / fn;
+                a1[j] = fmaxf(a1[j] - a0[j] * md, 0.f);
+                a0[j] = k[j] + md;
+            }
+        }
+        cnt[threadIdx.x] = fn;
+    }
+#pragma unroll
+    for (int j = 0; j < VEC; ++j) {
+        red0[threadIdx.x * VEC + j] = a0[j];
+        red1[threadIdx.x * VEC + j] = a1[j];
+    }
     __syncthreads();
-    if (rl == 0 && c < C) {
-        float a0 = ((red0[0][cl] + red0[1][cl]) + red0[2][cl]) + red0[3][cl];
-        part0[(size_t)blockIdx.y * C + c] = a0;
-        if (MODE == 2) {
-            float a1 = ((red1[0][cl] + red1[1][cl]) + red1[2][cl]) + red1[3][cl];
-            part1[(size_t)blockIdx.y * C + c] = a1;
+    if (rl == 0 && on) {
+#pragma unroll
+        for (int j = 0; j < VEC; ++j) {
+            float s0 = red0[cl * VEC + j], s1 = red1[cl * VEC + j];
+            float na = (MODE == MODE_MOMENTS) ? cnt[cl] : 0.f;
+            for (int l = 1; l < RL; ++l) {
+                const int th = l * cg + cl;
+                if constexpr (MODE == MODE_MOMENTS) {
+                    chan_merge(na, s0, s1, cnt[th], red0[th * VEC + j], red1[th * VEC + j]);
+                } else {
+                    s0 += red0[th * VEC + j];
+                    s1 += red1[th * VEC + j];
+                }
+            }
+            if (c0 + j < C) {
+                part0[(size_t)blockIdx.y * C + c0 + j] = s0;
+                if (MODE != MODE_SUM) part1[(size_t)blockIdx.y * C + c0 + j] = s1;
+            }
         }
     }
 }
 
-// Final reduction of the row-block partials: workgroup = 64 channels x 16
-// lanes; lane l sums partial rows l, l+16, ...; the 16 lane sums are combined
-// in LDS in a fixed order.  mode 0: out = sum; 1: out = sum / M (mean);
-// 2: out = 1 / sqrt(sum / M + eps) (inverse standard deviation).
-constexpr int CF_LANES = 16;
+// Combination of the nb row-block partials of each channel: workgroup = 64
+// channels x 16 lanes; lane l takes blocks l, l+16, ... in order, then the 16
+// lane results are combined in order.
+//   FIN_SUM:   out0 = sum part0
+//   FIN_SUM2:  out0 = sum part0, out1 = sum part1
+//   FIN_STATS: merge (block mean, block squared deviations); out0 = mean,
+//              out1 = 1 / sqrt(biased variance + eps)
+enum { FIN_SUM = 0, FIN_SUM2 = 1, FIN_STATS = 2 };
+constexpr int CF_CH = 64, CF_LANES = 16;
 
-__global__ void colsum_final_kernel(const float* __restrict__ part, int nb, int C, long M,
-                                    float eps, int mode, float* __restrict__ out) {
-    __shared__ float red[CF_LANES][CS_CH];
-    const int cl = threadIdx.x % CS_CH;
-    const int rl = threadIdx.x / CS_CH;
-    const int c = blockIdx.x * CS_CH + cl;
-    float s = 0.f;
-    if (c < C)
-        for (int b = rl; b < nb; b += CF_LANES) s += part[(size_t)b * C + c];
-    red[rl][cl] = s;
+template <int FIN>
+__global__ void __launch_bounds__(CF_CH * CF_LANES)
+colsum_final_kernel(const float* __restrict__ part0, const float* __restrict__ part1, int nb,
+                    long rb, int C, long M, float eps, float* __restrict__ out0,
+                    float* __restrict__ out1) {
+    __shared__ float r0[CF_LANES][CF_CH], r1[CF_LANES][CF_CH], rn[CF_LANES][CF_CH];
+    const int cl = threadIdx.x % CF_CH;
+    const int ln = threadIdx.x / CF_CH;
+    const int c = blockIdx.x * CF_CH + cl;
+    float s0 = 0.f, s1 = 0.f, na = 0.f;
+    if (c < C) {
+        for (int b = ln; b < nb; b += CF_LANES) {
+            const float p0 = part0[(size_t)b * C + c];
+            if constexpr (FIN == FIN_STATS) {
+                const float cnt = (float)min(rb, M - (long)b * rb);
+                chan_merge(na, s0, s1, cnt, p0, part1[(size_t)b * C + c]);
+            } else {
+                s0 += p0;
+                if (FIN == FIN_SUM2) s1 += part1[(size_t)b * C + c];
+            }
+        }
+    }
+    r0[ln][cl] = s0;
+    r1[ln][cl] = s1;
+    rn[ln][cl] = na;
     __syncthreads();
-    if (rl == 0 && c < C) {
-        float t = 0.f;
-        for (int l = 0; l < CF_LANES; ++l) t += red[l][cl];
-        if (mode == 1) t = t / (float)M;
-        else if (mode == 2) t = 1.f / sqrtf(t / (float)M + eps);
-        out[c] = t;
+    if (ln == 0 && c < C) {
+        for (int l = 1; l < CF_LANES; ++l) {
+            if constexpr (FIN == FIN_STATS) {
+                chan_merge(na, s0, s1, rn[l][cl], r0[l][cl], r1[l][cl]);
+            } else {
+                s0 += r0[l][cl];
+                s1 += r1[l][cl];
+            }
+        }
+        if constexpr (FIN == FIN_STATS) {
+            out0[c] = s0;
+            out1[c] = 1.f / sqrtf(s1 / (float)M + eps);
+        } else {
+            out0[c] = s0;
+            if (FIN == FIN_SUM2) out1[c] = s1;
+        }
     }
 }
 
@@ -438,33 +567,88 @@ hipError_t launch_gap_bwd(const float* dy, float* dx, int N, int HW, int C, int 
     return hipGetLastError();
 }
 
-size_t colsum_ws_floats(long M, int C) { return (size_t)cs_row_blocks(M) * C; }
+namespace {
+
+// Launch shape of a column reduction: VEC channels per thread (4 when the
+// channel count and the operands allow float4 loads), cg channel lanes, gx x nb
+// workgroups of rb rows.
+struct ColPlan {
+    int vec, cg, gx, nb;
+    long rb;
+};
+
+ColPlan col_plan(long M, int C, int vec) {
+    ColPlan p;
+    p.vec = vec;
+    const int groups = (C + vec - 1) / vec;
+    int cg = 1;
+    while (cg < groups && cg < 64) cg <<= 1;
+    p.cg = cg;
+    const int rl = CS_THREADS / cg;
+    p.gx = (groups + cg - 1) / cg;
+    const long want = std::max(1, 512 / p.gx);
+    const long most = std::max(1L, (M + 4L * rl - 1) / (4L * rl));
+    const long nb = std::min(want, most);
+    long rb = (std::max(M, 1L) + nb - 1) / nb;
+    rb = (rb + rl - 1) / rl * rl;
+    p.rb = rb;
+    p.nb = (int)((std::max(M, 1L) + rb - 1) / rb);
+    return p;
+}
+
+bool vec4_ok(int C, std::initializer_list<const void*> ptrs) {
+    if (C % 4) return false;
+    for (const void* q : ptrs)
+        if (((uintptr_t)q) & 15) return false;
+    return true;
+}
+
+int col_blocks_max(long M, int C) {
+    return std::max(col_plan(M, C, 4).nb, col_plan(M, C, 1).nb);
+}
+
+template <int MODE>
+void launch_partial(const ColPlan& p, const float* v, const float* x, const float* relu_y,
+                    const float* mean, const float* invstd, long M, int C, float* part0,
+                    float* part1, hipStream_t s) {
+    const dim3 grid(p.gx, p.nb);
+    if (p.vec == 4)
+        hipLaunchKernelGGL((colsum_partial_kernel<MODE, 4>), grid, dim3(CS_THREADS), 0, s, v, x,
+                           relu_y, mean, invstd, M, C, p.cg, p.rb, part0, part1);
+    else
+        hipLaunchKernelGGL((colsum_partial_kernel<MODE, 1>), grid, dim3(CS_THREADS), 0, s, v, x,
+                           relu_y, mean, invstd, M, C, p.cg, p.rb, part0, part1);
+}
+
+template <int FIN>
+void launch_final(const ColPlan& p, const float* part0, const float* part1, long M, int C,
+                  float eps, float* out0, float* out1, hipStream_t s) {
+    hipLaunchKernelGGL((colsum_final_kernel<FIN>), dim3((C + CF_CH - 1) / CF_CH),
+                       dim3(CF_CH * CF_LANES), 0, s, part0, part1, p.nb, p.rb, C, M, eps, out0,
+                       out1);
+}
+
+}  // namespace
+
+size_t colsum_ws_floats(long M, int C) { return (size_t)col_blocks_max(M, C) * C; }
 
 hipError_t launch_colsum(const float* v, long M, int C, float* out, float* ws, hipStream_t s) {
-    int nb = cs_row_blocks(M);
-    dim3 grid((C + CS_CH - 1) / CS_CH, nb);
-    hipLaunchKernelGGL(colsum_partial_kernel<0>, grid, dim3(256), 0, s, v, nullptr, nullptr,
-                       nullptr, nullptr, M, C, ws, nullptr);
-    hipLaunchKernelGGL(colsum_final_kernel, dim3((C + CS_CH - 1) / CS_CH), dim3(CS_CH * CF_LANES), 0,
-                       s, ws, nb, C, M, 0.f, 0, out);
+    const ColPlan p = col_plan(M, C, vec4_ok(C, {v}) ? 4 : 1);
+    launch_partial<MODE_SUM>(p, v, nullptr, nullptr, nullptr, nullptr, M, C, ws, nullptr, s);
+    launch_final<FIN_SUM>(p, ws, nullptr, M, C, 0.f, out, nullptr, s);
     return hipGetLastError();
 }
 
-size_t bn_ws_floats(long M, int C) { return 2 * (size_t)cs_row_blocks(M) * C + 2 * (size_t)C; }
+size_t bn_ws_floats(long M, int C) { return 2 * (size_t)col_blocks_max(M, C) * C; }
 
 hipError_t launch_bn_fwd(const float* x, long M, int C, const float* gamma, const float* beta,
                          float eps, float* y, float* mean, float* invstd, int relu, float* ws,
                          hipStream_t s) {
-    int nb = cs_row_blocks(M);
-    dim3 grid((C + CS_CH - 1) / CS_CH, nb);
-    hipLaunchKernelGGL(colsum_partial_kernel<0>, grid, dim3(256), 0, s, x, nullptr, nullptr,
-                       nullptr, nullptr, M, C, ws, nullptr);
-    hipLaunchKernelGGL(colsum_final_kernel, dim3((C + CS_CH - 1) / CS_CH), dim3(CS_CH * CF_LANES), 0,
-                       s, ws, nb, C, M, 0.f, 1, mean);
-    hipLaunchKernelGGL(colsum_partial_kernel<1>, grid, dim3(256), 0, s, x, nullptr, nullptr, mean,
-                       nullptr, M, C, ws, nullptr);
-    hipLaunchKernelGGL(colsum_final_kernel, dim3((C + CS_CH - 1) / CS_CH), dim3(CS_CH * CF_LANES), 0,
-                       s, ws, nb, C, M, eps, 2, invstd);
+    const ColPlan p = col_plan(M, C, vec4_ok(C, {x}) ? 4 : 1);
+    float* p0 = ws;
+    float* p1 = ws + (size_t)p.nb * C;
+    launch_partial<MODE_MOMENTS>(p, x, nullptr, nullptr, nullptr, nullptr, M, C, p0, p1, s);
+    launch_final<FIN_STATS>(p, p0, p1, M, C, eps, mean, invstd, s);
     size_t n = (size_t)M * C;
     hipLaunchKernelGGL(bn_apply_kernel, dim3(ew_blocks(n)), dim3(EW_THREADS), 0, s, x, M, C, gamma,
                        beta, mean, invstd, y, relu);
@@ -474,16 +658,11 @@ hipError_t launch_bn_fwd(const float* x, long M, int C, const float* gamma, cons
 hipError_t launch_bn_bwd(const float* x, const float* dy, const float* relu_y, long M, int C,
                          const float* gamma, const float* mean, const float* invstd, float* dx,
                          float* dgamma, float* dbeta, int accumulate, float* ws, hipStream_t s) {
-    int nb = cs_row_blocks(M);
+    const ColPlan p = col_plan(M, C, vec4_ok(C, {x, dy, relu_y, mean, invstd}) ? 4 : 1);
     float* p0 = ws;
-    float* p1 = ws + (size_t)nb * C;
-    dim3 grid((C + CS_CH - 1) / CS_CH, nb);
-    hipLaunchKernelGGL(colsum_partial_kernel<2>, grid, dim3(256), 0, s, dy, x, relu_y, mean,
-                       invstd, M, C, p0, p1);
-    hipLaunchKernelGGL(colsum_final_kernel, dim3((C + CS_CH - 1) / CS_CH), dim3(CS_CH * CF_LANES), 0,
-                       s, p0, nb, C, M, 0.f, 0, dbeta);
-    hipLaunchKernelGGL(colsum_final_kernel, dim3((C + CS_CH - 1) / CS_CH), dim3(CS_CH * CF_LANES), 0,
-                       s, p1, nb, C, M, 0.f, 0, dgamma);
+    float* p1 = ws + (size_t)p.nb * C;
+    launch_partial<MODE_BNBWD>(p, dy, x, relu_y, mean, invstd, M, C, p0, p1, s);
+    launch_final<FIN_SUM2>(p, p0, p1, M, C, 0.f, dbeta, dgamma, s);
     if (!dx) return hipGetLastError();      // parameter gradients only
     size_t n = (size_t)M * C;
     hipLaunchKernelGGL(bn_bwd_apply_kernel, dim3(ew_blocks(n)), dim3(EW_THREADS), 0, s, x, dy,
