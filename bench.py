@@ -77,6 +77,33 @@ def measured_traffic(workload):
     return d.get("bytes_per_step")
 
 
+# Algorithmic HBM bytes per parameter of each WSP update kernel (fp32):
+#   local update starting a wave: read g, w_newest; write w_new, u~     16 B
+#   other local updates:          read g, w_newest, u~; write w_new, u~  20 B
+#   wave push:                    read w_g, u~; write w_g                12 B
+#   pull:                         read w_g; write the ring slot           8 B
+UPDATE_BYTES_PER_PARAM = {"update_first": 16, "update": 20, "push": 12, "pull": 8}
+
+
+def update_roofline(P, ms, launches):
+    """HBM roofline of the WSP update kernels over the timed steps (device
+    time from HIP events around every launch on the server's stream)."""
+    per = {}
+    tot_b = tot_ms = 0.0
+    for k, b in UPDATE_BYTES_PER_PARAM.items():
+        if launches[k]:
+            nbytes = b * P * launches[k]
+            per[k] = {"launches": launches[k], "avg_us": round(ms[k] * 1e3 / launches[k], 2),
+                      "GB/s": round(nbytes / (ms[k] * 1e-3) / 1e9, 1)}
+            tot_b += nbytes
+            tot_ms += ms[k]
+    if not tot_ms:
+        return None
+    achieved = tot_b / (tot_ms * 1e-3) / 1e9
+    return {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4), "params": P, "kernels": per}
+
+
 def cpu_baseline(wl, layers, out_shape, images):
     """The oracle (plain C loops, fp64 accumulation, OpenMP) on the first
     `images` images of minibatch 1: forward + backward of the stage and the
@@ -156,7 +183,9 @@ def main():
         drv.minibatch(next_vw())
     torch.cuda.synchronize()
     st.read_timing()                      # discard
+    drv.ps.read_timing()
     st.set_timing(True)
+    drv.ps.set_timing(True)
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -171,6 +200,8 @@ def main():
     ev_ms = start.elapsed_time(stop)
     ms, launches = st.read_timing()
     st.set_timing(False)
+    ums, ulaunch = drv.ps.read_timing()
+    drv.ps.set_timing(False)
 
     ms_step = max(wall, ev_ms / 1e3) * 1e3 / args.steps
     value = wl.batch * args.steps / (max(wall, ev_ms / 1e3))
@@ -201,6 +232,7 @@ def main():
                      "flop_per_step": flops_step, "ms_per_step": round(gemm_ms_step, 4),
                      "launches_per_step": launches["contraction"] / args.steps},
         "other_kernels_ms_per_step": round(ms["other"] / args.steps, 4),
+        "wsp_update_roofline": update_roofline(st.P, ums, ulaunch),
     }
     drv.close()
     st.close()

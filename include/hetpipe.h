@@ -140,6 +140,15 @@ int hp_ps_destroy(hp_ps *ps);
 /* Device pointer to w_g (read-only for the caller) and the global clock. */
 int hp_ps_weights(const hp_ps *ps, const float **wg);
 int hp_ps_clock(const hp_ps *ps, int *c_global);
+/* Device timing of the WSP update kernels, for profiling.  While enabled,
+ * every kernel enqueued by hp_wsp_local_update, hp_wsp_push_wave and
+ * hp_wsp_pull of this server's virtual workers is bracketed by HIP events on
+ * the server's stream.  hp_ps_read_timing synchronises the stream, returns the
+ * summed device time in milliseconds and the launch counts of [0] local
+ * updates whose minibatch starts a wave, [1] the other local updates, [2]
+ * wave pushes, [3] pulls that copied w_g, and resets the sums. */
+int hp_ps_set_timing(hp_ps *ps, int enable);
+int hp_ps_read_timing(hp_ps *ps, double ms[4], int64_t launches[4]);
 
 /* ======================================================= virtual worker */
 

@@ -128,6 +128,7 @@ struct hp_stage {
 struct hp_vw;
 
 struct hp_ps {
+    StageTimer timer;
     size_t P = 0;
     float* wg = nullptr;
     int N = 0, D = 0;
@@ -414,21 +415,29 @@ extern "C" int hp_stage_set_timing(hp_stage* st, int enable) {
     return HP_OK;
 }
 
-extern "C" int hp_stage_read_timing(hp_stage* st, double ms[2], int64_t launches[2]) {
-    if (!st || !ms || !launches) return fail(HP_ERR_ARG, "hp_stage_read_timing: NULL argument");
-    HP_HIP(hipStreamSynchronize(st->stream));
-    ms[0] = ms[1] = 0.0;
-    launches[0] = launches[1] = 0;
-    for (auto& r : st->timer.recs) {
+namespace {
+
+// Sums the recorded event pairs per category (after synchronising `s`) and
+// returns the events to the pool.
+int read_timer(StageTimer& tm, hipStream_t s, int ncat, double* ms, int64_t* launches) {
+    HP_HIP(hipStreamSynchronize(s));
+    for (int i = 0; i < ncat; ++i) { ms[i] = 0.0; launches[i] = 0; }
+    for (auto& r : tm.recs) {
         float t = 0.f;
         HP_HIP(hipEventElapsedTime(&t, r.a, r.b));
-        ms[r.cat] += t;
-        launches[r.cat] += 1;
-        st->timer.pool.push_back(r.a);
-        st->timer.pool.push_back(r.b);
+        if (r.cat >= 0 && r.cat < ncat) { ms[r.cat] += t; launches[r.cat] += 1; }
+        tm.pool.push_back(r.a);
+        tm.pool.push_back(r.b);
     }
-    st->timer.recs.clear();
+    tm.recs.clear();
     return HP_OK;
+}
+
+}  // namespace
+
+extern "C" int hp_stage_read_timing(hp_stage* st, double ms[2], int64_t launches[2]) {
+    if (!st || !ms || !launches) return fail(HP_ERR_ARG, "hp_stage_read_timing: NULL argument");
+    return read_timer(st->timer, st->stream, 2, ms, launches);
 }
 
 extern "C" int hp_stage_forward(hp_stage* st, const float* w, const float* x, float* y,
@@ -676,6 +685,17 @@ extern "C" int hp_ps_clock(const hp_ps* ps, int* c_global) {
     return HP_OK;
 }
 
+extern "C" int hp_ps_set_timing(hp_ps* ps, int enable) {
+    if (!ps) return fail(HP_ERR_ARG, "hp_ps_set_timing: NULL server");
+    ps->timer.on = enable != 0;
+    return HP_OK;
+}
+
+extern "C" int hp_ps_read_timing(hp_ps* ps, double ms[4], int64_t launches[4]) {
+    if (!ps || !ms || !launches) return fail(HP_ERR_ARG, "hp_ps_read_timing: NULL argument");
+    return read_timer(ps->timer, ps->stream, 4, ms, launches);
+}
+
 // ========================================================== virtual worker
 
 extern "C" int hp_vw_create(hp_ps* ps, int id, int s_local, hp_vw** out) {
@@ -753,9 +773,12 @@ extern "C" int hp_wsp_local_update(hp_vw* v, const float* grad, float lr) {
     const int slot = (int)((q - 1) % W);
     const int newest = (int)((q - 2 + W) % W);
     const int first = ((q - 1) % W) == 0;
+    StageTimer& tm = v->ps->timer;
+    tm.begin(first ? 0 : 1, v->ps->stream);
     hipError_t e = launch_wsp_local_update(grad, v->ring + (size_t)newest * v->stride,
                                            v->ring + (size_t)slot * v->stride, v->ut, v->P, lr,
                                            first, v->ps->stream);
+    tm.end(v->ps->stream);
     if (e != hipSuccess) return fail(HP_ERR_HIP, "local update launch: %s", hipGetErrorString(e));
     std::vector<int64_t> nv = v->V[newest];
     nv[v->id] += 1;
@@ -771,7 +794,9 @@ extern "C" int hp_wsp_push_wave(hp_vw* v, hp_ps* ps) {
     if (v->ps != ps) return fail(HP_ERR_ARG, "hp_wsp_push_wave: VW belongs to another server");
     if (!v->push_due)
         return fail(HP_ERR_STATE, "hp_wsp_push_wave: VW %d has no completed, unpushed wave", v->id);
+    ps->timer.begin(2, ps->stream);
     hipError_t e = launch_wsp_push(ps->wg, v->ut, v->P, ps->stream);
+    ps->timer.end(ps->stream);
     if (e != hipSuccess) return fail(HP_ERR_HIP, "push launch: %s", hipGetErrorString(e));
     ps->pushed[v->id] += 1;
     v->c = (int)(v->p / v->W);
@@ -793,7 +818,9 @@ extern "C" int hp_wsp_pull(hp_vw* v, hp_ps* ps) {
     }
     if (ps->cg < need) return HP_WOULD_BLOCK;
     const int slot = (int)((v->p - 1) % v->W);
+    ps->timer.begin(3, ps->stream);
     hipError_t e = launch_wsp_copy(ps->wg, v->ring + (size_t)slot * v->stride, v->P, ps->stream);
+    ps->timer.end(ps->stream);
     if (e != hipSuccess) return fail(HP_ERR_HIP, "pull launch: %s", hipGetErrorString(e));
     for (int n = 0; n < ps->N; ++n) v->V[slot][n] = (int64_t)v->W * ps->pushed[n];
     v->g = ps->cg;

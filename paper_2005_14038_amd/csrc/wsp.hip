@@ -1,8 +1,11 @@
 // WSP update kernels (gfx950): local update + wave accumulation, push, pull.
 //
 // All three stream flat fp32 parameter vectors once, so they are HBM-bound:
-// float4 accesses, a grid of a few workgroups per CU striding over the vector,
-// and a scalar tail for lengths that are not multiples of 4.  The arithmetic
+// float4 accesses (four per thread per iteration on long vectors, all loads
+// issued before the first use), a grid of up to 16 workgroups per CU striding
+// over the vector, and a scalar tail for lengths that are not multiples of 4.  Operands
+// read once and not needed again soon (the gradient, u~ in the push) are
+// loaded non-temporally.  The arithmetic
 // is fixed to one IEEE fp32 operation at a time (contraction into fused
 // multiply-add is switched off for this file), so the result is bit-identical to any
 // other implementation that performs the same operations in the same order:
@@ -16,9 +19,14 @@ namespace hp {
 namespace {
 
 constexpr int WSP_THREADS = 256;
+// float4 per thread per iteration: 4 for long vectors (all loads issued
+// before the first use), 1 for short ones, where more workgroups start sooner.
+constexpr size_t WSP_LONG = size_t(1) << 20;     // float4 elements (16 MB)
 
-inline int wsp_blocks(size_t n4) {
-    size_t b = (n4 + WSP_THREADS - 1) / WSP_THREADS;
+inline int wsp_unroll(size_t n4) { return n4 >= WSP_LONG ? 4 : 1; }
+
+inline int wsp_blocks(size_t n4, int unroll) {
+    size_t b = (n4 + (size_t)WSP_THREADS * unroll - 1) / ((size_t)WSP_THREADS * unroll);
     if (b > 4096) b = 4096;      // 16 workgroups per CU, grid-stride beyond that
     return (int)(b ? b : 1);
 }
@@ -26,35 +34,62 @@ inline int wsp_blocks(size_t n4) {
 __device__ __forceinline__ float mul_rn(float a, float b) { return a * b; }
 __device__ __forceinline__ float add_rn(float a, float b) { return a + b; }
 
-template <bool FIRST>
-__global__ void local_update_kernel(const float* __restrict__ g, const float* newest,
-                                    float* dst, float* __restrict__ ut, size_t n, float neg_lr,
-                                    int vec) {
+typedef float fx4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ float4 ld4(const float4* p) {
+    const fx4 v = __builtin_nontemporal_load(reinterpret_cast<const fx4*>(p));
+    return make_float4(v.x, v.y, v.z, v.w);
+}
+
+// Vector part: workgroup b's iteration covers U * blockDim.x consecutive
+// float4 elements starting at (it * gridDim.x + b) * U * blockDim.x; thread t
+// takes elements base + k * blockDim.x (k < U), so every load instruction of a
+// wave reads 1 KB contiguous.
+#define WSP_VECTOR_LOOP(n4)                                                               \
+    const size_t stride = (size_t)gridDim.x * blockDim.x;                                 \
+    for (size_t base = (size_t)blockIdx.x * blockDim.x * U + threadIdx.x; base < (n4);    \
+         base += stride * U)
+
+template <bool FIRST, int U>
+__global__ void __launch_bounds__(WSP_THREADS)
+local_update_kernel(const float* __restrict__ g, const float* newest, float* dst,
+                    float* __restrict__ ut, size_t n, float neg_lr, int vec) {
     // newest and dst may alias (wave length 1): each element is read before it
     // is written by the same thread.
     const size_t n4 = vec ? n / 4 : 0;
-    const size_t stride = (size_t)gridDim.x * blockDim.x;
     const float4* g4 = reinterpret_cast<const float4*>(g);
     const float4* w4 = reinterpret_cast<const float4*>(newest);
     float4* d4 = reinterpret_cast<float4*>(dst);
     float4* u4 = reinterpret_cast<float4*>(ut);
-    for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += stride) {
-        float4 gv = g4[i];
-        float4 wv = w4[i];
-        float4 u;
-        u.x = mul_rn(neg_lr, gv.x); u.y = mul_rn(neg_lr, gv.y);
-        u.z = mul_rn(neg_lr, gv.z); u.w = mul_rn(neg_lr, gv.w);
-        float4 nw;
-        nw.x = add_rn(wv.x, u.x); nw.y = add_rn(wv.y, u.y);
-        nw.z = add_rn(wv.z, u.z); nw.w = add_rn(wv.w, u.w);
-        d4[i] = nw;
-        if (FIRST) {
-            u4[i] = u;
-        } else {
-            float4 a = u4[i];
-            a.x = add_rn(a.x, u.x); a.y = add_rn(a.y, u.y);
-            a.z = add_rn(a.z, u.z); a.w = add_rn(a.w, u.w);
-            u4[i] = a;
+    WSP_VECTOR_LOOP(n4) {
+        float4 gv[U], wv[U], av[U];
+#pragma unroll
+        for (int k = 0; k < U; ++k) {
+            const size_t i = base + (size_t)k * blockDim.x;
+            if (i < n4) {
+                gv[k] = ld4(g4 + i);
+                wv[k] = w4[i];
+                if (!FIRST) av[k] = u4[i];
+            }
+        }
+#pragma unroll
+        for (int k = 0; k < U; ++k) {
+            const size_t i = base + (size_t)k * blockDim.x;
+            if (i >= n4) break;
+            float4 u;
+            u.x = mul_rn(neg_lr, gv[k].x); u.y = mul_rn(neg_lr, gv[k].y);
+            u.z = mul_rn(neg_lr, gv[k].z); u.w = mul_rn(neg_lr, gv[k].w);
+            float4 nw;
+            nw.x = add_rn(wv[k].x, u.x); nw.y = add_rn(wv[k].y, u.y);
+            nw.z = add_rn(wv[k].z, u.z); nw.w = add_rn(wv[k].w, u.w);
+            d4[i] = nw;
+            if (FIRST) {
+                u4[i] = u;
+            } else {
+                float4 a = av[k];
+                a.x = add_rn(a.x, u.x); a.y = add_rn(a.y, u.y);
+                a.z = add_rn(a.z, u.z); a.w = add_rn(a.w, u.w);
+                u4[i] = a;
+            }
         }
     }
     for (size_t i = n4 * 4 + (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
@@ -64,29 +99,52 @@ __global__ void local_update_kernel(const float* __restrict__ g, const float* ne
     }
 }
 
-__global__ void push_kernel(float* __restrict__ wg, const float* __restrict__ ut, size_t n,
-                            int vec) {
+template <int U>
+__global__ void __launch_bounds__(WSP_THREADS)
+push_kernel(float* __restrict__ wg, const float* __restrict__ ut, size_t n, int vec) {
     const size_t n4 = vec ? n / 4 : 0;
-    const size_t stride = (size_t)gridDim.x * blockDim.x;
     float4* w4 = reinterpret_cast<float4*>(wg);
     const float4* u4 = reinterpret_cast<const float4*>(ut);
-    for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += stride) {
-        float4 a = w4[i], b = u4[i];
-        a.x = add_rn(a.x, b.x); a.y = add_rn(a.y, b.y);
-        a.z = add_rn(a.z, b.z); a.w = add_rn(a.w, b.w);
-        w4[i] = a;
+    WSP_VECTOR_LOOP(n4) {
+        float4 a[U], b[U];
+#pragma unroll
+        for (int k = 0; k < U; ++k) {
+            const size_t i = base + (size_t)k * blockDim.x;
+            if (i < n4) { a[k] = w4[i]; b[k] = ld4(u4 + i); }
+        }
+#pragma unroll
+        for (int k = 0; k < U; ++k) {
+            const size_t i = base + (size_t)k * blockDim.x;
+            if (i >= n4) break;
+            float4 v = a[k];
+            v.x = add_rn(v.x, b[k].x); v.y = add_rn(v.y, b[k].y);
+            v.z = add_rn(v.z, b[k].z); v.w = add_rn(v.w, b[k].w);
+            w4[i] = v;
+        }
     }
     for (size_t i = n4 * 4 + (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride)
         wg[i] = add_rn(wg[i], ut[i]);
 }
 
-__global__ void copy_kernel(const float* __restrict__ src, float* __restrict__ dst, size_t n,
-                            int vec) {
+template <int U>
+__global__ void __launch_bounds__(WSP_THREADS)
+copy_kernel(const float* __restrict__ src, float* __restrict__ dst, size_t n, int vec) {
     const size_t n4 = vec ? n / 4 : 0;
-    const size_t stride = (size_t)gridDim.x * blockDim.x;
     const float4* s4 = reinterpret_cast<const float4*>(src);
     float4* d4 = reinterpret_cast<float4*>(dst);
-    for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += stride) d4[i] = s4[i];
+    WSP_VECTOR_LOOP(n4) {
+        float4 a[U];
+#pragma unroll
+        for (int k = 0; k < U; ++k) {
+            const size_t i = base + (size_t)k * blockDim.x;
+            if (i < n4) a[k] = s4[i];
+        }
+#pragma unroll
+        for (int k = 0; k < U; ++k) {
+            const size_t i = base + (size_t)k * blockDim.x;
+            if (i < n4) d4[i] = a[k];
+        }
+    }
     for (size_t i = n4 * 4 + (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride)
         dst[i] = src[i];
 }
@@ -103,27 +161,45 @@ hipError_t launch_wsp_local_update(const float* g, const float* newest, float* d
                                    size_t n, float lr, int first, hipStream_t s) {
     const float neg_lr = -lr;
     const int vec = aligned16(g, newest, dst, ut);
-    const int blocks = wsp_blocks(vec ? n / 4 : n);
-    if (first)
-        hipLaunchKernelGGL(local_update_kernel<true>, dim3(blocks), dim3(WSP_THREADS), 0, s, g,
-                           newest, dst, ut, n, neg_lr, vec);
+    const size_t n4 = vec ? n / 4 : n;
+    const int u = wsp_unroll(n4);
+    const dim3 grid(wsp_blocks(n4, u)), block(WSP_THREADS);
+    if (first && u == 4)
+        hipLaunchKernelGGL((local_update_kernel<true, 4>), grid, block, 0, s, g, newest, dst, ut, n,
+                           neg_lr, vec);
+    else if (first)
+        hipLaunchKernelGGL((local_update_kernel<true, 1>), grid, block, 0, s, g, newest, dst, ut, n,
+                           neg_lr, vec);
+    else if (u == 4)
+        hipLaunchKernelGGL((local_update_kernel<false, 4>), grid, block, 0, s, g, newest, dst, ut, n,
+                           neg_lr, vec);
     else
-        hipLaunchKernelGGL(local_update_kernel<false>, dim3(blocks), dim3(WSP_THREADS), 0, s, g,
-                           newest, dst, ut, n, neg_lr, vec);
+        hipLaunchKernelGGL((local_update_kernel<false, 1>), grid, block, 0, s, g, newest, dst, ut, n,
+                           neg_lr, vec);
     return hipGetLastError();
 }
 
 hipError_t launch_wsp_push(float* wg, const float* ut, size_t n, hipStream_t s) {
     const int vec = aligned16(wg, ut);
-    hipLaunchKernelGGL(push_kernel, dim3(wsp_blocks(vec ? n / 4 : n)), dim3(WSP_THREADS), 0, s, wg,
-                       ut, n, vec);
+    const size_t n4 = vec ? n / 4 : n;
+    const int u = wsp_unroll(n4);
+    const dim3 grid(wsp_blocks(n4, u)), block(WSP_THREADS);
+    if (u == 4)
+        hipLaunchKernelGGL(push_kernel<4>, grid, block, 0, s, wg, ut, n, vec);
+    else
+        hipLaunchKernelGGL(push_kernel<1>, grid, block, 0, s, wg, ut, n, vec);
     return hipGetLastError();
 }
 
 hipError_t launch_wsp_copy(const float* src, float* dst, size_t n, hipStream_t s) {
     const int vec = aligned16(src, dst);
-    hipLaunchKernelGGL(copy_kernel, dim3(wsp_blocks(vec ? n / 4 : n)), dim3(WSP_THREADS), 0, s, src,
-                       dst, n, vec);
+    const size_t n4 = vec ? n / 4 : n;
+    const int u = wsp_unroll(n4);
+    const dim3 grid(wsp_blocks(n4, u)), block(WSP_THREADS);
+    if (u == 4)
+        hipLaunchKernelGGL(copy_kernel<4>, grid, block, 0, s, src, dst, n, vec);
+    else
+        hipLaunchKernelGGL(copy_kernel<1>, grid, block, 0, s, src, dst, n, vec);
     return hipGetLastError();
 }
 

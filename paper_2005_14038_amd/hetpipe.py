@@ -25,7 +25,8 @@ EXPORTS = [
     "hp_stage_create", "hp_stage_destroy", "hp_stage_param_count", "hp_stage_param_layout",
     "hp_stage_output_shape", "hp_stage_device_bytes", "hp_stage_set_timing",
     "hp_stage_read_timing", "hp_stage_forward", "hp_stage_backward",
-    "hp_ps_create", "hp_ps_destroy", "hp_ps_weights", "hp_ps_clock",
+    "hp_ps_create", "hp_ps_destroy", "hp_ps_weights", "hp_ps_clock", "hp_ps_set_timing",
+    "hp_ps_read_timing",
     "hp_vw_create", "hp_vw_destroy", "hp_wsp_weights", "hp_wsp_local_update",
     "hp_wsp_push_wave", "hp_wsp_pull", "hp_wsp_state", "hp_wsp_version", "hp_wsp_buffers",
     "hp_last_error",
@@ -81,6 +82,9 @@ def lib():
     L.hp_ps_destroy.argtypes = [_vp]
     L.hp_ps_weights.argtypes = [_vp, _pp]
     L.hp_ps_clock.argtypes = [_vp, ctypes.POINTER(i32)]
+    L.hp_ps_set_timing.argtypes = [_vp, i32]
+    L.hp_ps_read_timing.argtypes = [_vp, ctypes.POINTER(ctypes.c_double * 4),
+                                    ctypes.POINTER(ctypes.c_int64 * 4)]
     L.hp_vw_create.argtypes = [_vp, i32, i32, _pp]
     L.hp_vw_destroy.argtypes = [_vp]
     L.hp_wsp_weights.argtypes = [_vp, _pp]
@@ -224,6 +228,20 @@ class ParameterServer:
         c = ctypes.c_int()
         _check(self._L.hp_ps_clock(self.h, ctypes.byref(c)))
         return c.value
+
+    TIMING_CLASSES = ("update_first", "update", "push", "pull")
+
+    def set_timing(self, on=True):
+        _check(self._L.hp_ps_set_timing(self.h, 1 if on else 0))
+
+    def read_timing(self):
+        """({class: ms}, {class: launches}) of the WSP update kernels for the
+        classes in TIMING_CLASSES; resets the sums."""
+        ms = (ctypes.c_double * 4)()
+        n = (ctypes.c_int64 * 4)()
+        _check(self._L.hp_ps_read_timing(self.h, ctypes.byref(ms), ctypes.byref(n)))
+        return ({k: ms[i] for i, k in enumerate(self.TIMING_CLASSES)},
+                {k: int(n[i]) for i, k in enumerate(self.TIMING_CLASSES)})
 
 
 class VirtualWorker:
