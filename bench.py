@@ -11,8 +11,11 @@ Default workload: VGG-19 stage 1 (conv1_1 .. conv3_4 with two max-pools),
 batch 32 of 224x224x3 fp32 images, upstream gradient N(0, 1e-3^2), one
 virtual worker with s_local = 3.
 
-Prints one JSON line (metric, value = images/s, roofline of the dominant
-kernel class -- the implicit-GEMM contractions -- and the CPU oracle baseline).
+Prints one JSON line: metric, value = images/s over K timed steps run exactly
+as a user runs them, the roofline of the dominant kernel class (the
+implicit-GEMM contractions) and of the WSP update kernels, both from HIP
+events around every launch during K further steps of the same schedule, and
+the CPU oracle baseline.
 """
 import argparse
 import hashlib
@@ -182,10 +185,8 @@ def main():
     for _ in range(args.warmup):
         drv.minibatch(next_vw())
     torch.cuda.synchronize()
-    st.read_timing()                      # discard
-    drv.ps.read_timing()
-    st.set_timing(True)
-    drv.ps.set_timing(True)
+
+    # timed region: K steps exactly as a user runs them (no instrumentation)
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -198,6 +199,19 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ev_ms = start.elapsed_time(stop)
+
+    # kernel-timing pass: K more steps of the same schedule with HIP events
+    # recorded around every launch on the stream it is issued to (the library's
+    # stage and server timers); the per-kernel-class device times give the
+    # rooflines.  The events themselves cost a few microseconds per launch,
+    # which is why the throughput above is measured without them.
+    st.read_timing()                      # discard
+    drv.ps.read_timing()
+    st.set_timing(True)
+    drv.ps.set_timing(True)
+    for _ in range(args.steps):
+        drv.minibatch(next_vw())
+    torch.cuda.synchronize()
     ms, launches = st.read_timing()
     st.set_timing(False)
     ums, ulaunch = drv.ps.read_timing()
@@ -229,6 +243,7 @@ def main():
         "roofline": {"bound": "mfma", "achieved": round(achieved, 3), "peak": peak,
                      "unit": "TFLOP/s", "frac": round(achieved / peak, 4), "traffic": traffic,
                      "kernel": "implicit-GEMM conv/FC contractions (all launches of a step)",
+                     "timing": f"HIP events around every launch, {args.steps} further steps",
                      "flop_per_step": flops_step, "ms_per_step": round(gemm_ms_step, 4),
                      "launches_per_step": launches["contraction"] / args.steps},
         "other_kernels_ms_per_step": round(ms["other"] / args.steps, 4),

@@ -453,6 +453,27 @@ __global__ void bn_bwd_apply_kernel(const float* __restrict__ x, const float* __
     }
 }
 
+// bf16 copy, round to nearest even (the operand rounding of the bf16 contractions)
+__device__ __forceinline__ unsigned bf16_bits(float x) {
+    const unsigned u = __float_as_uint(x);
+    return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+}
+
+__global__ void cast_bf16_kernel(const float* __restrict__ src, uint16_t* __restrict__ dst,
+                                 size_t n, int vec) {
+    const size_t n4 = vec ? n / 4 : 0;
+    const size_t stride = (size_t)gridDim.x * blockDim.x;
+    const float4* s4 = reinterpret_cast<const float4*>(src);
+    uint2* d2 = reinterpret_cast<uint2*>(dst);
+    for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n4; i += stride) {
+        const float4 v = s4[i];
+        d2[i] = make_uint2(bf16_bits(v.x) | (bf16_bits(v.y) << 16),
+                           bf16_bits(v.z) | (bf16_bits(v.w) << 16));
+    }
+    for (size_t i = n4 * 4 + (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride)
+        dst[i] = (uint16_t)bf16_bits(src[i]);
+}
+
 // softmax cross-entropy: one workgroup per row
 __global__ void softmax_ce_kernel(const float* __restrict__ z, const int32_t* __restrict__ labels,
                                   int B, int K, float* __restrict__ row_loss,
@@ -667,6 +688,13 @@ hipError_t launch_bn_bwd(const float* x, const float* dy, const float* relu_y, l
     size_t n = (size_t)M * C;
     hipLaunchKernelGGL(bn_bwd_apply_kernel, dim3(ew_blocks(n)), dim3(EW_THREADS), 0, s, x, dy,
                        relu_y, M, C, gamma, mean, invstd, dbeta, dgamma, dx, accumulate);
+    return hipGetLastError();
+}
+
+hipError_t launch_cast_bf16(const float* src, uint16_t* dst, size_t n, hipStream_t s) {
+    const int vec = ((((uintptr_t)src) & 15) | (((uintptr_t)dst) & 7)) == 0;
+    hipLaunchKernelGGL(cast_bf16_kernel, dim3(ew_blocks(vec ? (n + 3) / 4 : n)), dim3(EW_THREADS), 0,
+                       s, src, dst, n, vec);
     return hipGetLastError();
 }
 

@@ -68,6 +68,10 @@ struct Node {
     GemmPlan fwd{}, dgrad{}, wgrad{};
     float* mean = nullptr;
     float* invstd = nullptr;
+    // bf16 mode: bf16 copy of this node's output, read by contractions that
+    // stage bf16 operands directly (made once per forward pass)
+    uint16_t* y16 = nullptr;
+    bool y16_ready = false;
 };
 
 size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
@@ -119,6 +123,12 @@ struct hp_stage {
     std::vector<void*> allocs;
     size_t bytes = 0;
     bool has_loss = false;
+    // bf16 mode with bf16 operands in memory: copies of the weights, of the
+    // stage input and (scratch, one conv at a time) of a conv's output gradient
+    uint16_t* w16 = nullptr;
+    uint16_t* x16 = nullptr;
+    uint16_t* g16 = nullptr;
+    bool x16_ready = false;
     // forward bookkeeping for backward
     const float* fwd_w = nullptr;
     const float* fwd_x = nullptr;
@@ -165,6 +175,13 @@ int dev_alloc(hp_stage* st, float** p, size_t floats) {
     st->bytes += floats * sizeof(float);
     *p = (float*)q;
     return HP_OK;
+}
+
+int dev_alloc16(hp_stage* st, uint16_t** p, size_t n) {
+    float* q = nullptr;
+    int rc = dev_alloc(st, &q, (n + 1) / 2);
+    *p = reinterpret_cast<uint16_t*>(q);
+    return rc;
 }
 
 int num_cus() {
@@ -333,6 +350,25 @@ int build_stage(hp_stage* st, const hp_layer* layers, int n_layers) {
             if ((rc = dev_alloc(st, &nd.invstd, nd.C))) return rc;
         }
     }
+    // bf16 operand copies for the contractions whose geometry allows them
+    size_t g16_elems = 0;
+    for (int i = 0; i < n_layers; ++i) {
+        Node& nd = st->nodes[i];
+        if ((nd.L.kind != HP_CONV && nd.L.kind != HP_FC) || !nd.fwd.h16) continue;
+        g16_elems = std::max(g16_elems, nd.out_elems);
+        const int j = nd.L.in0;
+        int rc = HP_OK;
+        if (j < 0 && !st->x16)
+            rc = dev_alloc16(st, &st->x16, (size_t)st->batch * st->H * st->W * st->C);
+        else if (j >= 0 && !st->nodes[j].y16)
+            rc = dev_alloc16(st, &st->nodes[j].y16, st->nodes[j].out_elems);
+        if (rc) return rc;
+    }
+    if (g16_elems) {
+        int rc = dev_alloc16(st, &st->w16, st->P);
+        if (!rc) rc = dev_alloc16(st, &st->g16, g16_elems);
+        if (rc) return rc;
+    }
     return dev_alloc(st, &st->ws, std::max<size_t>(st->ws_floats, 64));
 }
 
@@ -450,12 +486,37 @@ extern "C" int hp_stage_forward(hp_stage* st, const float* w, const float* x, fl
     if (!st->has_loss && !y) return fail(HP_ERR_ARG, "hp_stage_forward: y is NULL");
     hipStream_t s = st->stream;
     const int B = st->batch;
+    st->x16_ready = false;
+    for (Node& nd : st->nodes) nd.y16_ready = false;
+    if (st->w16) {
+        st->timer.begin(1, s);
+        hipError_t e = launch_cast_bf16(w, st->w16, st->P, s);
+        st->timer.end(s);
+        int rc = launch_ok(e, "weight cast", -1);
+        if (rc) return rc;
+    }
     for (size_t i = 0; i < st->nodes.size(); ++i) {
         Node& nd = st->nodes[i];
         const hp_layer& L = nd.L;
         const float* in = L.in0 < 0 ? x : st->nodes[L.in0].y;
         hipError_t e = hipSuccess;
         StageTimer& tm = st->timer;
+        const uint16_t* in16 = nullptr;
+        if ((L.kind == HP_CONV || L.kind == HP_FC) && nd.fwd.h16 && st->w16) {
+            // bf16 copy of the input value, made by its first contraction consumer
+            in16 = L.in0 < 0 ? st->x16 : st->nodes[L.in0].y16;
+            bool& ready = L.in0 < 0 ? st->x16_ready : st->nodes[L.in0].y16_ready;
+            if (!ready) {
+                const size_t n_in = L.in0 < 0 ? (size_t)B * st->H * st->W * st->C
+                                              : st->nodes[L.in0].out_elems;
+                tm.begin(1, s);
+                e = launch_cast_bf16(in, const_cast<uint16_t*>(in16), n_in, s);
+                tm.end(s);
+                int rc = launch_ok(e, "activation cast", (int)i);
+                if (rc) return rc;
+                ready = true;
+            }
+        }
         tm.begin(L.kind == HP_CONV || L.kind == HP_FC ? 0 : 1, s);
         switch (L.kind) {
             case HP_CONV:
@@ -463,7 +524,8 @@ extern "C" int hp_stage_forward(hp_stage* st, const float* w, const float* x, fl
                 Epilogue ep;
                 ep.flags = (L.bias ? EPI_BIAS : 0) | (nd.fuses_relu ? EPI_RELU : 0);
                 ep.bias = L.bias ? w + nd.b_off : nullptr;
-                e = launch_gemm(nd.fwd, nd.geo, in, w + nd.w_off, nd.y, ep, st->ws, s);
+                e = launch_gemm(nd.fwd, nd.geo, in, w + nd.w_off, nd.y, ep, st->ws, s, in16,
+                                in16 ? st->w16 + nd.w_off : nullptr);
                 break;
             }
             case HP_RELU:
@@ -562,10 +624,21 @@ extern "C" int hp_stage_backward(hp_stage* st, const float* w, const float* dy, 
             case HP_CONV:
             case HP_FC: {
                 StageTimer& tm = st->timer;
+                const uint16_t* in16 = nullptr;
+                const uint16_t* g16 = nullptr;
+                if (nd.fwd.h16 && st->w16) {
+                    in16 = L.in0 < 0 ? st->x16 : st->nodes[L.in0].y16;
+                    tm.begin(1, s);
+                    e = launch_cast_bf16(gin, st->g16, nd.out_elems, s);
+                    tm.end(s);
+                    g16 = st->g16;
+                }
                 tm.begin(0, s);
                 Epilogue wep;                     // bias gradient = appended column
                 wep.bias_out = nd.bias_in_wgrad ? grad + nd.b_off : nullptr;
-                e = launch_gemm(nd.wgrad, nd.geo, in, gin, grad + nd.w_off, wep, st->ws, s);
+                if (e == hipSuccess)
+                    e = launch_gemm(nd.wgrad, nd.geo, in, gin, grad + nd.w_off, wep, st->ws, s,
+                                    in16, g16);
                 tm.end(s);
                 if (e == hipSuccess && L.bias && !nd.bias_in_wgrad) {
                     tm.begin(1, s);
@@ -581,7 +654,8 @@ extern "C" int hp_stage_backward(hp_stage* st, const float* w, const float* dy, 
                         dep.mask = st->nodes[L.in0].y;
                     }
                     tm.begin(0, s);
-                    e = launch_gemm(nd.dgrad, nd.geo, gin, w + nd.w_off, d, dep, st->ws, s);
+                    e = launch_gemm(nd.dgrad, nd.geo, gin, w + nd.w_off, d, dep, st->ws, s, g16,
+                                    g16 ? st->w16 + nd.w_off : nullptr);
                     tm.end(s);
                 }
                 break;

@@ -65,6 +65,8 @@ struct KArgs {
     int kchunk;       // reduction length of a chunk (multiple of the K tile)
     float* ws;        // partial tiles of the cut tiles: [tile - tfull][split][BM * BN]
     int epi;
+    const unsigned short* a16;   // bf16 copies of a and b (16-bit operand kernel only)
+    const unsigned short* b16;
 };
 
 // Destination of output element (row, col): the bias-gradient column of a
@@ -136,33 +138,67 @@ __device__ __forceinline__ Work decode_work(const KArgs& args) {
 // Writes a wave's accumulators: acc[i][j][v] holds
 // out[m0 + wm + 32i + 8(v/4) + 4(lane/32) + v%4][n0 + wn + 32j + lane%32]
 // (the output layout of the 32x32 MFMAs), through the epilogue, or raw into
-// the workspace slot of a cut tile.
+// the workspace slot of a cut tile.  The epilogue's reads (the previous
+// output to accumulate into, the ReLU mask) of one 32x32 tile are all issued
+// before its stores: a store may alias a later read as far as the compiler
+// knows, so interleaving them would serialise one memory latency per element.
+constexpr int EPI_CHUNK = 8;     // outputs per lane whose epilogue reads are batched
+
 template <int BM, int BN, int TM, int TN>
 __device__ __forceinline__ void store_tile(const KArgs& args, const Work& w,
                                            const floatx16 (&acc)[TM][TN], int wm, int wn,
                                            int lane) {
     const int lr = lane & 31, lk = lane >> 5;
-    float* pslot = w.partial
-                       ? args.ws + ((long)(w.tile - args.tfull) * args.splits + w.z) * (BM * BN)
-                       : nullptr;
+    if (w.partial) {
+        float* pslot = args.ws + ((long)(w.tile - args.tfull) * args.splits + w.z) * (BM * BN);
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+            const int lcol = wn + 32 * j + lr;
+            if (w.n0 + lcol >= args.Ncols) continue;
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) {
+                    const int lrow = wm + 32 * i + 8 * (v >> 2) + 4 * lk + (v & 3);
+                    if (w.m0 + lrow < args.M) pslot[lrow * BN + lcol] = acc[i][j][v];
+                }
+        }
+        return;
+    }
+    const int epi = args.epi;
 #pragma unroll
     for (int j = 0; j < TN; ++j) {
-        const int lcol = wn + 32 * j + lr;
-        const long col = w.n0 + lcol;
+        const long col = w.n0 + wn + 32 * j + lr;
         if (col >= args.Ncols) continue;
 #pragma unroll
         for (int i = 0; i < TM; ++i) {
+            const long row0 = w.m0 + wm + 32 * i + 4 * lk;
 #pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                const int lrow = wm + 32 * i + 8 * (v >> 2) + 4 * lk + (v & 3);
-                const long row = w.m0 + lrow;
-                if (row >= args.M) continue;
-                float val = acc[i][j][v];
-                if (w.partial) {
-                    pslot[lrow * BN + lcol] = val;
-                } else {
-                    float* dst = out_ptr(args.out, args.bias_out, row, col, args.Ncols, args.epi);
-                    *dst = epilogue(val, row, col, args.Ncols, args.epi, args.bias, args.mask, dst);
+            for (int v0 = 0; v0 < 16; v0 += EPI_CHUNK) {
+                float prev[EPI_CHUNK], msk[EPI_CHUNK];
+#pragma unroll
+                for (int u = 0; u < EPI_CHUNK; ++u) {
+                    const int v = v0 + u;
+                    const long row = row0 + 8 * (v >> 2) + (v & 3);
+                    prev[u] = 0.f;
+                    msk[u] = 1.f;
+                    if (row < args.M) {
+                        if (epi & EPI_ACCUM)
+                            prev[u] = *out_ptr(args.out, args.bias_out, row, col, args.Ncols, epi);
+                        if (epi & EPI_MASK) msk[u] = args.mask[row * args.Ncols + col];
+                    }
+                }
+#pragma unroll
+                for (int u = 0; u < EPI_CHUNK; ++u) {
+                    const int v = v0 + u;
+                    const long row = row0 + 8 * (v >> 2) + (v & 3);
+                    if (row >= args.M) continue;
+                    float val = acc[i][j][v];
+                    if (epi & EPI_BIAS) val += args.bias[col];
+                    if (epi & EPI_RELU) val = fmaxf(val, 0.f);
+                    if ((epi & EPI_MASK) && !(msk[u] > 0.f)) val = 0.f;
+                    if (epi & EPI_ACCUM) val += prev[u];
+                    *out_ptr(args.out, args.bias_out, row, col, args.Ncols, epi) = val;
                 }
             }
         }
@@ -818,6 +854,297 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_bf16_kern
 }
 
 
+// ---- bf16 kernel on bf16 operands -------------------------------------------
+// The bf16 contractions when both operands are already rounded to bf16 in
+// memory (a16 / b16): same LDS layout and MFMA loop as igemm_bf16_kernel, but
+// the staging moves bf16 bits straight to LDS.  k-major operands load 8
+// consecutive k (16 bytes) of a row and store them with one 16-byte LDS
+// write; m-major operands load 4 x 4 blocks (4 reduction rows of 4 columns, 8
+// bytes each) and transpose them in registers.  Used only when every
+// contiguous axis is a multiple of 8 elements and the operands are 16-byte
+// aligned, so there is no scalar path and no bias column.
+template <int OP, int BM, int BN, int WM, int WN>
+__global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_h16_kernel(KArgs args) {
+    constexpr int NT = 64 * (BM / WM) * (BN / WN);
+    constexpr int TM = WM / 32, TN = WN / 32;
+    constexpr bool A_KMAJ = (OP != OP_WGRAD);
+    constexpr bool B_KMAJ = (OP == OP_FWD);
+    constexpr int WAVES_N = BN / WN;
+    constexpr int KG = BKH / 8;                  // 8-k groups per k-major row
+    constexpr int GA = BM * KG / NT;             // k-major groups per thread
+    constexpr int GB = BN * KG / NT;
+    constexpr int CGA = BM / 4, CGB = BN / 4;    // column groups of an m-major operand
+    constexpr int PA = (2 * BM + NT - 1) / NT;   // m-major 4x4 blocks per thread
+    constexpr int PB = (2 * BN + NT - 1) / NT;
+    static_assert(GA >= 1 && GB >= 1 && NT % KG == 0 && NT % CGA == 0 && NT % CGB == 0,
+                  "tile shape");
+    __shared__ __attribute__((aligned(16))) unsigned short smem[2 * (BM + BN) * LDH];
+
+    const ConvGeo& g = args.g;
+    const int t = threadIdx.x;
+    const int lane = t & 63;
+    const int wave = t >> 6;
+    const int wm = (wave / WAVES_N) * WM;
+    const int wn = (wave % WAVES_N) * WN;
+    const Work wk = decode_work<BM, BN>(args);
+    const int ktiles = (int)((wk.kend - wk.kbeg + BKH - 1) / BKH);
+    const int kg = (t % KG) * 8;
+    const bool a_act = A_KMAJ || 2 * BM >= NT || t < 2 * BM;
+    const bool b_act = B_KMAJ || 2 * BN >= NT || t < 2 * BN;
+    const unsigned short* A = args.a16;
+    const unsigned short* Bm = args.b16;
+
+    int arow_base[GA], arow_h[GA], arow_w[GA];
+    bool arow_ok[GA];
+    long acol = 0;
+    if constexpr (A_KMAJ) {
+#pragma unroll
+        for (int i = 0; i < GA; ++i) {
+            const long m = wk.m0 + t / KG + i * (NT / KG);
+            arow_ok[i] = m < args.M;
+            const long mm = arow_ok[i] ? m : 0;
+            if constexpr (OP == OP_FWD) {
+                int q = (int)(mm % g.Q); long tt = mm / g.Q;
+                int p = (int)(tt % g.P); int n = (int)(tt / g.P);
+                arow_base[i] = n * g.H * g.W * g.C;
+                arow_h[i] = p * g.st - g.pad;
+                arow_w[i] = q * g.st - g.pad;
+            } else {
+                int w = (int)(mm % g.W); long tt = mm / g.W;
+                int h = (int)(tt % g.H); int n = (int)(tt / g.H);
+                arow_base[i] = n * g.P * g.Q * g.K;
+                arow_h[i] = h + g.pad;
+                arow_w[i] = w + g.pad;
+            }
+        }
+    } else {
+        acol = wk.m0 + (t % CGA) * 4;
+    }
+    long brow_n[GB];
+    bool brow_ok[GB];
+    long bcol = 0;
+    int bcol_r = 0, bcol_s = 0, bcol_c = 0;
+    bool bcol_ok = false;
+    if constexpr (B_KMAJ) {
+#pragma unroll
+        for (int i = 0; i < GB; ++i) {
+            const long n = wk.n0 + t / KG + i * (NT / KG);
+            brow_ok[i] = n < args.Ncols;
+            brow_n[i] = brow_ok[i] ? n : 0;
+        }
+    } else {
+        bcol = wk.n0 + (t % CGB) * 4;
+        bcol_ok = bcol < args.Ncols;
+        const long cc = bcol_ok ? bcol : 0;
+        if constexpr (OP == OP_WGRAD) {
+            bcol_c = (int)(cc % g.C); long tt = cc / g.C;
+            bcol_s = (int)(tt % g.S); bcol_r = (int)(tt / g.S);
+        } else {
+            bcol_c = (int)cc;
+        }
+    }
+
+    uintx4 areg_k[A_KMAJ ? GA : 1], breg_k[B_KMAJ ? GB : 1];
+    uintx2 areg_m[A_KMAJ ? 1 : 4 * PA], breg_m[B_KMAJ ? 1 : 4 * PB];
+
+    auto ld16 = [](const unsigned short* p, bool ok) -> uintx4 {
+        return ok ? *reinterpret_cast<const uintx4*>(p) : uintx4{0u, 0u, 0u, 0u};
+    };
+    auto ld8 = [](const unsigned short* p, bool ok) -> uintx2 {
+        return ok ? *reinterpret_cast<const uintx2*>(p) : uintx2{0u, 0u};
+    };
+
+    auto gload = [&](int kt) {
+        const int k0 = (int)(wk.kbeg + (long)kt * BKH);
+        const int kend_i = (int)wk.kend;
+        if constexpr (OP == OP_FWD || OP == OP_DGRAD) {
+            const int CC = (OP == OP_FWD) ? g.C : g.K;
+            const int rs0 = k0 / CC;
+            const int c0 = k0 - rs0 * CC;
+            const int r0 = rs0 / g.S;
+            const int s0 = rs0 - r0 * g.S;
+            {
+                int c = c0 + kg, r = r0, sx = s0;
+                while (c >= CC) { c -= CC; if (++sx == g.S) { sx = 0; ++r; } }
+                const bool kin = k0 + kg < kend_i;
+#pragma unroll
+                for (int i = 0; i < GA; ++i) {
+                    bool ok;
+                    long off;
+                    if constexpr (OP == OP_FWD) {
+                        const int h = arow_h[i] + r, w = arow_w[i] + sx;
+                        ok = arow_ok[i] && kin && (unsigned)h < (unsigned)g.H &&
+                             (unsigned)w < (unsigned)g.W;
+                        off = arow_base[i] + ((long)h * g.W + w) * g.C + c;
+                    } else {
+                        const int tp = arow_h[i] - r, tq = arow_w[i] - sx;
+                        int p = tp, q = tq;
+                        bool on_grid = true;
+                        if (g.st != 1) {
+                            p = tp / g.st;
+                            q = tq / g.st;
+                            on_grid = p * g.st == tp && q * g.st == tq;
+                        }
+                        ok = arow_ok[i] && kin && tp >= 0 && tq >= 0 && on_grid && p < g.P &&
+                             q < g.Q;
+                        off = arow_base[i] + ((long)p * g.Q + q) * g.K + c;
+                    }
+                    areg_k[i] = ld16(A + (ok ? off : 0), ok);
+                }
+            }
+            if constexpr (OP == OP_FWD) {
+                const int kk = k0 + kg;
+#pragma unroll
+                for (int i = 0; i < GB; ++i) {
+                    const bool ok = brow_ok[i] && kk < kend_i;
+                    breg_k[i] = ld16(Bm + (ok ? (brow_n[i] * args.Kred + kk) : 0), ok);
+                }
+            } else if (b_act) {     // B[kk = (r,s,k)][c] = w[k][r][s][c]
+#pragma unroll
+                for (int i = 0; i < PB; ++i) {
+                    const int kq = ((t + i * NT) / CGB) * 4;
+                    int k = c0 + kq, r = r0, sx = s0;
+                    while (k >= CC) { k -= CC; if (++sx == g.S) { sx = 0; ++r; } }
+#pragma unroll
+                    for (int jr = 0; jr < 4; ++jr) {
+                        if (jr > 0 && ++k == CC) { k = 0; if (++sx == g.S) { sx = 0; ++r; } }
+                        const bool ok = bcol_ok && k0 + kq + jr < kend_i;
+                        const long off = (((long)k * g.R + r) * g.S + sx) * g.C + bcol_c;
+                        breg_m[4 * i + jr] = ld8(Bm + (ok ? off : 0), ok);
+                    }
+                }
+            }
+        } else {
+            if (a_act) {            // A[kk][m] = dy[kk][m]
+#pragma unroll
+                for (int i = 0; i < PA; ++i) {
+                    const int kq = ((t + i * NT) / CGA) * 4;
+#pragma unroll
+                    for (int jr = 0; jr < 4; ++jr) {
+                        const int kk = k0 + kq + jr;
+                        const bool ok = kk < kend_i && acol < args.M;
+                        areg_m[4 * i + jr] = ld8(Bm + (ok ? (long)kk * g.K + acol : 0), ok);
+                    }
+                }
+            }
+            if (b_act) {            // B[kk = (n,p,q)][j = (r,s,c)] = x[n, p*st-pad+r, q*st-pad+s, c]
+                const int q0 = k0 % g.Q;
+                const int t0 = k0 / g.Q;
+                const int p0 = t0 % g.P;
+                const int n0i = t0 / g.P;
+#pragma unroll
+                for (int i = 0; i < PB; ++i) {
+                    const int kq = ((t + i * NT) / CGB) * 4;
+                    int q = q0 + kq, p = p0, n = n0i;
+                    while (q >= g.Q) { q -= g.Q; if (++p == g.P) { p = 0; ++n; } }
+#pragma unroll
+                    for (int jr = 0; jr < 4; ++jr) {
+                        if (jr > 0 && ++q == g.Q) { q = 0; if (++p == g.P) { p = 0; ++n; } }
+                        const int h = p * g.st - g.pad + bcol_r;
+                        const int w = q * g.st - g.pad + bcol_s;
+                        const bool ok = bcol_ok && k0 + kq + jr < kend_i &&
+                                        (unsigned)h < (unsigned)g.H && (unsigned)w < (unsigned)g.W;
+                        const long off = (((long)n * g.H + h) * g.W + w) * g.C + bcol_c;
+                        breg_m[4 * i + jr] = ld8(A + (ok ? off : 0), ok);
+                    }
+                }
+            }
+        }
+    };
+
+    // column c (0..3) of four 4-element rows, as two (row j, row j+1) pairs
+    auto col_pairs = [](const uintx2* rows, int c) -> uintx2 {
+        auto el = [&](int j) -> unsigned {
+            const unsigned w = (c < 2) ? rows[j].x : rows[j].y;
+            return (c & 1) ? (w >> 16) : (w & 0xFFFFu);
+        };
+        return uintx2{el(0) | (el(1) << 16), el(2) | (el(3) << 16)};
+    };
+
+    auto sstore = [&](int buf) {
+        unsigned short* As = smem + buf * (BM + BN) * LDH;
+        unsigned short* Bs = As + BM * LDH;
+        if constexpr (A_KMAJ) {
+#pragma unroll
+            for (int i = 0; i < GA; ++i) {
+                const int row = t / KG + i * (NT / KG);
+                *reinterpret_cast<uintx4*>(As + row * LDH + kg) = areg_k[i];
+            }
+        } else if (a_act) {
+#pragma unroll
+            for (int i = 0; i < PA; ++i) {
+                const int kq = ((t + i * NT) / CGA) * 4;
+#pragma unroll
+                for (int c = 0; c < 4; ++c) {
+                    const int col = (t % CGA) * 4 + c;
+                    *reinterpret_cast<uintx2*>(As + col * LDH + kq) = col_pairs(&areg_m[4 * i], c);
+                }
+            }
+        }
+        if constexpr (B_KMAJ) {
+#pragma unroll
+            for (int i = 0; i < GB; ++i) {
+                const int row = t / KG + i * (NT / KG);
+                *reinterpret_cast<uintx4*>(Bs + row * LDH + kg) = breg_k[i];
+            }
+        } else if (b_act) {
+#pragma unroll
+            for (int i = 0; i < PB; ++i) {
+                const int kq = ((t + i * NT) / CGB) * 4;
+#pragma unroll
+                for (int c = 0; c < 4; ++c) {
+                    const int col = (t % CGB) * 4 + c;
+                    *reinterpret_cast<uintx2*>(Bs + col * LDH + kq) = col_pairs(&breg_m[4 * i], c);
+                }
+            }
+        }
+    };
+
+    floatx16 acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+
+    if (ktiles > 0) {
+        gload(0);
+        sstore(0);
+    }
+    __syncthreads();
+    const int lr = lane & 31;
+    const int lk = lane >> 5;
+    for (int kt = 0; kt < ktiles; ++kt) {
+        const int buf = kt & 1;
+        if (kt + 1 < ktiles) gload(kt + 1);
+        const unsigned short* As = smem + buf * (BM + BN) * LDH;
+        const unsigned short* Bs = As + BM * LDH;
+#pragma unroll
+        for (int kk = 0; kk < BKH; kk += 16) {
+            bf16x8 av[TM], bv[TN];
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+                av[i] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uintx4*>(
+                                                       As + (wm + 32 * i + lr) * LDH + kk + 8 * lk));
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+                bv[j] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uintx4*>(
+                                                       Bs + (wn + 32 * j + lr) * LDH + kk + 8 * lk));
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int j = 0; j < TN; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[i], bv[j], acc[i][j], 0,
+                                                                         0, 0);
+        }
+        if (kt + 1 < ktiles) sstore(buf ^ 1);
+        __syncthreads();
+    }
+    store_tile<BM, BN, TM, TN>(args, wk, acc, wm, wn, lane);
+}
+
+
 // Reduction of the cut tiles: workgroup = 64 elements of one tile x 16 split
 // lanes; lane l adds splits l, l+16, ...; the lane sums are combined in a
 // fixed order (deterministic), then the epilogue runs.
@@ -869,12 +1196,20 @@ __global__ void __launch_bounds__(256) igemm_cut_reduce_kernel(KArgs args, int B
             acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
         }
         const float a4[4] = {acc.x, acc.y, acc.z, acc.w};
+        float prev[4] = {0.f, 0.f, 0.f, 0.f};
+        // epilogue reads first (see store_tile)
+        if (args.epi & EPI_ACCUM) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                if (col0 + j < args.Ncols)
+                    prev[j] = *out_ptr(args.out, args.bias_out, row, col0 + j, args.Ncols, args.epi);
+        }
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             const long col = col0 + j;
             if (col >= args.Ncols) break;
             float* dst = out_ptr(args.out, args.bias_out, row, col, args.Ncols, args.epi);
-            *dst = epilogue(a4[j], row, col, args.Ncols, args.epi, args.bias, args.mask, dst);
+            *dst = epilogue(a4[j], row, col, args.Ncols, args.epi, args.bias, args.mask, prev + j);
         }
     }
 }
@@ -888,7 +1223,9 @@ template <int OP, int CFG, int VW, bool BF>
 KernelRef kref() {
     constexpr TileCfg c = kCfgs[CFG];
     constexpr int nt = 64 * (c.bm / c.wm) * (c.bn / c.wn);
-    if constexpr (BF)
+    if constexpr (VW == 8)
+        return {reinterpret_cast<const void*>(&igemm_h16_kernel<OP, c.bm, c.bn, c.wm, c.wn>), nt};
+    else if constexpr (BF)
         return {reinterpret_cast<const void*>(&igemm_bf16_kernel<OP, c.bm, c.bn, c.wm, c.wn, VW>),
                 nt};
     else
@@ -897,7 +1234,8 @@ KernelRef kref() {
 }
 
 // Every configuration is instantiated with vector width 4 (channel counts
-// divisible by 4, aligned operands) and 1 (everything else).
+// divisible by 4, aligned operands) and 1 (everything else); bf16 also with
+// bf16 operands in memory ("vector width" 8).
 template <int OP, int VW, bool BF>
 KernelRef kref_cfg(int cfg) {
     switch (cfg) {
@@ -909,16 +1247,18 @@ KernelRef kref_cfg(int cfg) {
     }
 }
 
+// vw: 1, 4, or 8 (bf16 only: operands already bf16 in memory)
 template <int OP>
-KernelRef kref_op(int cfg, bool v4, bool bf) {
-    if (v4) return bf ? kref_cfg<OP, 4, true>(cfg) : kref_cfg<OP, 4, false>(cfg);
+KernelRef kref_op(int cfg, int vw, bool bf) {
+    if (bf && vw == 8) return kref_cfg<OP, 8, true>(cfg);
+    if (vw == 4) return bf ? kref_cfg<OP, 4, true>(cfg) : kref_cfg<OP, 4, false>(cfg);
     return bf ? kref_cfg<OP, 1, true>(cfg) : kref_cfg<OP, 1, false>(cfg);
 }
 
-KernelRef kernel_for(int op, int cfg, bool v4, bool bf) {
-    if (op == OP_FWD) return kref_op<OP_FWD>(cfg, v4, bf);
-    if (op == OP_DGRAD) return kref_op<OP_DGRAD>(cfg, v4, bf);
-    return kref_op<OP_WGRAD>(cfg, v4, bf);
+KernelRef kernel_for(int op, int cfg, int vw, bool bf) {
+    if (op == OP_FWD) return kref_op<OP_FWD>(cfg, vw, bf);
+    if (op == OP_DGRAD) return kref_op<OP_DGRAD>(cfg, vw, bf);
+    return kref_op<OP_WGRAD>(cfg, vw, bf);
 }
 
 // Tile configuration for a contraction of M x N (x Kred): the 128x128 tile
@@ -946,6 +1286,8 @@ GemmPlan plan_gemm(int op, const ConvGeo& g, int bf16, int num_cus, int bias_col
         p.Kred = (long)g.N * g.P * g.Q;
     }
     const bool v4 = (op == OP_FWD) ? (g.C % 4 == 0) : (g.C % 4 == 0 && g.K % 4 == 0);
+    // bf16 operands in memory: every contiguous axis a multiple of 8 (16 bytes)
+    p.h16 = (bf16 && g.C % 8 == 0 && g.K % 8 == 0) ? 1 : 0;
     p.cfg = choose_cfg(p.M, p.Ncols);
     if (p.bias_col) {
         // the bias-gradient column rides along unless it adds more than 10% of
@@ -964,7 +1306,7 @@ GemmPlan plan_gemm(int op, const ConvGeo& g, int bf16, int num_cus, int bias_col
     const int bk = bf16 ? BKH : c.bk;
     const long ktiles = (p.Kred + bk - 1) / bk;
     // workgroups resident at once
-    KernelRef kr = kernel_for(op, p.cfg, v4, bf16 != 0);
+    KernelRef kr = kernel_for(op, p.cfg, p.h16 ? 8 : (v4 ? 4 : 1), bf16 != 0);
     int occ = 0;
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, kr.fn, kr.nt, 0) != hipSuccess || occ < 1)
         occ = 1;
@@ -996,7 +1338,8 @@ GemmPlan plan_gemm(int op, const ConvGeo& g, int bf16, int num_cus, int bias_col
 }
 
 hipError_t launch_gemm(const GemmPlan& plan, const ConvGeo& g, const float* a, const float* b,
-                       float* out, const Epilogue& ep, float* ws, hipStream_t s) {
+                       float* out, const Epilogue& ep, float* ws, hipStream_t s,
+                       const uint16_t* a16, const uint16_t* b16) {
     KArgs k{};
     k.g = g;
     k.a = a;
@@ -1013,6 +1356,8 @@ hipError_t launch_gemm(const GemmPlan& plan, const ConvGeo& g, const float* a, c
     k.splits = plan.splits;
     k.kchunk = plan.kchunk;
     k.ws = ws;
+    k.a16 = a16;
+    k.b16 = b16;
     const TileCfg& c = kCfgs[plan.cfg];
     k.tiles_m = (int)((plan.M + c.bm - 1) / c.bm);
     k.tiles_n = (int)((plan.Ncols + c.bn - 1) / c.bn);
@@ -1020,7 +1365,9 @@ hipError_t launch_gemm(const GemmPlan& plan, const ConvGeo& g, const float* a, c
     // operand bases 16-byte aligned
     bool v4 = (plan.op == OP_FWD) ? (g.C % 4 == 0) : (g.C % 4 == 0 && g.K % 4 == 0);
     v4 = v4 && ((((uintptr_t)a) | ((uintptr_t)b)) & 15) == 0;
-    KernelRef kr = kernel_for(plan.op, plan.cfg, v4, plan.bf16 != 0);
+    const bool h16 = plan.h16 && plan.bf16 && !plan.bias_col && a16 && b16 &&
+                     ((((uintptr_t)a16) | ((uintptr_t)b16)) & 15) == 0;
+    KernelRef kr = kernel_for(plan.op, plan.cfg, h16 ? 8 : (v4 ? 4 : 1), plan.bf16 != 0);
     void* kargs[] = {&k};
     hipError_t e = hipLaunchKernel(kr.fn, dim3(plan.nwg), dim3(kr.nt), kargs, 0, s);
     const int cut = k.tiles_m * k.tiles_n - plan.tfull;

@@ -24,6 +24,7 @@ enum GemmOp { OP_FWD = 0, OP_DGRAD = 1, OP_WGRAD = 2 };
 struct GemmPlan {
     int op;
     int bf16;          // round operands to bf16 (RNE) when staging
+    int h16;           // bf16: the geometry allows bf16 operands in memory (launch_gemm a16/b16)
     int bias_col;      // OP_WGRAD: Ncols includes the bias-gradient column
     int cfg;           // tile configuration
     int tfull;         // tiles computed whole (one workgroup each)
@@ -55,9 +56,15 @@ struct Epilogue {
     float* bias_out = nullptr;
 };
 
+// a16 / b16 (bf16 plans with plan.h16, optional): the same operands already
+// rounded to bf16, 16-byte aligned; when given, the kernel stages them directly.
 hipError_t launch_gemm(const GemmPlan& plan, const ConvGeo& g, const float* a,
                        const float* b, float* out, const Epilogue& ep, float* ws,
-                       hipStream_t s);
+                       hipStream_t s, const uint16_t* a16 = nullptr,
+                       const uint16_t* b16 = nullptr);
+
+// dst[i] = bf16(src[i]) (round to nearest even), n elements
+hipError_t launch_cast_bf16(const float* src, uint16_t* dst, size_t n, hipStream_t s);
 
 // ---- element-wise / reduction kernels (elementwise.hip) -------------------
 // y = max(x, 0)
