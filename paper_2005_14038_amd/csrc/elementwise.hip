@@ -19,9 +19,52 @@ namespace {
 
 constexpr int EW_THREADS = 256;
 
+inline bool aligned16(std::initializer_list<const void*> ptrs) {
+    for (const void* q : ptrs)
+        if (((uintptr_t)q) & 15) return false;
+    return true;
+}
+
 inline int ew_blocks(size_t n) {
     size_t b = (n + EW_THREADS - 1) / EW_THREADS;
     return (int)(b < 16384 ? (b ? b : 1) : 16384);
+}
+
+// ---- vector helpers: VEC consecutive floats (float4 when VEC == 4) ---------
+template <int VEC>
+__device__ __forceinline__ void ldv(const float* p, float* o) {
+    if constexpr (VEC == 4) {
+        const float4 t = *reinterpret_cast<const float4*>(p);
+        o[0] = t.x; o[1] = t.y; o[2] = t.z; o[3] = t.w;
+    } else {
+        o[0] = *p;
+    }
+}
+
+template <int VEC>
+__device__ __forceinline__ void stv(float* p, const float* v) {
+    if constexpr (VEC == 4) {
+        *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
+    } else {
+        *p = v[0];
+    }
+}
+
+// bf16 copy, round to nearest even (the operand rounding of the bf16 contractions)
+__device__ __forceinline__ unsigned bf16_bits(float x) {
+    const unsigned u = __float_as_uint(x);
+    return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+}
+
+// VEC values as bf16 to p (8-byte store when VEC == 4)
+template <int VEC>
+__device__ __forceinline__ void st16v(uint16_t* p, const float* v) {
+    if constexpr (VEC == 4) {
+        *reinterpret_cast<uint2*>(p) = make_uint2(bf16_bits(v[0]) | (bf16_bits(v[1]) << 16),
+                                                  bf16_bits(v[2]) | (bf16_bits(v[3]) << 16));
+    } else {
+        *p = (uint16_t)bf16_bits(v[0]);
+    }
 }
 
 __global__ void relu_fwd_kernel(const float* __restrict__ x, float* __restrict__ y, size_t n) {
@@ -30,35 +73,64 @@ __global__ void relu_fwd_kernel(const float* __restrict__ x, float* __restrict__
         y[i] = fmaxf(x[i], 0.f);
 }
 
+template <int VEC>
 __global__ void relu_bwd_kernel(const float* __restrict__ y, const float* __restrict__ dy,
                                 float* __restrict__ dx, size_t n, int acc) {
-    for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
-         i += (size_t)gridDim.x * blockDim.x) {
-        float v = y[i] > 0.f ? dy[i] : 0.f;
-        dx[i] = acc ? dx[i] + v : v;
+    for (size_t i = ((size_t)blockIdx.x * blockDim.x + threadIdx.x) * VEC; i < n;
+         i += (size_t)gridDim.x * blockDim.x * VEC) {
+        float yv[VEC], g[VEC], d[VEC];
+        ldv<VEC>(y + i, yv);
+        ldv<VEC>(dy + i, g);
+        if (acc) ldv<VEC>(dx + i, d);
+#pragma unroll
+        for (int j = 0; j < VEC; ++j) {
+            const float v = yv[j] > 0.f ? g[j] : 0.f;
+            d[j] = acc ? d[j] + v : v;
+        }
+        stv<VEC>(dx + i, d);
     }
 }
 
+template <int VEC>
 __global__ void add_fwd_kernel(const float* __restrict__ a, const float* __restrict__ b,
-                               float* __restrict__ y, size_t n, int relu) {
-    for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
-         i += (size_t)gridDim.x * blockDim.x) {
-        float v = a[i] + b[i];
-        y[i] = relu ? fmaxf(v, 0.f) : v;
+                               float* __restrict__ y, size_t n, int relu,
+                               uint16_t* __restrict__ y16) {
+    for (size_t i = ((size_t)blockIdx.x * blockDim.x + threadIdx.x) * VEC; i < n;
+         i += (size_t)gridDim.x * blockDim.x * VEC) {
+        float av[VEC], bv[VEC];
+        ldv<VEC>(a + i, av);
+        ldv<VEC>(b + i, bv);
+#pragma unroll
+        for (int j = 0; j < VEC; ++j) {
+            const float v = av[j] + bv[j];
+            av[j] = relu ? fmaxf(v, 0.f) : v;
+        }
+        stv<VEC>(y + i, av);
+        if (y16) st16v<VEC>(y16 + i, av);
     }
 }
 
+template <int VEC>
 __global__ void copy_or_acc_kernel(const float* __restrict__ v, float* __restrict__ out, size_t n,
                                    int acc) {
-    for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
-         i += (size_t)gridDim.x * blockDim.x)
-        out[i] = acc ? out[i] + v[i] : v[i];
+    for (size_t i = ((size_t)blockIdx.x * blockDim.x + threadIdx.x) * VEC; i < n;
+         i += (size_t)gridDim.x * blockDim.x * VEC) {
+        float a[VEC], o[VEC];
+        ldv<VEC>(v + i, a);
+        if (acc) {
+            ldv<VEC>(out + i, o);
+#pragma unroll
+            for (int j = 0; j < VEC; ++j) a[j] = o[j] + a[j];
+        }
+        stv<VEC>(out + i, a);
+    }
 }
 
 // max-pool forward: padded taps never win; the first maximum in row-major
 // window order is kept (strict '>' comparison).
 __global__ void maxpool_fwd_kernel(const float* __restrict__ x, float* __restrict__ y, int N, int H,
-                                   int W, int C, int R, int S, int st, int pad, int P, int Q) {
+                                   int W, int C, int R, int S, int st, int pad, int P, int Q,
+                                   uint16_t* __restrict__ y16) {
     const size_t total = (size_t)N * P * Q * C;
     for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
          i += (size_t)gridDim.x * blockDim.x) {
@@ -80,6 +152,7 @@ __global__ void maxpool_fwd_kernel(const float* __restrict__ x, float* __restric
             }
         }
         y[i] = m;
+        if (y16) y16[i] = (uint16_t)bf16_bits(m);
     }
 }
 
@@ -226,15 +299,6 @@ __global__ void gap_bwd_kernel(const float* __restrict__ dy, float* __restrict__
 enum { MODE_SUM = 0, MODE_MOMENTS = 1, MODE_BNBWD = 2 };
 constexpr int CS_THREADS = 256;
 
-template <int VEC>
-__device__ __forceinline__ void ldv(const float* p, float* o) {
-    if constexpr (VEC == 4) {
-        const float4 t = *reinterpret_cast<const float4*>(p);
-        o[0] = t.x; o[1] = t.y; o[2] = t.z; o[3] = t.w;
-    } else {
-        o[0] = *p;
-    }
-}
 
 // (n_a, mean_a, m2_a) <- merge with (n_b, mean_b, m2_b)
 __device__ __forceinline__ void chan_merge(float& na, float& mean_a, float& m2a, float nb,
@@ -418,46 +482,68 @@ colsum_final_kernel(const float* __restrict__ part0, const float* __restrict__ p
     }
 }
 
+template <int VEC>
 __global__ void bn_apply_kernel(const float* __restrict__ x, long M, int C,
                                 const float* __restrict__ gamma, const float* __restrict__ beta,
                                 const float* __restrict__ mean, const float* __restrict__ invstd,
-                                float* __restrict__ y, int relu) {
+                                float* __restrict__ y, int relu, uint16_t* __restrict__ y16) {
     const size_t total = (size_t)M * C;
-    for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
-         i += (size_t)gridDim.x * blockDim.x) {
-        int c = (int)(i % C);
-        float v = gamma[c] * ((x[i] - mean[c]) * invstd[c]) + beta[c];
-        y[i] = relu ? fmaxf(v, 0.f) : v;
+    for (size_t i = ((size_t)blockIdx.x * blockDim.x + threadIdx.x) * VEC; i < total;
+         i += (size_t)gridDim.x * blockDim.x * VEC) {
+        const int c = (int)(i % C);
+        float xv[VEC], ga[VEC], be[VEC], mu[VEC], is[VEC];
+        ldv<VEC>(x + i, xv);
+        ldv<VEC>(gamma + c, ga);
+        ldv<VEC>(beta + c, be);
+        ldv<VEC>(mean + c, mu);
+        ldv<VEC>(invstd + c, is);
+#pragma unroll
+        for (int j = 0; j < VEC; ++j) {
+            const float v = ga[j] * ((xv[j] - mu[j]) * is[j]) + be[j];
+            xv[j] = relu ? fmaxf(v, 0.f) : v;
+        }
+        stv<VEC>(y + i, xv);
+        if (y16) st16v<VEC>(y16 + i, xv);
     }
 }
 
 // dx = gamma*invstd*(dy' - sdy/M - xhat*sdyx/M)
+template <int VEC>
 __global__ void bn_bwd_apply_kernel(const float* __restrict__ x, const float* __restrict__ dy,
                                     const float* __restrict__ relu_y, long M, int C,
                                     const float* __restrict__ gamma,
                                     const float* __restrict__ mean,
                                     const float* __restrict__ invstd,
                                     const float* __restrict__ sdy, const float* __restrict__ sdyx,
-                                    float* __restrict__ dx, int acc) {
+                                    float* __restrict__ dx, int acc,
+                                    uint16_t* __restrict__ dx16) {
     const size_t total = (size_t)M * C;
     const float invM = 1.f / (float)M;
-    for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
-         i += (size_t)gridDim.x * blockDim.x) {
-        int c = (int)(i % C);
-        float g = dy[i];
-        if (relu_y && !(relu_y[i] > 0.f)) g = 0.f;
-        float is = invstd[c];
-        float xh = (x[i] - mean[c]) * is;
-        float v = gamma[c] * is * (g - sdy[c] * invM - xh * (sdyx[c] * invM));
-        dx[i] = acc ? dx[i] + v : v;
+    for (size_t i = ((size_t)blockIdx.x * blockDim.x + threadIdx.x) * VEC; i < total;
+         i += (size_t)gridDim.x * blockDim.x * VEC) {
+        const int c = (int)(i % C);
+        float g[VEC], xv[VEC], yv[VEC], d[VEC], ga[VEC], mu[VEC], is[VEC], s0[VEC], s1[VEC];
+        ldv<VEC>(dy + i, g);
+        ldv<VEC>(x + i, xv);
+        if (relu_y) ldv<VEC>(relu_y + i, yv);
+        if (acc) ldv<VEC>(dx + i, d);
+        ldv<VEC>(gamma + c, ga);
+        ldv<VEC>(mean + c, mu);
+        ldv<VEC>(invstd + c, is);
+        ldv<VEC>(sdy + c, s0);
+        ldv<VEC>(sdyx + c, s1);
+#pragma unroll
+        for (int j = 0; j < VEC; ++j) {
+            const float gj = (relu_y && !(yv[j] > 0.f)) ? 0.f : g[j];
+            const float xh = (xv[j] - mu[j]) * is[j];
+            const float v = ga[j] * is[j] * (gj - s0[j] * invM - xh * (s1[j] * invM));
+            d[j] = acc ? d[j] + v : v;
+        }
+        stv<VEC>(dx + i, d);
+        if (dx16) st16v<VEC>(dx16 + i, d);
     }
 }
 
-// bf16 copy, round to nearest even (the operand rounding of the bf16 contractions)
-__device__ __forceinline__ unsigned bf16_bits(float x) {
-    const unsigned u = __float_as_uint(x);
-    return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
-}
 
 __global__ void cast_bf16_kernel(const float* __restrict__ src, uint16_t* __restrict__ dst,
                                  size_t n, int vec) {
@@ -528,30 +614,42 @@ hipError_t launch_relu_fwd(const float* x, float* y, size_t n, hipStream_t s) {
 
 hipError_t launch_relu_bwd(const float* y, const float* dy, float* dx, size_t n, int accumulate,
                            hipStream_t s) {
-    hipLaunchKernelGGL(relu_bwd_kernel, dim3(ew_blocks(n)), dim3(EW_THREADS), 0, s, y, dy, dx, n,
-                       accumulate);
+    if (n % 4 == 0 && aligned16({y, dy, dx}))
+        hipLaunchKernelGGL(relu_bwd_kernel<4>, dim3(ew_blocks(n / 4)), dim3(EW_THREADS), 0, s, y, dy,
+                           dx, n, accumulate);
+    else
+        hipLaunchKernelGGL(relu_bwd_kernel<1>, dim3(ew_blocks(n)), dim3(EW_THREADS), 0, s, y, dy, dx,
+                           n, accumulate);
     return hipGetLastError();
 }
 
 hipError_t launch_add_fwd(const float* a, const float* b, float* y, size_t n, int relu,
-                          hipStream_t s) {
-    hipLaunchKernelGGL(add_fwd_kernel, dim3(ew_blocks(n)), dim3(EW_THREADS), 0, s, a, b, y, n,
-                       relu);
+                          hipStream_t s, uint16_t* y16) {
+    if (n % 4 == 0 && aligned16({a, b, y}) && ((uintptr_t)y16 & 7) == 0)
+        hipLaunchKernelGGL(add_fwd_kernel<4>, dim3(ew_blocks(n / 4)), dim3(EW_THREADS), 0, s, a, b, y,
+                           n, relu, y16);
+    else
+        hipLaunchKernelGGL(add_fwd_kernel<1>, dim3(ew_blocks(n)), dim3(EW_THREADS), 0, s, a, b, y, n,
+                           relu, y16);
     return hipGetLastError();
 }
 
 hipError_t launch_copy_or_acc(const float* v, float* out, size_t n, int accumulate,
                               hipStream_t s) {
-    hipLaunchKernelGGL(copy_or_acc_kernel, dim3(ew_blocks(n)), dim3(EW_THREADS), 0, s, v, out, n,
-                       accumulate);
+    if (n % 4 == 0 && aligned16({v, out}))
+        hipLaunchKernelGGL(copy_or_acc_kernel<4>, dim3(ew_blocks(n / 4)), dim3(EW_THREADS), 0, s, v,
+                           out, n, accumulate);
+    else
+        hipLaunchKernelGGL(copy_or_acc_kernel<1>, dim3(ew_blocks(n)), dim3(EW_THREADS), 0, s, v, out,
+                           n, accumulate);
     return hipGetLastError();
 }
 
 hipError_t launch_maxpool_fwd(const float* x, float* y, int N, int H, int W, int C, int R, int S,
-                              int st, int pad, int P, int Q, hipStream_t s) {
+                              int st, int pad, int P, int Q, hipStream_t s, uint16_t* y16) {
     size_t n = (size_t)N * P * Q * C;
     hipLaunchKernelGGL(maxpool_fwd_kernel, dim3(ew_blocks(n)), dim3(EW_THREADS), 0, s, x, y, N, H,
-                       W, C, R, S, st, pad, P, Q);
+                       W, C, R, S, st, pad, P, Q, y16);
     return hipGetLastError();
 }
 
@@ -664,21 +762,26 @@ size_t bn_ws_floats(long M, int C) { return 2 * (size_t)col_blocks_max(M, C) * C
 
 hipError_t launch_bn_fwd(const float* x, long M, int C, const float* gamma, const float* beta,
                          float eps, float* y, float* mean, float* invstd, int relu, float* ws,
-                         hipStream_t s) {
+                         hipStream_t s, uint16_t* y16) {
     const ColPlan p = col_plan(M, C, vec4_ok(C, {x}) ? 4 : 1);
     float* p0 = ws;
     float* p1 = ws + (size_t)p.nb * C;
     launch_partial<MODE_MOMENTS>(p, x, nullptr, nullptr, nullptr, nullptr, M, C, p0, p1, s);
     launch_final<FIN_STATS>(p, p0, p1, M, C, eps, mean, invstd, s);
     size_t n = (size_t)M * C;
-    hipLaunchKernelGGL(bn_apply_kernel, dim3(ew_blocks(n)), dim3(EW_THREADS), 0, s, x, M, C, gamma,
-                       beta, mean, invstd, y, relu);
+    if (vec4_ok(C, {x, y, gamma, beta, mean, invstd}) && ((uintptr_t)y16 & 7) == 0)
+        hipLaunchKernelGGL(bn_apply_kernel<4>, dim3(ew_blocks(n / 4)), dim3(EW_THREADS), 0, s, x, M,
+                           C, gamma, beta, mean, invstd, y, relu, y16);
+    else
+        hipLaunchKernelGGL(bn_apply_kernel<1>, dim3(ew_blocks(n)), dim3(EW_THREADS), 0, s, x, M, C,
+                           gamma, beta, mean, invstd, y, relu, y16);
     return hipGetLastError();
 }
 
 hipError_t launch_bn_bwd(const float* x, const float* dy, const float* relu_y, long M, int C,
                          const float* gamma, const float* mean, const float* invstd, float* dx,
-                         float* dgamma, float* dbeta, int accumulate, float* ws, hipStream_t s) {
+                         float* dgamma, float* dbeta, int accumulate, float* ws, hipStream_t s,
+                         uint16_t* dx16) {
     const ColPlan p = col_plan(M, C, vec4_ok(C, {x, dy, relu_y, mean, invstd}) ? 4 : 1);
     float* p0 = ws;
     float* p1 = ws + (size_t)p.nb * C;
@@ -686,8 +789,14 @@ hipError_t launch_bn_bwd(const float* x, const float* dy, const float* relu_y, l
     launch_final<FIN_SUM2>(p, p0, p1, M, C, 0.f, dbeta, dgamma, s);
     if (!dx) return hipGetLastError();      // parameter gradients only
     size_t n = (size_t)M * C;
-    hipLaunchKernelGGL(bn_bwd_apply_kernel, dim3(ew_blocks(n)), dim3(EW_THREADS), 0, s, x, dy,
-                       relu_y, M, C, gamma, mean, invstd, dbeta, dgamma, dx, accumulate);
+    if (vec4_ok(C, {x, dy, relu_y, dx, gamma, mean, invstd, dbeta, dgamma}) &&
+        ((uintptr_t)dx16 & 7) == 0)
+        hipLaunchKernelGGL(bn_bwd_apply_kernel<4>, dim3(ew_blocks(n / 4)), dim3(EW_THREADS), 0, s, x,
+                           dy, relu_y, M, C, gamma, mean, invstd, dbeta, dgamma, dx, accumulate,
+                           dx16);
+    else
+        hipLaunchKernelGGL(bn_bwd_apply_kernel<1>, dim3(ew_blocks(n)), dim3(EW_THREADS), 0, s, x, dy,
+                           relu_y, M, C, gamma, mean, invstd, dbeta, dgamma, dx, accumulate, dx16);
     return hipGetLastError();
 }
 

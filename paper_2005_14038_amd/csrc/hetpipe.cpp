@@ -55,6 +55,7 @@ struct Node {
     int consumers = 0;
     bool relu_fused = false;            // producer applies the ReLU (this node is a ReLU)
     bool fuses_relu = false;            // this node applies its consumer ReLU
+    int relu_node = -1;                 // ... which is this node
     float* y = nullptr;                 // forward output (a fused ReLU aliases its producer)
     float* g = nullptr;                 // gradient of the output
     bool g_written = false;
@@ -129,6 +130,7 @@ struct hp_stage {
     uint16_t* x16 = nullptr;
     uint16_t* g16 = nullptr;
     bool x16_ready = false;
+    int g16_node = -1;          // g16 already holds this conv's output gradient
     // forward bookkeeping for backward
     const float* fwd_w = nullptr;
     const float* fwd_x = nullptr;
@@ -318,6 +320,7 @@ int build_stage(hp_stage* st, const hp_layer* layers, int n_layers) {
         if ((k == HP_CONV || k == HP_FC || k == HP_BN || k == HP_ADD) && pr.consumers == 1 &&
             !pr.fuses_relu) {
             pr.fuses_relu = true;
+            pr.relu_node = i;
             nd.relu_fused = true;
         }
     }
@@ -517,6 +520,16 @@ extern "C" int hp_stage_forward(hp_stage* st, const float* w, const float* x, fl
                 ready = true;
             }
         }
+        // producers that can write the bf16 copy of the value they make (the
+        // ReLU node's value when they apply their consumer ReLU)
+        uint16_t* out16 = nullptr;
+        if (L.kind == HP_BN || L.kind == HP_ADD || L.kind == HP_MAXPOOL) {
+            Node& vis = nd.fuses_relu ? st->nodes[nd.relu_node] : nd;
+            if (vis.y16) {
+                out16 = vis.y16;
+                vis.y16_ready = true;
+            }
+        }
         tm.begin(L.kind == HP_CONV || L.kind == HP_FC ? 0 : 1, s);
         switch (L.kind) {
             case HP_CONV:
@@ -533,15 +546,16 @@ extern "C" int hp_stage_forward(hp_stage* st, const float* w, const float* x, fl
                 break;
             case HP_MAXPOOL:
                 e = launch_maxpool_fwd(in, nd.y, B, nd.inH, nd.inW, nd.inC, L.R, L.S, L.stride,
-                                       L.pad, nd.H, nd.W, s);
+                                       L.pad, nd.H, nd.W, s, out16);
                 break;
             case HP_BN:
                 e = launch_bn_fwd(in, (long)B * nd.H * nd.W, nd.C, w + nd.w_off, w + nd.b_off,
-                                  L.eps, nd.y, nd.mean, nd.invstd, nd.fuses_relu ? 1 : 0, st->ws, s);
+                                  L.eps, nd.y, nd.mean, nd.invstd, nd.fuses_relu ? 1 : 0, st->ws, s,
+                                  out16);
                 break;
             case HP_ADD: {
                 const float* in1 = L.in1 < 0 ? x : st->nodes[L.in1].y;
-                e = launch_add_fwd(in, in1, nd.y, nd.out_elems, nd.fuses_relu ? 1 : 0, s);
+                e = launch_add_fwd(in, in1, nd.y, nd.out_elems, nd.fuses_relu ? 1 : 0, s, out16);
                 break;
             }
             case HP_GAP:
@@ -588,6 +602,7 @@ extern "C" int hp_stage_backward(hp_stage* st, const float* w, const float* dy, 
         nd.g_alias = nullptr;
     }
     bool dx_written = false;
+    st->g16_node = -1;
     if (st->has_loss) st->nodes[st->nodes.back().L.in0].g_written = true;  // dz from forward
 
     // destination of a gradient sent to value j: (pointer, accumulate?)
@@ -628,9 +643,12 @@ extern "C" int hp_stage_backward(hp_stage* st, const float* w, const float* dy, 
                 const uint16_t* g16 = nullptr;
                 if (nd.fwd.h16 && st->w16) {
                     in16 = L.in0 < 0 ? st->x16 : st->nodes[L.in0].y16;
-                    tm.begin(1, s);
-                    e = launch_cast_bf16(gin, st->g16, nd.out_elems, s);
-                    tm.end(s);
+                    if (st->g16_node != i) {
+                        tm.begin(1, s);
+                        e = launch_cast_bf16(gin, st->g16, nd.out_elems, s);
+                        tm.end(s);
+                    }
+                    st->g16_node = -1;
                     g16 = st->g16;
                 }
                 tm.begin(0, s);
@@ -685,9 +703,20 @@ extern "C" int hp_stage_backward(hp_stage* st, const float* w, const float* dy, 
             case HP_BN: {
                 // with a fused ReLU, nd.y holds the ReLU output and serves as the mask
                 bool want = dest(L.in0, &d, &acc);
+                // the producing conv reads this gradient as a bf16 operand: write
+                // that copy too when this BN is the conv's only consumer
+                uint16_t* d16 = nullptr;
+                if (want && L.in0 >= 0 && st->w16) {
+                    const Node& pc = st->nodes[L.in0];
+                    if ((pc.L.kind == HP_CONV || pc.L.kind == HP_FC) && pc.fwd.h16 &&
+                        pc.consumers == 1) {
+                        d16 = st->g16;
+                        st->g16_node = L.in0;
+                    }
+                }
                 e = launch_bn_bwd(in, gin, nd.fuses_relu ? nd.y : nullptr, (long)B * nd.H * nd.W,
                                   nd.C, w + nd.w_off, nd.mean, nd.invstd, want ? d : nullptr,
-                                  grad + nd.w_off, grad + nd.b_off, want ? acc : 0, st->ws, s);
+                                  grad + nd.w_off, grad + nd.b_off, want ? acc : 0, st->ws, s, d16);
                 break;
             }
             case HP_ADD: {

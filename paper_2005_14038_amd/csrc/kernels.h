@@ -73,13 +73,15 @@ hipError_t launch_relu_fwd(const float* x, float* y, size_t n, hipStream_t s);
 hipError_t launch_relu_bwd(const float* y, const float* dy, float* dx, size_t n,
                            int accumulate, hipStream_t s);
 // out = a + b (relu optional)
+// y16 (optional): also write y rounded to bf16
 hipError_t launch_add_fwd(const float* a, const float* b, float* y, size_t n, int relu,
-                          hipStream_t s);
+                          hipStream_t s, uint16_t* y16 = nullptr);
 // out = v (accumulate = 0) or out += v
 hipError_t launch_copy_or_acc(const float* v, float* out, size_t n, int accumulate,
                               hipStream_t s);
 hipError_t launch_maxpool_fwd(const float* x, float* y, int N, int H, int W, int C, int R,
-                              int S, int st, int pad, int P, int Q, hipStream_t s);
+                              int S, int st, int pad, int P, int Q, hipStream_t s,
+                              uint16_t* y16 = nullptr);
 // mask (optional, layout of dx): the pooled input is a ReLU output; dx is
 // zeroed where mask <= 0 (ReLU backward fused)
 hipError_t launch_maxpool_bwd(const float* x, const float* dy, float* dx, int N, int H, int W,
@@ -100,13 +102,14 @@ hipError_t launch_colsum(const float* v, long M, int C, float* out, float* ws, h
 size_t bn_ws_floats(long M, int C);
 hipError_t launch_bn_fwd(const float* x, long M, int C, const float* gamma, const float* beta,
                          float eps, float* y, float* mean, float* invstd, int relu, float* ws,
-                         hipStream_t s);
+                         hipStream_t s, uint16_t* y16 = nullptr);
 // Backward.  If relu_y != NULL the incoming gradient is first masked by
 // relu_y > 0 (BN followed by ReLU).  Writes dgamma, dbeta and, unless dx is NULL,
 // dx (accumulate optional).
 hipError_t launch_bn_bwd(const float* x, const float* dy, const float* relu_y, long M, int C,
                          const float* gamma, const float* mean, const float* invstd, float* dx,
-                         float* dgamma, float* dbeta, int accumulate, float* ws, hipStream_t s);
+                         float* dgamma, float* dbeta, int accumulate, float* ws, hipStream_t s,
+                         uint16_t* dx16 = nullptr);
 
 // Softmax cross-entropy: loss (one float) = mean_n (lse(z_n) - z_n[label]);
 // dz = (softmax(z) - onehot) / B.
