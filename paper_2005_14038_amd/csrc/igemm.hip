@@ -170,35 +170,47 @@ __device__ __forceinline__ void store_tile(const KArgs& args, const Work& w,
     for (int j = 0; j < TN; ++j) {
         const long col = w.n0 + wn + 32 * j + lr;
         if (col >= args.Ncols) continue;
+        // output row stride and the address of (row0, col); the bias-gradient
+        // column goes to bias_out[row]
+        long ld = args.Ncols;
+        float* cbase = args.out + col;
+        if (epi & EPI_BIASCOL) {
+            ld = args.Ncols - 1;
+            cbase = args.out + col;
+            if (col == args.Ncols - 1) { ld = 1; cbase = args.bias_out; }
+        }
+        const float bias = (epi & EPI_BIAS) ? args.bias[col] : 0.f;
 #pragma unroll
         for (int i = 0; i < TM; ++i) {
             const long row0 = w.m0 + wm + 32 * i + 4 * lk;
+            // rows row0 + 8(v/4) + v%4 of this lane; those >= M are outside
+            const int left = (int)min(args.M - row0, 32L);
+            float* obase = cbase + row0 * ld;
+            const float* mbase = (epi & EPI_MASK) ? args.mask + row0 * args.Ncols + col : nullptr;
+            const int ldi = (int)ld, ldm = (int)args.Ncols;
 #pragma unroll
             for (int v0 = 0; v0 < 16; v0 += EPI_CHUNK) {
                 float prev[EPI_CHUNK], msk[EPI_CHUNK];
 #pragma unroll
                 for (int u = 0; u < EPI_CHUNK; ++u) {
-                    const int v = v0 + u;
-                    const long row = row0 + 8 * (v >> 2) + (v & 3);
+                    const int r = 8 * ((v0 + u) >> 2) + ((v0 + u) & 3);
                     prev[u] = 0.f;
                     msk[u] = 1.f;
-                    if (row < args.M) {
-                        if (epi & EPI_ACCUM)
-                            prev[u] = *out_ptr(args.out, args.bias_out, row, col, args.Ncols, epi);
-                        if (epi & EPI_MASK) msk[u] = args.mask[row * args.Ncols + col];
+                    if (r < left) {
+                        if (epi & EPI_ACCUM) prev[u] = obase[r * ldi];
+                        if (epi & EPI_MASK) msk[u] = mbase[r * ldm];
                     }
                 }
 #pragma unroll
                 for (int u = 0; u < EPI_CHUNK; ++u) {
-                    const int v = v0 + u;
-                    const long row = row0 + 8 * (v >> 2) + (v & 3);
-                    if (row >= args.M) continue;
-                    float val = acc[i][j][v];
-                    if (epi & EPI_BIAS) val += args.bias[col];
+                    const int r = 8 * ((v0 + u) >> 2) + ((v0 + u) & 3);
+                    if (r >= left) continue;
+                    float val = acc[i][j][v0 + u];
+                    if (epi & EPI_BIAS) val += bias;
                     if (epi & EPI_RELU) val = fmaxf(val, 0.f);
                     if ((epi & EPI_MASK) && !(msk[u] > 0.f)) val = 0.f;
                     if (epi & EPI_ACCUM) val += prev[u];
-                    *out_ptr(args.out, args.bias_out, row, col, args.Ncols, epi) = val;
+                    obase[r * ldi] = val;
                 }
             }
         }
@@ -1262,11 +1274,15 @@ KernelRef kernel_for(int op, int cfg, int vw, bool bf) {
 }
 
 // Tile configuration for a contraction of M x N (x Kred): the 128x128 tile
-// unless one side is at most 64, where a tile of that width wastes less.
-int choose_cfg(long M, long N) {
+// unless one side is at most 64, where a tile of that width wastes less.  A
+// forward or data-gradient contraction with a short reduction (a 1x1
+// convolution over at most 512 channels) writes much more than it computes;
+// 64x64 tiles give it four times as many workgroups to overlap those writes.
+int choose_cfg(int op, long M, long N, long Kred) {
     if (M <= 64 && N <= 64) return 4;
     if (N <= 64) return 1;
     if (M <= 64) return (N % 256 == 0 || N >= 1024) ? 2 : 3;
+    if (op != OP_WGRAD && Kred <= 512) return 4;
     return 0;
 }
 
@@ -1288,12 +1304,12 @@ GemmPlan plan_gemm(int op, const ConvGeo& g, int bf16, int num_cus, int bias_col
     const bool v4 = (op == OP_FWD) ? (g.C % 4 == 0) : (g.C % 4 == 0 && g.K % 4 == 0);
     // bf16 operands in memory: every contiguous axis a multiple of 8 (16 bytes)
     p.h16 = (bf16 && g.C % 8 == 0 && g.K % 8 == 0) ? 1 : 0;
-    p.cfg = choose_cfg(p.M, p.Ncols);
+    p.cfg = choose_cfg(op, p.M, p.Ncols, p.Kred);
     if (p.bias_col) {
         // the bias-gradient column rides along unless it adds more than 10% of
         // tiles (then a separate column sum of dy is cheaper)
         const long wn = p.Ncols - 1;
-        const int c0 = choose_cfg(p.M, wn);
+        const int c0 = choose_cfg(op, p.M, wn, p.Kred);
         const long bn = kCfgs[c0].bn;
         if (c0 != p.cfg || 10 * ((p.Ncols + bn - 1) / bn) > 11 * ((wn + bn - 1) / bn)) {
             p.bias_col = 0;
