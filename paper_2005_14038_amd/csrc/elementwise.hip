@@ -427,15 +427,16 @@ colsum_partial_kernel(const float* __restrict__ v, const float* __restrict__ x,
     }
 }
 
-// Combination of the nb row-block partials of each channel: workgroup = 64
-// channels x 16 lanes; lane l takes blocks l, l+16, ... in order, then the 16
-// lane results are combined in order.
+// Combination of the nb row-block partials of each channel: workgroup = 16
+// channels x 64 lanes; lane l takes blocks l, l+64, ... in order, then the
+// lane results are combined by a fixed binary tree (lane l with l + 32, then
+// l + 16, ...), so the order of every addition is fixed.
 //   FIN_SUM:   out0 = sum part0
 //   FIN_SUM2:  out0 = sum part0, out1 = sum part1
 //   FIN_STATS: merge (block mean, block squared deviations); out0 = mean,
 //              out1 = 1 / sqrt(biased variance + eps)
 enum { FIN_SUM = 0, FIN_SUM2 = 1, FIN_STATS = 2 };
-constexpr int CF_CH = 64, CF_LANES = 16;
+constexpr int CF_CH = 16, CF_LANES = 64;
 
 template <int FIN>
 __global__ void __launch_bounds__(CF_CH * CF_LANES)
@@ -463,21 +464,28 @@ colsum_final_kernel(const float* __restrict__ part0, const float* __restrict__ p
     r1[ln][cl] = s1;
     rn[ln][cl] = na;
     __syncthreads();
-    if (ln == 0 && c < C) {
-        for (int l = 1; l < CF_LANES; ++l) {
+    for (int off = CF_LANES / 2; off > 0; off >>= 1) {
+        if (ln < off) {
             if constexpr (FIN == FIN_STATS) {
-                chan_merge(na, s0, s1, rn[l][cl], r0[l][cl], r1[l][cl]);
+                float n = rn[ln][cl], m = r0[ln][cl], q = r1[ln][cl];
+                chan_merge(n, m, q, rn[ln + off][cl], r0[ln + off][cl], r1[ln + off][cl]);
+                rn[ln][cl] = n;
+                r0[ln][cl] = m;
+                r1[ln][cl] = q;
             } else {
-                s0 += r0[l][cl];
-                s1 += r1[l][cl];
+                r0[ln][cl] += r0[ln + off][cl];
+                if (FIN == FIN_SUM2) r1[ln][cl] += r1[ln + off][cl];
             }
         }
+        __syncthreads();
+    }
+    if (ln == 0 && c < C) {
         if constexpr (FIN == FIN_STATS) {
-            out0[c] = s0;
-            out1[c] = 1.f / sqrtf(s1 / (float)M + eps);
+            out0[c] = r0[0][cl];
+            out1[c] = 1.f / sqrtf(r1[0][cl] / (float)M + eps);
         } else {
-            out0[c] = s0;
-            if (FIN == FIN_SUM2) out1[c] = s1;
+            out0[c] = r0[0][cl];
+            if (FIN == FIN_SUM2) out1[c] = r1[0][cl];
         }
     }
 }
