@@ -42,11 +42,14 @@ constexpr int PAD_V = 4;
 // WM x WN (a grid of (WM/32) x (WN/32) MFMA 32x32 tiles per wave); the
 // workgroup has (BM/WM) * (BN/WN) waves.
 struct TileCfg { int bm, bn, bk, wm, wn; };
+// Eight waves of 32x64 in the general tile and four in the 64x128 one hide
+// the staging latency better than four (two) waves of 64x64, at the cost of
+// more LDS reads per MFMA.
 constexpr TileCfg kCfgs[] = {
-    {128, 128, 16, 64, 64},    // 0: general
+    {128, 128, 16, 32, 64},    // 0: general (8 waves)
     {256, 64, 16, 64, 64},     // 1: narrow N (at most 64 output columns)
     {64, 256, 16, 64, 64},     // 2: narrow M, N a multiple of 256 or large
-    {64, 128, 16, 64, 64},     // 3: narrow M otherwise (2 waves)
+    {64, 128, 16, 32, 64},     // 3: narrow M otherwise (4 waves)
     {64, 64, 16, 32, 32},      // 4: small M and N (4 waves of 32x32)
 };
 
@@ -1158,9 +1161,10 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_h16_kerne
 
 
 // Reduction of the cut tiles: workgroup = 64 elements of one tile x 16 split
-// lanes; lane l adds splits l, l+16, ...; the lane sums are combined in a
-// fixed order (deterministic), then the epilogue runs.
-constexpr int SK_EL = 64, SK_LANES = 16;
+// lanes; lane l adds splits l, l+16, ... (eight loads in flight at a time,
+// added in split order), the lane sums are combined in a fixed order
+// (deterministic), then the epilogue runs.
+constexpr int SK_EL = 64, SK_LANES = 16, SK_BATCH = 8;
 
 __global__ void __launch_bounds__(SK_EL * SK_LANES)
 igemm_splitk_reduce_kernel(KArgs args, int BM, int BN) {
@@ -1175,7 +1179,16 @@ igemm_splitk_reduce_kernel(KArgs args, int BM, int BN) {
     const long col = (long)(tile % args.tiles_n) * BN + e % BN;
     float s = 0.f;
     const float* src = args.ws + (long)rt * args.splits * (BM * BN) + e;
-    for (int z = ln; z < args.splits; z += SK_LANES) s += src[(long)z * (BM * BN)];
+    for (int z0 = ln; z0 < args.splits; z0 += SK_LANES * SK_BATCH) {
+        float v[SK_BATCH];
+#pragma unroll
+        for (int b = 0; b < SK_BATCH; ++b) {
+            const int z = z0 + b * SK_LANES;
+            v[b] = z < args.splits ? src[(long)z * (BM * BN)] : 0.f;
+        }
+#pragma unroll
+        for (int b = 0; b < SK_BATCH; ++b) s += v[b];
+    }
     red[ln][el] = s;
     __syncthreads();
     if (ln == 0 && row < args.M && col < args.Ncols) {
@@ -1186,8 +1199,9 @@ igemm_splitk_reduce_kernel(KArgs args, int BM, int BN) {
     }
 }
 
-// The same reduction for few splits: one thread per 4 consecutive elements
-// of the cut tiles (one float4 per split), adding the splits in order.
+// The same reduction for at most 16 splits: one thread per 4 consecutive
+// elements of the cut tiles; all of its split partials (one float4 each) are
+// loaded before they are added, in split order.
 __global__ void __launch_bounds__(256) igemm_cut_reduce_kernel(KArgs args, int BM, int BN) {
     const int tile_elems = BM * BN;
     const int per_tile = tile_elems / 4;
@@ -1202,10 +1216,16 @@ __global__ void __launch_bounds__(256) igemm_cut_reduce_kernel(KArgs args, int B
         if (row >= args.M || col0 >= args.Ncols) continue;
         const float4* src =
             reinterpret_cast<const float4*>(args.ws + (long)rt * args.splits * tile_elems + e);
-        float4 acc = src[0];
-        for (int z = 1; z < args.splits; ++z) {
-            const float4 v = src[(long)z * per_tile];
-            acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
+        float4 part[SK_LANES];
+#pragma unroll
+        for (int z = 0; z < SK_LANES; ++z)
+            part[z] = z < args.splits ? src[(long)z * per_tile] : make_float4(0.f, 0.f, 0.f, 0.f);
+        float4 acc = part[0];
+#pragma unroll
+        for (int z = 1; z < SK_LANES; ++z) {
+            if (z < args.splits) {
+                acc.x += part[z].x; acc.y += part[z].y; acc.z += part[z].z; acc.w += part[z].w;
+            }
         }
         const float a4[4] = {acc.x, acc.y, acc.z, acc.w};
         float prev[4] = {0.f, 0.f, 0.f, 0.f};
@@ -1216,12 +1236,17 @@ __global__ void __launch_bounds__(256) igemm_cut_reduce_kernel(KArgs args, int B
                 if (col0 + j < args.Ncols)
                     prev[j] = *out_ptr(args.out, args.bias_out, row, col0 + j, args.Ncols, args.epi);
         }
+        const int epi = args.epi;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             const long col = col0 + j;
             if (col >= args.Ncols) break;
-            float* dst = out_ptr(args.out, args.bias_out, row, col, args.Ncols, args.epi);
-            *dst = epilogue(a4[j], row, col, args.Ncols, args.epi, args.bias, args.mask, prev + j);
+            float v = a4[j];
+            if (epi & EPI_BIAS) v += args.bias[col];
+            if (epi & EPI_RELU) v = fmaxf(v, 0.f);
+            if ((epi & EPI_MASK) && !(args.mask[row * args.Ncols + col] > 0.f)) v = 0.f;
+            if (epi & EPI_ACCUM) v += prev[j];
+            *out_ptr(args.out, args.bias_out, row, col, args.Ncols, epi) = v;
         }
     }
 }
