@@ -42,12 +42,12 @@ constexpr int PAD_V = 4;
 // WM x WN (a grid of (WM/32) x (WN/32) MFMA 32x32 tiles per wave); the
 // workgroup has (BM/WM) * (BN/WN) waves.
 struct TileCfg { int bm, bn, bk, wm, wn; };
-// Eight waves of 32x64 in the general tile and four in the 64x128 one hide
-// the staging latency better than four (two) waves of 64x64, at the cost of
-// more LDS reads per MFMA.
+// Waves of 32x64 (eight in the general tile, four in the 128x64 and 64x128
+// ones) hide the staging latency better than fewer waves of 64x64, at the
+// cost of more LDS reads per MFMA.
 constexpr TileCfg kCfgs[] = {
     {128, 128, 16, 32, 64},    // 0: general (8 waves)
-    {256, 64, 16, 64, 64},     // 1: narrow N (at most 64 output columns)
+    {128, 64, 16, 32, 64},     // 1: narrow N (at most 64 output columns, 4 waves)
     {64, 256, 16, 64, 64},     // 2: narrow M, N a multiple of 256 or large
     {64, 128, 16, 32, 64},     // 3: narrow M otherwise (4 waves)
     {64, 64, 16, 32, 32},      // 4: small M and N (4 waves of 32x32)
@@ -1364,8 +1364,12 @@ GemmPlan plan_gemm(int op, const ConvGeo& g, int bf16, int num_cus, int bias_col
         }
         if (splits > 1) tfull = rounds * slots;
     } else {
-        // too few tiles: cut every tile so that one round is filled
+        // too few tiles: cut every tile so that one round is filled.  Long
+        // fp32 reductions (weight gradients over N*P*Q) are cut for two
+        // workgroups per slot as long as a chunk keeps 64 K tiles: a chunk
+        // that long outweighs writing and re-reading its partial tile.
         splits = std::min<long>(slots / tiles, ktiles / 8);
+        if (!bf16) splits = std::max(splits, std::min<long>(2 * slots / tiles, ktiles / 64));
         if (splits >= 2) tfull = 0;
         else splits = 1;
     }
