@@ -3,9 +3,9 @@
 // All three stream flat fp32 parameter vectors once, so they are HBM-bound:
 // float4 accesses (four per thread per iteration on long vectors, all loads
 // issued before the first use), a grid of up to 16 workgroups per CU striding
-// over the vector, and a scalar tail for lengths that are not multiples of 4.  Operands
-// read once and not needed again soon (the gradient, u~ in the push) are
-// loaded non-temporally.  The arithmetic
+// over the vector, and a scalar tail for lengths that are not multiples of 4.
+// Every vector is streamed once per kernel and not read again before other
+// kernels have passed through the caches, so the loads are non-temporal.  The arithmetic
 // is fixed to one IEEE fp32 operation at a time (contraction into fused
 // multiply-add is switched off for this file), so the result is bit-identical to any
 // other implementation that performs the same operations in the same order:
@@ -67,8 +67,8 @@ local_update_kernel(const float* __restrict__ g, const float* newest, float* dst
             const size_t i = base + (size_t)k * blockDim.x;
             if (i < n4) {
                 gv[k] = ld4(g4 + i);
-                wv[k] = w4[i];
-                if (!FIRST) av[k] = u4[i];
+                wv[k] = ld4(w4 + i);
+                if (!FIRST) av[k] = ld4(u4 + i);
             }
         }
 #pragma unroll
@@ -110,7 +110,7 @@ push_kernel(float* __restrict__ wg, const float* __restrict__ ut, size_t n, int 
 #pragma unroll
         for (int k = 0; k < U; ++k) {
             const size_t i = base + (size_t)k * blockDim.x;
-            if (i < n4) { a[k] = w4[i]; b[k] = ld4(u4 + i); }
+            if (i < n4) { a[k] = ld4(w4 + i); b[k] = ld4(u4 + i); }
         }
 #pragma unroll
         for (int k = 0; k < U; ++k) {
@@ -137,7 +137,7 @@ copy_kernel(const float* __restrict__ src, float* __restrict__ dst, size_t n, in
 #pragma unroll
         for (int k = 0; k < U; ++k) {
             const size_t i = base + (size_t)k * blockDim.x;
-            if (i < n4) a[k] = s4[i];
+            if (i < n4) a[k] = ld4(s4 + i);
         }
 #pragma unroll
         for (int k = 0; k < U; ++k) {
