@@ -133,6 +133,64 @@ def cpu_baseline(wl, layers, out_shape, images):
                       f"backward + local update, {dt:.1f} s"}
 
 
+def run_pipeline(args, wl, dev):
+    """Throughput of one virtual worker run as a K-partition pipeline (K HIP
+    streams, up to W = s_local + 1 minibatches in flight, partitions balanced
+    by nominal work at block boundaries), against K = 1 in the same process.
+    A step is one minibatch; the timed region covers whole waves after one
+    warm-up wave, so pipeline fill and drain are included once."""
+    import torch
+    from paper_2005_14038_amd import workloads
+    from paper_2005_14038_amd.pipeline import PipelinedVW, balanced_cuts, layer_costs
+    b = wl.builder()
+    layers = b.layers
+    if not wl.has_loss:
+        sys.exit("--pipeline needs a workload with a loss head (tiny, vgg19, resnet152)")
+    w0 = torch.from_numpy(workloads.initial_weights(wl, layers)).to(dev)
+    pool = {}
+
+    def data(n, q):
+        j = (q - 1) % args.pool
+        if j not in pool:
+            x, lab, _ = workloads.inputs(wl, None, 0, j + 1)
+            pool[j] = (torch.from_numpy(x).to(dev), torch.from_numpy(lab).to(dev), None)
+        return pool[j]
+
+    W = wl.s_local + 1
+    waves = max(1, -(-args.steps // W))
+    result = {}
+    for k in (1, args.pipeline):
+        cuts = balanced_cuts(layers, k, layer_costs(layers, wl.H, wl.W, wl.C, wl.batch)) \
+            if k > 1 else []
+        pv = PipelinedVW(layers, wl.batch, wl.H, wl.W, wl.C, w0, wl.s_local, wl.lr, data, cuts,
+                         dtype=wl.dtype)
+        pv.run(1)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        pv.run(1 + waves)
+        torch.cuda.synchronize()
+        dt = time.perf_counter() - t0
+        result[k] = (waves * W * wl.batch / dt, dt * 1e3 / (waves * W), cuts)
+        pv.close()
+        del pv
+        torch.cuda.empty_cache()
+    K = args.pipeline
+    value, ms, cuts = result[K]
+    out = {
+        "metric": "pipelined virtual worker images/sec (fwd+bwd+WSP update, K partitions on "
+                  "K streams of one GPU)",
+        "value": round(value, 3), "unit": "images/s", "n_gpus": 1, "steps": waves * W,
+        "warmup": W, "ms_per_step": round(ms, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32" if wl.dtype == "fp32" else "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"{wl.name}: batch {wl.batch} x {wl.H}x{wl.W}x{wl.C}, one virtual "
+                               f"worker, N_m = {W}, {K} partitions cut after layers {cuts}",
+                   "global_batch": wl.batch, "parallelism": f"pipeline {K} streams, one GPU"},
+        "one_partition": {"value": round(result[1][0], 3), "ms_per_step": round(result[1][1], 4)},
+    }
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -143,6 +201,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-images", type=int, default=4,
                     help="images of the oracle's bounded CPU sample")
+    ap.add_argument("--pipeline", type=int, default=0, metavar="K",
+                    help="run one virtual worker as a K-partition pipeline on K streams "
+                         "(workloads with a loss head) instead of the stage step")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -159,6 +220,8 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda:0")
     wl = workloads.WORKLOADS[args.workload]
+    if args.pipeline:
+        return run_pipeline(args, wl, dev)
     b = wl.builder()
     layers = b.layers
     st = Stage(layers, wl.batch, wl.H, wl.W, wl.C, dtype=wl.dtype)

@@ -158,19 +158,24 @@ int hp_ps_read_timing(hp_ps *ps, double ms[4], int64_t launches[4]);
 int hp_vw_create(hp_ps *ps, int id, int s_local, hp_vw **out);
 int hp_vw_destroy(hp_vw *vw);
 
-/* Weights for the VW's next minibatch q = p+1: the ring version holding the
- * local updates 1 .. q-W (Sec. 4) -- a device pointer into the ring, valid
- * until this VW's next hp_wsp_local_update.  Errors: HP_ERR_STATE if a
- * completed wave has not been pushed yet, or its pull has not succeeded. */
+/* Starts the VW's next minibatch q = p + i + 1, where p minibatches have
+ * completed and i (0 <= i < W) are in flight -- a VW runs up to N_m = W
+ * minibatches concurrently in its pipeline (Sec. 4).  Returns the ring version
+ * holding the local updates 1 .. q-W, a device pointer into the ring that
+ * stays valid until minibatch q's own hp_wsp_local_update.  Minibatches
+ * complete in the order they start.  Errors: HP_ERR_STATE if W minibatches are
+ * already in flight, a completed wave has not been pushed yet, or its pull has
+ * not succeeded. */
 int hp_wsp_weights(hp_vw *vw, const float **w);
 
-/* Local update after minibatch q completes (Sec. 4: w_local = w_local + u_q,
- * u_q = -lr * grad) and wave accumulation (Sec. 5: u~ sums the wave's u_q).
+/* Local update after the oldest in-flight minibatch q = p+1 completes (Sec. 4:
+ * w_local = w_local + u_q, u_q = -lr * grad) and wave accumulation (Sec. 5:
+ * u~ sums the wave's u_q).
  * Computes, element by element in fp32 without fused multiply-add,
  *   u = (-lr) * grad;  ring[(q-1) mod W] = ring[(q-2) mod W] + u;
  *   u~ = u (first minibatch of a wave) or u~ + u,
  * and advances p.  `grad` is caller-owned (P floats).
- * Errors: HP_ERR_STATE if hp_wsp_weights was not called for this minibatch. */
+ * Errors: HP_ERR_STATE if no minibatch is in flight. */
 int hp_wsp_local_update(hp_vw *vw, const float *grad, float lr);
 
 /* Push at the end of wave c (Sec. 5): w_g = w_g + u~, the VW's local clock
@@ -196,12 +201,13 @@ typedef struct hp_wsp_state {
     int32_t g;          /* global clock reflected by the last pull */
     int32_t push_due;   /* a completed wave awaits hp_wsp_push_wave */
     int32_t gated;      /* a push happened and its pull has not succeeded */
-    int32_t next_slot;  /* ring slot the next minibatch reads */
+    int32_t next_slot;  /* ring slot the next minibatch to start reads */
     int32_t n_vw;       /* N */
+    int32_t in_flight;  /* minibatches started and not completed (0 .. W) */
 } hp_wsp_state_t;
 int hp_wsp_state(const hp_vw *vw, hp_wsp_state_t *out);
 
-/* Version vector of the weights the next minibatch will read: V[n] = number
+/* Version vector of the weights the next minibatch to start will read: V[n] = number
  * of minibatch updates of VW n contained in them (n < N).  `V` is host memory
  * of N int64 entries. */
 int hp_wsp_version(const hp_vw *vw, int64_t *V);

@@ -160,7 +160,8 @@ struct hp_vw {
     float* ut = nullptr;
     int64_t p = 0;
     int c = 0, g = 0;
-    bool in_flight = false, push_due = false, need_pull = false;
+    int inflight = 0;                      // started, not yet completed (at most W)
+    bool push_due = false, need_pull = false;
     std::vector<std::vector<int64_t>> V;   // [W][N] version vectors of the ring slots
 };
 
@@ -860,16 +861,19 @@ extern "C" int hp_wsp_weights(hp_vw* v, const float** w) {
     if (v->push_due) return fail(HP_ERR_STATE, "hp_wsp_weights: wave %d not pushed yet", v->c);
     if (v->need_pull)
         return fail(HP_ERR_STATE, "hp_wsp_weights: VW %d is gated by the clock bound", v->id);
-    int slot = (int)(v->p % v->W);
+    if (v->inflight >= v->W)
+        return fail(HP_ERR_STATE, "hp_wsp_weights: VW %d already has %d minibatches in flight",
+                    v->id, v->inflight);
+    int slot = (int)((v->p + v->inflight) % v->W);
     *w = v->ring + (size_t)slot * v->stride;
-    v->in_flight = true;
+    v->inflight += 1;
     return HP_OK;
 }
 
 extern "C" int hp_wsp_local_update(hp_vw* v, const float* grad, float lr) {
     if (!v || !grad) return fail(HP_ERR_ARG, "hp_wsp_local_update: NULL argument");
     if (!v->ps) return fail(HP_ERR_STATE, "hp_wsp_local_update: parameter server destroyed");
-    if (!v->in_flight)
+    if (v->inflight == 0)
         return fail(HP_ERR_STATE, "hp_wsp_local_update: no minibatch was started (hp_wsp_weights)");
     const int64_t q = v->p + 1;
     const int W = v->W;
@@ -887,7 +891,7 @@ extern "C" int hp_wsp_local_update(hp_vw* v, const float* grad, float lr) {
     nv[v->id] += 1;
     v->V[slot] = nv;
     v->p = q;
-    v->in_flight = false;
+    v->inflight -= 1;
     if (q % W == 0) v->push_due = true;
     return HP_OK;
 }
@@ -939,14 +943,15 @@ extern "C" int hp_wsp_state(const hp_vw* v, hp_wsp_state_t* out) {
     out->g = v->g;
     out->push_due = v->push_due ? 1 : 0;
     out->gated = v->need_pull ? 1 : 0;
-    out->next_slot = (int)(v->p % v->W);
+    out->next_slot = (int)((v->p + v->inflight) % v->W);
+    out->in_flight = v->inflight;
     out->n_vw = v->ps ? v->ps->N : (int)v->V[0].size();
     return HP_OK;
 }
 
 extern "C" int hp_wsp_version(const hp_vw* v, int64_t* V) {
     if (!v || !V) return fail(HP_ERR_ARG, "hp_wsp_version: NULL argument");
-    const std::vector<int64_t>& vv = v->V[(size_t)(v->p % v->W)];
+    const std::vector<int64_t>& vv = v->V[(size_t)((v->p + v->inflight) % v->W)];
     for (size_t n = 0; n < vv.size(); ++n) V[n] = vv[n];
     return HP_OK;
 }

@@ -49,7 +49,8 @@ class hp_layer(ctypes.Structure):
 class hp_wsp_state_t(ctypes.Structure):
     _fields_ = [("p", ctypes.c_int64), ("W", ctypes.c_int32), ("c", ctypes.c_int32),
                 ("g", ctypes.c_int32), ("push_due", ctypes.c_int32), ("gated", ctypes.c_int32),
-                ("next_slot", ctypes.c_int32), ("n_vw", ctypes.c_int32)]
+                ("next_slot", ctypes.c_int32), ("n_vw", ctypes.c_int32),
+                ("in_flight", ctypes.c_int32)]
 
 
 _lib = None

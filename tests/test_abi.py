@@ -32,7 +32,8 @@ def test_library_exports_every_declared_symbol():
 def test_layer_struct_matches_header():
     # 10 int32 fields and one float: 44 bytes, no padding
     assert ctypes.sizeof(hetpipe.hp_layer) == 44
-    assert ctypes.sizeof(hetpipe.hp_wsp_state_t) == 8 + 7 * 4 + 4
+    # one int64 and eight int32: 40 bytes, no padding
+    assert ctypes.sizeof(hetpipe.hp_wsp_state_t) == 8 + 8 * 4
 
 
 def test_error_text_without_device_work():
