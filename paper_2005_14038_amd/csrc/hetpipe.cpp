@@ -63,6 +63,7 @@ struct Node {
     int mask_into = -1;                 // data gradient goes to this producer, ReLU-masked
     bool bias_in_wgrad = false;         // bias gradient computed by the weight-gradient GEMM
     bool bwd_by_consumer = false;       // (ReLU) its backward is fused into its consumer
+    bool wgrad_side = false;            // weight gradient on the stage's second stream
     size_t p_off = 0, p_cnt = 0;        // all parameters of the node
     size_t w_off = 0, b_off = 0;        // conv/fc weight, bias; bn gamma, beta
     ConvGeo geo{};
@@ -73,6 +74,10 @@ struct Node {
     // stage bf16 operands directly (made once per forward pass)
     uint16_t* y16 = nullptr;
     bool y16_ready = false;
+    // bf16 mode, conv / FC: bf16 copy of this node's output gradient (written by
+    // the BN backward that produces it, else cast before the weight gradient)
+    uint16_t* g16 = nullptr;
+    bool g16_ready = false;
 };
 
 size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
@@ -128,9 +133,15 @@ struct hp_stage {
     // stage input and (scratch, one conv at a time) of a conv's output gradient
     uint16_t* w16 = nullptr;
     uint16_t* x16 = nullptr;
-    uint16_t* g16 = nullptr;
     bool x16_ready = false;
-    int g16_node = -1;          // g16 already holds this conv's output gradient
+    // the weight gradients run on a second stream beside the data-gradient
+    // chain (they only feed the caller's gradient vector), with a workspace
+    // of their own; events order the two streams
+    hipStream_t side = nullptr;
+    std::vector<hipEvent_t> evs;
+    size_t ev_next = 0;
+    float* ws2 = nullptr;
+    size_t ws2_floats = 0;
     // forward bookkeeping for backward
     const float* fwd_w = nullptr;
     const float* fwd_x = nullptr;
@@ -252,11 +263,15 @@ int build_stage(hp_stage* st, const hp_layer* layers, int n_layers) {
                 nd.wgrad = plan_gemm(OP_WGRAD, nd.geo, st->dtype, cus,
                                      (L.bias && st->dtype == HP_FP32) ? 1 : 0);
                 nd.bias_in_wgrad = nd.wgrad.bias_col != 0;
+                // a small weight gradient (under 20 GFLOP) leaves most of the GPU
+                // idle: it runs beside the data-gradient chain; a large one fills
+                // the GPU by itself and stays in stream order
+                nd.wgrad_side = 2.0 * nd.wgrad.M * nd.wgrad.Ncols * nd.wgrad.Kred < 2e10;
+                size_t& wsw = nd.wgrad_side ? st->ws2_floats : st->ws_floats;
                 if (L.bias && !nd.bias_in_wgrad)
-                    st->ws_floats = std::max(st->ws_floats,
-                                             colsum_ws_floats((long)B * P * Q, L.K));
-                st->ws_floats = std::max({st->ws_floats, nd.fwd.ws_floats, nd.dgrad.ws_floats,
-                                          nd.wgrad.ws_floats});
+                    wsw = std::max(wsw, colsum_ws_floats((long)B * P * Q, L.K));
+                wsw = std::max(wsw, nd.wgrad.ws_floats);
+                st->ws_floats = std::max({st->ws_floats, nd.fwd.ws_floats, nd.dgrad.ws_floats});
                 break;
             }
             case HP_RELU:
@@ -355,24 +370,28 @@ int build_stage(hp_stage* st, const hp_layer* layers, int n_layers) {
         }
     }
     // bf16 operand copies for the contractions whose geometry allows them
-    size_t g16_elems = 0;
+    bool any16 = false;
     for (int i = 0; i < n_layers; ++i) {
         Node& nd = st->nodes[i];
         if ((nd.L.kind != HP_CONV && nd.L.kind != HP_FC) || !nd.fwd.h16) continue;
-        g16_elems = std::max(g16_elems, nd.out_elems);
+        any16 = true;
         const int j = nd.L.in0;
-        int rc = HP_OK;
-        if (j < 0 && !st->x16)
+        int rc = dev_alloc16(st, &nd.g16, nd.out_elems);
+        if (!rc && j < 0 && !st->x16)
             rc = dev_alloc16(st, &st->x16, (size_t)st->batch * st->H * st->W * st->C);
-        else if (j >= 0 && !st->nodes[j].y16)
+        else if (!rc && j >= 0 && !st->nodes[j].y16)
             rc = dev_alloc16(st, &st->nodes[j].y16, st->nodes[j].out_elems);
         if (rc) return rc;
     }
-    if (g16_elems) {
+    if (any16) {
         int rc = dev_alloc16(st, &st->w16, st->P);
-        if (!rc) rc = dev_alloc16(st, &st->g16, g16_elems);
         if (rc) return rc;
     }
+    int rc = dev_alloc(st, &st->ws2, std::max<size_t>(st->ws2_floats, 64));
+    if (rc) return rc;
+    HP_HIP(hipStreamCreateWithFlags(&st->side, hipStreamNonBlocking));
+    st->evs.resize(4, nullptr);
+    for (auto& e : st->evs) HP_HIP(hipEventCreateWithFlags(&e, hipEventDisableTiming));
     return dev_alloc(st, &st->ws, std::max<size_t>(st->ws_floats, 64));
 }
 
@@ -413,6 +432,10 @@ extern "C" int hp_stage_create(const hp_layer* layers, int n_layers, int batch, 
 extern "C" int hp_stage_destroy(hp_stage* st) {
     if (!st) return HP_OK;
     if (st->stream || !st->allocs.empty()) (void)hipStreamSynchronize(st->stream);
+    if (st->side) (void)hipStreamSynchronize(st->side);
+    for (auto e : st->evs)
+        if (e) (void)hipEventDestroy(e);
+    if (st->side) (void)hipStreamDestroy(st->side);
     for (void* p : st->allocs) (void)hipFree(p);
     delete st;
     return HP_OK;
@@ -603,7 +626,13 @@ extern "C" int hp_stage_backward(hp_stage* st, const float* w, const float* dy, 
         nd.g_alias = nullptr;
     }
     bool dx_written = false;
-    st->g16_node = -1;
+    for (Node& nd : st->nodes) nd.g16_ready = false;
+    // `a` happens before everything enqueued on `b` afterwards
+    auto order = [&](hipStream_t a, hipStream_t b) -> hipError_t {
+        hipEvent_t e = st->evs[st->ev_next++ % st->evs.size()];
+        hipError_t r = hipEventRecord(e, a);
+        return r == hipSuccess ? hipStreamWaitEvent(b, e, 0) : r;
+    };
     if (st->has_loss) st->nodes[st->nodes.back().L.in0].g_written = true;  // dz from forward
 
     // destination of a gradient sent to value j: (pointer, accumulate?)
@@ -644,25 +673,29 @@ extern "C" int hp_stage_backward(hp_stage* st, const float* w, const float* dy, 
                 const uint16_t* g16 = nullptr;
                 if (nd.fwd.h16 && st->w16) {
                     in16 = L.in0 < 0 ? st->x16 : st->nodes[L.in0].y16;
-                    if (st->g16_node != i) {
+                    if (!nd.g16_ready) {
                         tm.begin(1, s);
-                        e = launch_cast_bf16(gin, st->g16, nd.out_elems, s);
+                        e = launch_cast_bf16(gin, nd.g16, nd.out_elems, s);
                         tm.end(s);
                     }
-                    st->g16_node = -1;
-                    g16 = st->g16;
+                    g16 = nd.g16;
                 }
-                tm.begin(0, s);
+                // weight gradient (and a separate bias column sum), on the side
+                // stream once gin and its bf16 copy are complete
+                hipStream_t sd = nd.wgrad_side ? st->side : s;
+                float* wsw = nd.wgrad_side ? st->ws2 : st->ws;
+                if (e == hipSuccess && nd.wgrad_side) e = order(s, sd);
+                tm.begin(0, sd);
                 Epilogue wep;                     // bias gradient = appended column
                 wep.bias_out = nd.bias_in_wgrad ? grad + nd.b_off : nullptr;
                 if (e == hipSuccess)
-                    e = launch_gemm(nd.wgrad, nd.geo, in, gin, grad + nd.w_off, wep, st->ws, s,
+                    e = launch_gemm(nd.wgrad, nd.geo, in, gin, grad + nd.w_off, wep, wsw, sd,
                                     in16, g16);
-                tm.end(s);
+                tm.end(sd);
                 if (e == hipSuccess && L.bias && !nd.bias_in_wgrad) {
-                    tm.begin(1, s);
-                    e = launch_colsum(gin, (long)B * nd.H * nd.W, nd.C, grad + nd.b_off, st->ws, s);
-                    tm.end(s);
+                    tm.begin(1, sd);
+                    e = launch_colsum(gin, (long)B * nd.H * nd.W, nd.C, grad + nd.b_off, wsw, sd);
+                    tm.end(sd);
                 }
                 const int tgt = nd.mask_into >= 0 ? nd.mask_into : L.in0;
                 if (e == hipSuccess && dest(tgt, &d, &acc)) {
@@ -708,11 +741,11 @@ extern "C" int hp_stage_backward(hp_stage* st, const float* w, const float* dy, 
                 // that copy too when this BN is the conv's only consumer
                 uint16_t* d16 = nullptr;
                 if (want && L.in0 >= 0 && st->w16) {
-                    const Node& pc = st->nodes[L.in0];
+                    Node& pc = st->nodes[L.in0];
                     if ((pc.L.kind == HP_CONV || pc.L.kind == HP_FC) && pc.fwd.h16 &&
                         pc.consumers == 1) {
-                        d16 = st->g16;
-                        st->g16_node = L.in0;
+                        d16 = pc.g16;
+                        pc.g16_ready = true;
                     }
                 }
                 e = launch_bn_bwd(in, gin, nd.fuses_relu ? nd.y : nullptr, (long)B * nd.H * nd.W,
@@ -735,6 +768,8 @@ extern "C" int hp_stage_backward(hp_stage* st, const float* w, const float* dy, 
         int rc = launch_ok(e, "backward", i);
         if (rc) return rc;
     }
+    // the caller's stream sees the complete gradient
+    HP_HIP(order(st->side, s));
     st->fwd_done = false;
     return HP_OK;
 }
