@@ -128,129 +128,180 @@ __global__ void copy_or_acc_kernel(const float* __restrict__ v, float* __restric
 
 // max-pool forward: padded taps never win; the first maximum in row-major
 // window order is kept (strict '>' comparison).
+// max-pool forward: VEC consecutive channels of one output pixel per thread
+template <int VEC>
 __global__ void maxpool_fwd_kernel(const float* __restrict__ x, float* __restrict__ y, int N, int H,
                                    int W, int C, int R, int S, int st, int pad, int P, int Q,
                                    uint16_t* __restrict__ y16) {
     const size_t total = (size_t)N * P * Q * C;
-    for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
-         i += (size_t)gridDim.x * blockDim.x) {
-        int c = (int)(i % C);
+    for (size_t i = ((size_t)blockIdx.x * blockDim.x + threadIdx.x) * VEC; i < total;
+         i += (size_t)gridDim.x * blockDim.x * VEC) {
+        const int c = (int)(i % C);
         size_t t = i / C;
-        int q = (int)(t % Q); t /= Q;
-        int p = (int)(t % P);
-        int n = (int)(t / P);
-        float m = -INFINITY;
+        const int q = (int)(t % Q); t /= Q;
+        const int p = (int)(t % P);
+        const int n = (int)(t / P);
+        float m[VEC];
         bool any = false;
         for (int r = 0; r < R; ++r) {
-            int h = p * st - pad + r;
+            const int h = p * st - pad + r;
             if (h < 0 || h >= H) continue;
             for (int s = 0; s < S; ++s) {
-                int w = q * st - pad + s;
+                const int w = q * st - pad + s;
                 if (w < 0 || w >= W) continue;
-                float v = x[(((size_t)n * H + h) * W + w) * C + c];
-                if (!any || v > m) { m = v; any = true; }
+                float v[VEC];
+                ldv<VEC>(x + (((size_t)n * H + h) * W + w) * C + c, v);
+#pragma unroll
+                for (int j = 0; j < VEC; ++j)
+                    if (!any || v[j] > m[j]) m[j] = v[j];
+                any = true;
             }
         }
-        y[i] = m;
-        if (y16) y16[i] = (uint16_t)bf16_bits(m);
+        stv<VEC>(y + i, m);
+        if (y16) st16v<VEC>(y16 + i, m);
     }
 }
 
 // max-pool backward as a gather: each input element sums dy over the windows
-// whose first maximum it is (the window's argmax is recomputed from x).
+// whose first maximum it is (the window's argmax is recomputed from x), in
+// window order; VEC consecutive channels per thread.
+template <int VEC>
 __global__ void maxpool_bwd_kernel(const float* __restrict__ x, const float* __restrict__ dy,
                                    float* __restrict__ dx, int N, int H, int W, int C, int R,
                                    int S, int st, int pad, int P, int Q, int acc,
                                    const float* __restrict__ mask) {
     const size_t total = (size_t)N * H * W * C;
-    for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
-         i += (size_t)gridDim.x * blockDim.x) {
-        int c = (int)(i % C);
+    for (size_t i = ((size_t)blockIdx.x * blockDim.x + threadIdx.x) * VEC; i < total;
+         i += (size_t)gridDim.x * blockDim.x * VEC) {
+        const int c = (int)(i % C);
         size_t t = i / C;
-        int w0 = (int)(t % W); t /= W;
-        int h0 = (int)(t % H);
-        int n = (int)(t / H);
-        float sum = 0.f;
+        const int w0 = (int)(t % W); t /= W;
+        const int h0 = (int)(t % H);
+        const int n = (int)(t / H);
+        float sum[VEC];
+#pragma unroll
+        for (int j = 0; j < VEC; ++j) sum[j] = 0.f;
         for (int r = 0; r < R; ++r) {
-            int tp = h0 + pad - r;
+            const int tp = h0 + pad - r;
             if (tp < 0 || tp % st) continue;
-            int p = tp / st;
+            const int p = tp / st;
             if (p >= P) continue;
             for (int s = 0; s < S; ++s) {
-                int tq = w0 + pad - s;
+                const int tq = w0 + pad - s;
                 if (tq < 0 || tq % st) continue;
-                int q = tq / st;
+                const int q = tq / st;
                 if (q >= Q) continue;
-                // first argmax of window (p, q)
-                int best = -1;
-                float m = -INFINITY;
+                // first argmax of window (p, q), per channel
+                int best[VEC];
+                float m[VEC];
+#pragma unroll
+                for (int j = 0; j < VEC; ++j) { best[j] = -1; m[j] = 0.f; }
                 for (int rr = 0; rr < R; ++rr) {
-                    int h = p * st - pad + rr;
+                    const int h = p * st - pad + rr;
                     if (h < 0 || h >= H) continue;
                     for (int ss = 0; ss < S; ++ss) {
-                        int w = q * st - pad + ss;
+                        const int w = q * st - pad + ss;
                         if (w < 0 || w >= W) continue;
-                        float v = x[(((size_t)n * H + h) * W + w) * C + c];
-                        if (best < 0 || v > m) { m = v; best = rr * S + ss; }
+                        float v[VEC];
+                        ldv<VEC>(x + (((size_t)n * H + h) * W + w) * C + c, v);
+#pragma unroll
+                        for (int j = 0; j < VEC; ++j)
+                            if (best[j] < 0 || v[j] > m[j]) { m[j] = v[j]; best[j] = rr * S + ss; }
                     }
                 }
-                if (best == r * S + s) sum += dy[(((size_t)n * P + p) * Q + q) * C + c];
+                float g[VEC];
+                ldv<VEC>(dy + (((size_t)n * P + p) * Q + q) * C + c, g);
+#pragma unroll
+                for (int j = 0; j < VEC; ++j)
+                    if (best[j] == r * S + s) sum[j] += g[j];
             }
         }
-        if (mask && !(mask[i] > 0.f)) sum = 0.f;
-        dx[i] = acc ? dx[i] + sum : sum;
+        if (mask) {
+            float mk[VEC];
+            ldv<VEC>(mask + i, mk);
+#pragma unroll
+            for (int j = 0; j < VEC; ++j)
+                if (!(mk[j] > 0.f)) sum[j] = 0.f;
+        }
+        if (acc) {
+            float d[VEC];
+            ldv<VEC>(dx + i, d);
+#pragma unroll
+            for (int j = 0; j < VEC; ++j) sum[j] = d[j] + sum[j];
+        }
+        stv<VEC>(dx + i, sum);
     }
 }
 
 // max-pool backward for non-overlapping windows (window = stride, no padding,
-// windows tile the input exactly): one thread per output element writes its
-// whole window -- dy at the first maximum, zero elsewhere.
-template <int RT>   // RT > 0: window size fixed at compile time; 0: runtime R
+// windows tile the input exactly): one thread per output pixel and VEC
+// channels writes its whole window (dy at the first argmax, zero elsewhere).
+// RT > 0 fixes the window edge at compile time and keeps the taps in
+// registers; when the pooled input is a ReLU output the taps are the mask.
+template <int RT, int VEC>
 __global__ void maxpool_bwd_tiled_kernel(const float* __restrict__ x, const float* __restrict__ dy,
                                          float* __restrict__ dx, int N, int H, int W, int C, int Rr,
                                          int P, int Q, int acc, const float* __restrict__ mask) {
     const int R = RT > 0 ? RT : Rr;
     const size_t total = (size_t)N * P * Q * C;
-    for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
-         i += (size_t)gridDim.x * blockDim.x) {
-        int c = (int)(i % C);
+    for (size_t i = ((size_t)blockIdx.x * blockDim.x + threadIdx.x) * VEC; i < total;
+         i += (size_t)gridDim.x * blockDim.x * VEC) {
+        const int c = (int)(i % C);
         size_t t = i / C;
-        int q = (int)(t % Q); t /= Q;
-        int p = (int)(t % P);
-        int n = (int)(t / P);
+        const int q = (int)(t % Q); t /= Q;
+        const int p = (int)(t % P);
+        const int n = (int)(t / P);
         const size_t base = (((size_t)n * H + p * R) * W + q * R) * C + c;
-        const float g = dy[i];
+        float g[VEC];
+        ldv<VEC>(dy + i, g);
         if constexpr (RT > 0) {
-            // taps kept in registers; when pooling a ReLU output the taps are the mask
-            float v[RT * RT];
-            int best = 0;
+            float v[RT * RT][VEC];
+            float m[VEC];
+            int best[VEC];
 #pragma unroll
             for (int k = 0; k < RT * RT; ++k) {
-                v[k] = x[base + ((size_t)(k / RT) * W + k % RT) * C];
-                if (v[k] > v[best]) best = k;
+                ldv<VEC>(x + base + ((size_t)(k / RT) * W + k % RT) * C, v[k]);
+#pragma unroll
+                for (int j = 0; j < VEC; ++j)
+                    if (k == 0 || v[k][j] > m[j]) { m[j] = v[k][j]; best[j] = k; }
             }
 #pragma unroll
             for (int k = 0; k < RT * RT; ++k) {
-                size_t j = base + ((size_t)(k / RT) * W + k % RT) * C;
-                float o = (k == best) ? g : 0.f;
-                if (mask && !((mask == x ? v[k] : mask[j]) > 0.f)) o = 0.f;
-                dx[j] = acc ? dx[j] + o : o;
+                const size_t e = base + ((size_t)(k / RT) * W + k % RT) * C;
+                float o[VEC], mk[VEC], d[VEC];
+                if (mask && mask != x) ldv<VEC>(mask + e, mk);
+                if (acc) ldv<VEC>(dx + e, d);
+#pragma unroll
+                for (int j = 0; j < VEC; ++j) {
+                    o[j] = (k == best[j]) ? g[j] : 0.f;
+                    if (mask && !((mask == x ? v[k][j] : mk[j]) > 0.f)) o[j] = 0.f;
+                    if (acc) o[j] = d[j] + o[j];
+                }
+                stv<VEC>(dx + e, o);
             }
         } else {
-            int best = 0;
-            float m = x[base];
-            for (int r = 0; r < R; ++r)
-                for (int s = 0; s < R; ++s) {
-                    float v = x[base + ((size_t)r * W + s) * C];
-                    if (v > m) { m = v; best = r * R + s; }
+            float m[VEC];
+            int best[VEC];
+            for (int k = 0; k < R * R; ++k) {
+                float v[VEC];
+                ldv<VEC>(x + base + ((size_t)(k / R) * W + k % R) * C, v);
+#pragma unroll
+                for (int j = 0; j < VEC; ++j)
+                    if (k == 0 || v[j] > m[j]) { m[j] = v[j]; best[j] = k; }
+            }
+            for (int k = 0; k < R * R; ++k) {
+                const size_t e = base + ((size_t)(k / R) * W + k % R) * C;
+                float o[VEC], mk[VEC], d[VEC];
+                if (mask) ldv<VEC>(mask + e, mk);
+                if (acc) ldv<VEC>(dx + e, d);
+#pragma unroll
+                for (int j = 0; j < VEC; ++j) {
+                    o[j] = (k == best[j]) ? g[j] : 0.f;
+                    if (mask && !(mk[j] > 0.f)) o[j] = 0.f;
+                    if (acc) o[j] = d[j] + o[j];
                 }
-            for (int r = 0; r < R; ++r)
-                for (int s = 0; s < R; ++s) {
-                    size_t j = base + ((size_t)r * W + s) * C;
-                    float o = (r * R + s == best) ? g : 0.f;
-                    if (mask && !(mask[j] > 0.f)) o = 0.f;
-                    dx[j] = acc ? dx[j] + o : o;
-                }
+                stv<VEC>(dx + e, o);
+            }
         }
     }
 }
@@ -656,27 +707,43 @@ hipError_t launch_copy_or_acc(const float* v, float* out, size_t n, int accumula
 hipError_t launch_maxpool_fwd(const float* x, float* y, int N, int H, int W, int C, int R, int S,
                               int st, int pad, int P, int Q, hipStream_t s, uint16_t* y16) {
     size_t n = (size_t)N * P * Q * C;
-    hipLaunchKernelGGL(maxpool_fwd_kernel, dim3(ew_blocks(n)), dim3(EW_THREADS), 0, s, x, y, N, H,
-                       W, C, R, S, st, pad, P, Q, y16);
+    if (C % 4 == 0 && aligned16({x, y}) && ((uintptr_t)y16 & 7) == 0)
+        hipLaunchKernelGGL(maxpool_fwd_kernel<4>, dim3(ew_blocks(n / 4)), dim3(EW_THREADS), 0, s, x,
+                           y, N, H, W, C, R, S, st, pad, P, Q, y16);
+    else
+        hipLaunchKernelGGL(maxpool_fwd_kernel<1>, dim3(ew_blocks(n)), dim3(EW_THREADS), 0, s, x, y,
+                           N, H, W, C, R, S, st, pad, P, Q, y16);
     return hipGetLastError();
 }
 
 hipError_t launch_maxpool_bwd(const float* x, const float* dy, float* dx, int N, int H, int W,
                               int C, int R, int S, int st, int pad, int P, int Q, int accumulate,
                               const float* mask, hipStream_t s) {
+    const bool v4 = C % 4 == 0 && aligned16({x, dy, dx, mask});
     if (R == S && R == st && pad == 0 && P * st == H && Q * st == W) {
         size_t n = (size_t)N * P * Q * C;
-        if (R == 2)
-            hipLaunchKernelGGL(maxpool_bwd_tiled_kernel<2>, dim3(ew_blocks(n)), dim3(EW_THREADS), 0,
-                               s, x, dy, dx, N, H, W, C, R, P, Q, accumulate, mask);
+        const dim3 g(ew_blocks(v4 ? n / 4 : n)), b(EW_THREADS);
+        if (R == 2 && v4)
+            hipLaunchKernelGGL((maxpool_bwd_tiled_kernel<2, 4>), g, b, 0, s, x, dy, dx, N, H, W, C,
+                               R, P, Q, accumulate, mask);
+        else if (R == 2)
+            hipLaunchKernelGGL((maxpool_bwd_tiled_kernel<2, 1>), g, b, 0, s, x, dy, dx, N, H, W, C,
+                               R, P, Q, accumulate, mask);
+        else if (v4)
+            hipLaunchKernelGGL((maxpool_bwd_tiled_kernel<0, 4>), g, b, 0, s, x, dy, dx, N, H, W, C,
+                               R, P, Q, accumulate, mask);
         else
-            hipLaunchKernelGGL(maxpool_bwd_tiled_kernel<0>, dim3(ew_blocks(n)), dim3(EW_THREADS), 0,
-                               s, x, dy, dx, N, H, W, C, R, P, Q, accumulate, mask);
+            hipLaunchKernelGGL((maxpool_bwd_tiled_kernel<0, 1>), g, b, 0, s, x, dy, dx, N, H, W, C,
+                               R, P, Q, accumulate, mask);
         return hipGetLastError();
     }
     size_t n = (size_t)N * H * W * C;
-    hipLaunchKernelGGL(maxpool_bwd_kernel, dim3(ew_blocks(n)), dim3(EW_THREADS), 0, s, x, dy, dx,
-                       N, H, W, C, R, S, st, pad, P, Q, accumulate, mask);
+    if (v4)
+        hipLaunchKernelGGL(maxpool_bwd_kernel<4>, dim3(ew_blocks(n / 4)), dim3(EW_THREADS), 0, s, x,
+                           dy, dx, N, H, W, C, R, S, st, pad, P, Q, accumulate, mask);
+    else
+        hipLaunchKernelGGL(maxpool_bwd_kernel<1>, dim3(ew_blocks(n)), dim3(EW_THREADS), 0, s, x, dy,
+                           dx, N, H, W, C, R, S, st, pad, P, Q, accumulate, mask);
     return hipGetLastError();
 }
 
