@@ -168,6 +168,16 @@ int hp_vw_destroy(hp_vw *vw);
  * not succeeded. */
 int hp_wsp_weights(hp_vw *vw, const float **w);
 
+/* Momentum for this VW's local updates (an optimizer variant; the paper's
+ * update is plain SGD, mu = 0): from now on hp_wsp_local_update computes
+ *   v = mu * v + grad;  u = (-lr) * v
+ * (heavy ball, no dampening, one rounding per operation) in place of
+ * u = (-lr) * grad.  The velocity v (P floats, owned by the VW, local to it and
+ * never pushed) is reset to zero by every call; mu = 0 restores plain SGD.
+ * Errors: HP_ERR_ARG unless 0 <= mu < 1; HP_ERR_STATE while minibatches are
+ * in flight. */
+int hp_vw_set_momentum(hp_vw *vw, float mu);
+
 /* Local update after the oldest in-flight minibatch q = p+1 completes (Sec. 4:
  * w_local = w_local + u_q, u_q = -lr * grad) and wave accumulation (Sec. 5:
  * u~ sums the wave's u_q).

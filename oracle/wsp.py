@@ -39,6 +39,14 @@ Vector arithmetic is IEEE binary32 with round-to-nearest-even, one operation
 at a time (no fused multiply-add):  u = (-lr) * g,  new = newest + u,
 u~ = u (first minibatch of a wave) or u~ + u,  w_g = w_g + u~.
 
+Optimizer variants (beyond the paper's plain SGD step):
+  * ``lr`` may be a function lr(n, q) giving the step size of minibatch q of
+    VW n, e.g. the eta_t = sigma / sqrt(t) schedule of Theorem 1 (see
+    ``theorem1_schedule``);
+  * ``momentum`` mu != 0 keeps a velocity per VW, updated at every local
+    update before the step (heavy ball, no dampening):  v = mu * v + g,
+    u = (-lr) * v; the velocity is local to the VW and is never pushed.
+
 Every minibatch, push, pull and block is appended to ``events``:
   ("mb", n, q, V)        V = version vector of w_q: updates of each VW in it
   ("push", n, c, c_g)    local clock after the push and the new global clock
@@ -55,14 +63,15 @@ class DeadlockError(RuntimeError):
 
 
 class WSP:
-    def __init__(self, w0, N: int, s_local: int, D: int, lr: float, grad_fn,
-                 periods=None, dtype=np.float32, record=False):
+    def __init__(self, w0, N: int, s_local: int, D: int, lr, grad_fn,
+                 periods=None, dtype=np.float32, record=False, momentum=0.0):
         self.N = N
         self.W = s_local + 1
         self.s_local = s_local
         self.D = D
         self.dtype = dtype
-        self.neg_lr = -dtype(lr) if dtype is not object else -lr
+        self.lr = lr if callable(lr) else (lambda n, q, _lr=lr: _lr)
+        self.mu = dtype(momentum) if dtype is not object else momentum
         self.grad_fn = grad_fn
         self.T = list(periods) if periods is not None else [1] * N
         assert len(self.T) == N
@@ -72,6 +81,7 @@ class WSP:
         self.ring = [[w0.copy() for _ in range(W)] for _ in range(N)]
         self.VR = [[[0] * N for _ in range(W)] for _ in range(N)]
         self.ut = [np.zeros_like(w0) for _ in range(N)]
+        self.vel = [np.zeros_like(w0) for _ in range(N)]
         self.p = [0] * N          # minibatches completed
         self.c = [0] * N          # local clock = waves completed
         self.g = [0] * N          # global clock of the last pull
@@ -106,7 +116,13 @@ class WSP:
         w_q = self.ring[n][slot]
         self.events.append(("mb", n, q, tuple(self.VR[n][slot])))
         grad = np.asarray(self.grad_fn(n, q, w_q), dtype=self.dtype)
-        u = self.neg_lr * grad
+        lr = self.lr(n, q)
+        neg_lr = -self.dtype(lr) if self.dtype is not object else -lr
+        if self.mu != 0:
+            self.vel[n] = self._vec_add(self.mu * self.vel[n], grad)
+            u = neg_lr * self.vel[n]
+        else:
+            u = neg_lr * grad
         new = self._vec_add(self.ring[n][newest], u)
         vnew = list(self.VR[n][newest])
         vnew[n] += 1
@@ -166,6 +182,15 @@ class WSP:
             n = min(cand, key=lambda m: (self.t[m], m))
             self._minibatch(n, self.t[n])
         return self.events
+
+
+def theorem1_schedule(sigma: float, N: int):
+    """eta_t = sigma / sqrt(t) of Theorem 1 as a step-size function lr(n, q).
+    The theorem numbers the updates of all VWs in one sequence that takes the
+    VWs in turn: minibatch q of VW n is update t = (q - 1) * N + n + 1."""
+    def lr(n, q):
+        return sigma / np.sqrt((q - 1) * N + n + 1)
+    return lr
 
 
 def s_global(D: int, s_local: int) -> int:

@@ -169,6 +169,8 @@ struct hp_vw {
     size_t P = 0, stride = 0;
     float* ring = nullptr;
     float* ut = nullptr;
+    float* vel = nullptr;      // momentum velocity (allocated by hp_vw_set_momentum)
+    float mu = 0.f;
     int64_t p = 0;
     int c = 0, g = 0;
     int inflight = 0;                      // started, not yet completed (at most W)
@@ -886,7 +888,26 @@ extern "C" int hp_vw_destroy(hp_vw* v) {
     }
     (void)hipFree(v->ring);
     (void)hipFree(v->ut);
+    if (v->vel) (void)hipFree(v->vel);
     delete v;
+    return HP_OK;
+}
+
+extern "C" int hp_vw_set_momentum(hp_vw* v, float mu) {
+    if (!v) return fail(HP_ERR_ARG, "hp_vw_set_momentum: NULL VW");
+    if (!v->ps) return fail(HP_ERR_STATE, "hp_vw_set_momentum: parameter server destroyed");
+    if (!(mu >= 0.f && mu < 1.f))
+        return fail(HP_ERR_ARG, "hp_vw_set_momentum: momentum %g outside [0, 1)", (double)mu);
+    if (v->inflight)
+        return fail(HP_ERR_STATE, "hp_vw_set_momentum: VW %d has minibatches in flight", v->id);
+    if (mu != 0.f && !v->vel) {
+        hipError_t e = hipMalloc(&v->vel, v->stride * sizeof(float));
+        if (e != hipSuccess)
+            return fail(e == hipErrorOutOfMemory ? HP_ERR_NOMEM : HP_ERR_HIP,
+                        "hp_vw_set_momentum: %s", hipGetErrorString(e));
+    }
+    if (v->vel) HP_HIP(hipMemsetAsync(v->vel, 0, v->stride * sizeof(float), v->ps->stream));
+    v->mu = mu;
     return HP_OK;
 }
 
@@ -917,9 +938,13 @@ extern "C" int hp_wsp_local_update(hp_vw* v, const float* grad, float lr) {
     const int first = ((q - 1) % W) == 0;
     StageTimer& tm = v->ps->timer;
     tm.begin(first ? 0 : 1, v->ps->stream);
-    hipError_t e = launch_wsp_local_update(grad, v->ring + (size_t)newest * v->stride,
-                                           v->ring + (size_t)slot * v->stride, v->ut, v->P, lr,
-                                           first, v->ps->stream);
+    hipError_t e = v->mu != 0.f
+        ? launch_wsp_local_update_momentum(grad, v->ring + (size_t)newest * v->stride,
+                                           v->ring + (size_t)slot * v->stride, v->ut, v->vel,
+                                           v->P, lr, v->mu, first, v->ps->stream)
+        : launch_wsp_local_update(grad, v->ring + (size_t)newest * v->stride,
+                                  v->ring + (size_t)slot * v->stride, v->ut, v->P, lr, first,
+                                  v->ps->stream);
     tm.end(v->ps->stream);
     if (e != hipSuccess) return fail(HP_ERR_HIP, "local update launch: %s", hipGetErrorString(e));
     std::vector<int64_t> nv = v->V[newest];

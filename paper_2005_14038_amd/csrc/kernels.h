@@ -121,6 +121,10 @@ hipError_t launch_softmax_ce(const float* z, const int32_t* labels, int B, int K
 // u = (-lr)*g; dst = newest + u; ut = first ? u : ut + u   (no FMA contraction)
 hipError_t launch_wsp_local_update(const float* g, const float* newest, float* dst, float* ut,
                                    size_t n, float lr, int first, hipStream_t s);
+// with momentum: v = mu*v + g; u = (-lr)*v; then as above
+hipError_t launch_wsp_local_update_momentum(const float* g, const float* newest, float* dst,
+                                            float* ut, float* vel, size_t n, float lr, float mu,
+                                            int first, hipStream_t s);
 // wg = wg + ut
 hipError_t launch_wsp_push(float* wg, const float* ut, size_t n, hipStream_t s);
 // dst = src

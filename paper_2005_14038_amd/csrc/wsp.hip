@@ -99,6 +99,65 @@ local_update_kernel(const float* __restrict__ g, const float* newest, float* dst
     }
 }
 
+// Local update with momentum (heavy ball, no dampening): v = mu * v + g,
+// u = (-lr) * v, then as above.  One rounding per operation.
+template <bool FIRST, int U>
+__global__ void __launch_bounds__(WSP_THREADS)
+local_update_momentum_kernel(const float* __restrict__ g, const float* newest, float* dst,
+                             float* __restrict__ ut, float* __restrict__ vel, size_t n,
+                             float neg_lr, float mu, int vec) {
+    const size_t n4 = vec ? n / 4 : 0;
+    const float4* g4 = reinterpret_cast<const float4*>(g);
+    const float4* w4 = reinterpret_cast<const float4*>(newest);
+    float4* d4 = reinterpret_cast<float4*>(dst);
+    float4* u4 = reinterpret_cast<float4*>(ut);
+    float4* v4 = reinterpret_cast<float4*>(vel);
+    WSP_VECTOR_LOOP(n4) {
+        float4 gv[U], wv[U], vv[U], av[U];
+#pragma unroll
+        for (int k = 0; k < U; ++k) {
+            const size_t i = base + (size_t)k * blockDim.x;
+            if (i < n4) {
+                gv[k] = ld4(g4 + i);
+                wv[k] = ld4(w4 + i);
+                vv[k] = ld4(v4 + i);
+                if (!FIRST) av[k] = ld4(u4 + i);
+            }
+        }
+#pragma unroll
+        for (int k = 0; k < U; ++k) {
+            const size_t i = base + (size_t)k * blockDim.x;
+            if (i >= n4) break;
+            float4 v;
+            v.x = add_rn(mul_rn(mu, vv[k].x), gv[k].x); v.y = add_rn(mul_rn(mu, vv[k].y), gv[k].y);
+            v.z = add_rn(mul_rn(mu, vv[k].z), gv[k].z); v.w = add_rn(mul_rn(mu, vv[k].w), gv[k].w);
+            v4[i] = v;
+            float4 u;
+            u.x = mul_rn(neg_lr, v.x); u.y = mul_rn(neg_lr, v.y);
+            u.z = mul_rn(neg_lr, v.z); u.w = mul_rn(neg_lr, v.w);
+            float4 nw;
+            nw.x = add_rn(wv[k].x, u.x); nw.y = add_rn(wv[k].y, u.y);
+            nw.z = add_rn(wv[k].z, u.z); nw.w = add_rn(wv[k].w, u.w);
+            d4[i] = nw;
+            if (FIRST) {
+                u4[i] = u;
+            } else {
+                float4 a = av[k];
+                a.x = add_rn(a.x, u.x); a.y = add_rn(a.y, u.y);
+                a.z = add_rn(a.z, u.z); a.w = add_rn(a.w, u.w);
+                u4[i] = a;
+            }
+        }
+    }
+    for (size_t i = n4 * 4 + (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
+        const float v = add_rn(mul_rn(mu, vel[i]), g[i]);
+        vel[i] = v;
+        const float u = mul_rn(neg_lr, v);
+        dst[i] = add_rn(newest[i], u);
+        ut[i] = FIRST ? u : add_rn(ut[i], u);
+    }
+}
+
 template <int U>
 __global__ void __launch_bounds__(WSP_THREADS)
 push_kernel(float* __restrict__ wg, const float* __restrict__ ut, size_t n, int vec) {
@@ -176,6 +235,29 @@ hipError_t launch_wsp_local_update(const float* g, const float* newest, float* d
     else
         hipLaunchKernelGGL((local_update_kernel<false, 1>), grid, block, 0, s, g, newest, dst, ut, n,
                            neg_lr, vec);
+    return hipGetLastError();
+}
+
+hipError_t launch_wsp_local_update_momentum(const float* g, const float* newest, float* dst,
+                                            float* ut, float* vel, size_t n, float lr, float mu,
+                                            int first, hipStream_t s) {
+    const float neg_lr = -lr;
+    const int vec = aligned16(g, newest, dst, ut) && aligned16(vel, vel);
+    const size_t n4 = vec ? n / 4 : n;
+    const int u = wsp_unroll(n4);
+    const dim3 grid(wsp_blocks(n4, u)), block(WSP_THREADS);
+    if (first && u == 4)
+        hipLaunchKernelGGL((local_update_momentum_kernel<true, 4>), grid, block, 0, s, g, newest,
+                           dst, ut, vel, n, neg_lr, mu, vec);
+    else if (first)
+        hipLaunchKernelGGL((local_update_momentum_kernel<true, 1>), grid, block, 0, s, g, newest,
+                           dst, ut, vel, n, neg_lr, mu, vec);
+    else if (u == 4)
+        hipLaunchKernelGGL((local_update_momentum_kernel<false, 4>), grid, block, 0, s, g, newest,
+                           dst, ut, vel, n, neg_lr, mu, vec);
+    else
+        hipLaunchKernelGGL((local_update_momentum_kernel<false, 1>), grid, block, 0, s, g, newest,
+                           dst, ut, vel, n, neg_lr, mu, vec);
     return hipGetLastError();
 }
 

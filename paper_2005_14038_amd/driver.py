@@ -2,8 +2,9 @@
 
 Each minibatch runs through the C ABI: hp_wsp_weights (the ring version with
 the local updates 1..q-W, HetPipe Sec. 4), hp_stage_forward and
-hp_stage_backward at those weights, hp_wsp_local_update (u = -lr g, ring
-write, wave accumulation), and at a wave end hp_wsp_push_wave followed by
+hp_stage_backward at those weights, hp_wsp_local_update (u = -lr g, or with
+momentum u = -lr v, v = mu v + g; ring write, wave accumulation; lr may
+change per minibatch, e.g. the sigma/sqrt(t) schedule of Theorem 1), and at a wave end hp_wsp_push_wave followed by
 hp_wsp_pull, the clock-distance gate of Sec. 5.  A VW whose pull reports
 HP_WOULD_BLOCK stops until another VW's push lets its pull succeed.
 
@@ -29,18 +30,23 @@ class Deadlock(RuntimeError):
 
 
 class WSPDriver:
-    def __init__(self, stage: Stage, w0: torch.Tensor, N: int, s_local: int, D: int, lr: float,
+    def __init__(self, stage: Stage, w0: torch.Tensor, N: int, s_local: int, D: int, lr,
                  data_fn, periods=None, stream=None, need_dx=False, on_minibatch=None,
-                 grad_fn=None, P=None):
+                 grad_fn=None, P=None, momentum=0.0):
         # grad_fn(n, q, w_ptr, grad): fill `grad` without a stage (WSP-only runs)
         self.stage = stage
         self.grad_fn = grad_fn
-        self.N, self.W, self.D, self.lr = N, s_local + 1, D, lr
+        # lr: a step size, or a function lr(n, q) of the VW and its minibatch
+        self.N, self.W, self.D = N, s_local + 1, D
+        self.lr = lr if callable(lr) else (lambda n, q, _lr=lr: _lr)
         self.data_fn = data_fn
         self.T = list(periods) if periods else [1] * N
         self.P = stage.P if stage is not None else P
         self.ps = ParameterServer(self.P, w0, N, D, stream)
         self.vws = [VirtualWorker(self.ps, n, s_local) for n in range(N)]
+        if momentum:
+            for v in self.vws:
+                v.set_momentum(momentum)
         dev = w0.device
         self.grad = torch.empty(max(self.P, 1), dtype=torch.float32, device=dev)
         self.loss = torch.empty(1, dtype=torch.float32, device=dev)
@@ -80,7 +86,7 @@ class WSPDriver:
             self.stage.backward(w, dy, self.dx, self.grad)
         if self.on_minibatch is not None:
             self.on_minibatch(n, q, self)
-        vw.local_update(self.grad, self.lr)
+        vw.local_update(self.grad, self.lr(n, q))
         if q % self.W == 0:
             self._push_and_gate(n)
         self.t[n] += self.T[n]

@@ -27,7 +27,8 @@ EXPORTS = [
     "hp_stage_read_timing", "hp_stage_forward", "hp_stage_backward",
     "hp_ps_create", "hp_ps_destroy", "hp_ps_weights", "hp_ps_clock", "hp_ps_set_timing",
     "hp_ps_read_timing",
-    "hp_vw_create", "hp_vw_destroy", "hp_wsp_weights", "hp_wsp_local_update",
+    "hp_vw_create", "hp_vw_destroy", "hp_vw_set_momentum", "hp_wsp_weights",
+    "hp_wsp_local_update",
     "hp_wsp_push_wave", "hp_wsp_pull", "hp_wsp_state", "hp_wsp_version", "hp_wsp_buffers",
     "hp_last_error",
 ]
@@ -88,6 +89,7 @@ def lib():
                                     ctypes.POINTER(ctypes.c_int64 * 4)]
     L.hp_vw_create.argtypes = [_vp, i32, i32, _pp]
     L.hp_vw_destroy.argtypes = [_vp]
+    L.hp_vw_set_momentum.argtypes = [_vp, ctypes.c_float]
     L.hp_wsp_weights.argtypes = [_vp, _pp]
     L.hp_wsp_local_update.argtypes = [_vp, _vp, ctypes.c_float]
     L.hp_wsp_push_wave.argtypes = [_vp, _vp]
@@ -263,6 +265,9 @@ class VirtualWorker:
             self.h = None
 
     __del__ = close
+
+    def set_momentum(self, mu):
+        _check(self._L.hp_vw_set_momentum(self.h, ctypes.c_float(mu)))
 
     def weights(self):
         p = ctypes.c_void_p()

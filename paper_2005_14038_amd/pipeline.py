@@ -275,7 +275,7 @@ class PipelinedVW:
         self.parts = split(layers, cuts, H, W, C)
         self.k = len(self.parts)
         self.W = s_local + 1
-        self.lr = lr
+        self.lr = lr if callable(lr) else (lambda n, q, _lr=lr: _lr)
         self.batch = batch
         self.data_fn = data_fn
         self.d_fwd, self.d_bwd = d_fwd, d_bwd
@@ -372,7 +372,7 @@ class PipelinedVW:
         """Minibatch m completed: local update, push / pull at a wave end, then
         the next minibatch enters."""
         self._wait(self.ps_stream, ("B", m, 0))
-        self.vw.local_update(self.grads[slot], self.lr)
+        self.vw.local_update(self.grads[slot], self.lr(0, m))
         if m % self.W == 0:
             self.vw.push_wave()
             s = self.vw.state()

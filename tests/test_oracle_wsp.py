@@ -261,3 +261,65 @@ def test_stopped_worker_deadlocks_the_others():
     # the other VWs got at most D+1 waves ahead of the stopped one before blocking
     assert all(sim.blocked[n] for n in (0, 1))
     del W
+
+
+# ---------------------------------------------------------------- optimizer variants
+
+def test_theorem1_schedule_numbers_updates_across_workers():
+    # Theorem 1: eta_t = sigma / sqrt(t); the updates of all VWs form one
+    # sequence taking the VWs in turn (minibatch q of VW n is update (q-1)N+n+1)
+    lr = wsp.theorem1_schedule(0.6, 3)
+    assert lr(0, 1) == pytest.approx(0.6)
+    assert lr(2, 1) == pytest.approx(0.6 / np.sqrt(3))
+    assert lr(0, 2) == pytest.approx(0.3)
+    assert lr(1, 5) == pytest.approx(0.6 / np.sqrt(14))
+
+
+def test_schedule_single_worker_is_plain_sgd():
+    # N = 1, s_local = 0: w_{t+1} = w_t - sigma/sqrt(t) * grad(w_t)
+    a = np.array([0.5, -1.0, 2.0], np.float32)
+    w0 = np.array([1.0, 2.0, -3.0], np.float32)
+    lr = wsp.theorem1_schedule(0.3, 1)
+    sim = wsp.WSP(w0, 1, 0, 0, lr, lambda n, q, w: w - a)
+    sim.run(6)
+    w = w0.copy()
+    for t in range(1, 7):
+        w = w + (-np.float32(0.3 / np.sqrt(t))) * (w - a)
+    np.testing.assert_array_equal(sim.ring[0][0], w)
+
+
+def test_momentum_matches_heavy_ball_matrix_power():
+    # f(w) = a w^2 / 2, N = 1, no staleness: heavy ball is the linear map
+    # (w, v) -> (w - eta (mu v + a w), mu v + a w); k steps = k-th matrix power
+    a, eta, mu, w0 = Fraction(3, 2), Fraction(1, 5), Fraction(2, 3), Fraction(7, 4)
+    sim = wsp.WSP(np.array([w0], dtype=object), 1, 0, 0, eta,
+                   lambda n, q, w: np.array([a * w[0]], dtype=object), dtype=object,
+                   momentum=mu)
+    sim.run(7)
+    Mx = [[1 - eta * a, -eta * mu], [a, mu]]
+
+    def mul(A, B):
+        return [[sum(A[i][k] * B[k][j] for k in range(2)) for j in range(2)] for i in range(2)]
+    Pw = [[1, 0], [0, 1]]
+    for _ in range(7):
+        Pw = mul(Mx, Pw)
+    assert sim.ring[0][0][0] == Pw[0][0] * w0
+    assert sim.vel[0][0] == Pw[1][0] * w0
+
+
+def test_momentum_with_local_staleness_brute_force():
+    # N = 1, W = 3: minibatch q reads w0 + sum of u_1..u_{q-3}; velocity and
+    # steps follow completion order.  Written directly from those two rules.
+    a, eta, mu = Fraction(1, 2), Fraction(1, 3), Fraction(1, 2)
+    w0 = Fraction(5)
+    sim = wsp.WSP(np.array([w0], dtype=object), 1, 2, 0, eta,
+                   lambda n, q, w: np.array([a * w[0] - 1], dtype=object), dtype=object,
+                   momentum=mu)
+    sim.run(4)
+    us, v = [], Fraction(0)
+    for q in range(1, 13):
+        wq = w0 + sum(us[:max(0, q - 3)])
+        v = mu * v + (a * wq - 1)
+        us.append(-eta * v)
+    assert sim.wg[0] == w0 + sum(us)
+    assert sim.vel[0][0] == v
