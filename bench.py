@@ -18,6 +18,7 @@ events around every launch during K further steps of the same schedule, and
 the CPU oracle baseline.
 """
 import argparse
+import dataclasses
 import hashlib
 import json
 import os
@@ -201,6 +202,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-images", type=int, default=4,
                     help="images of the oracle's bounded CPU sample")
+    ap.add_argument("--dtype", choices=["fp32", "bf16"], default=None,
+                    help="contraction mode (default: the workload's); bf16 rounds the "
+                         "contraction operands and keeps fp32 master weights")
     ap.add_argument("--pipeline", type=int, default=0, metavar="K",
                     help="run one virtual worker as a K-partition pipeline on K streams "
                          "(workloads with a loss head) instead of the stage step")
@@ -220,6 +224,8 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda:0")
     wl = workloads.WORKLOADS[args.workload]
+    if args.dtype is not None:
+        wl = dataclasses.replace(wl, dtype=args.dtype)
     if args.pipeline:
         return run_pipeline(args, wl, dev)
     b = wl.builder()

@@ -619,6 +619,47 @@ __global__ void cast_bf16_kernel(const float* __restrict__ src, uint16_t* __rest
         dst[i] = (uint16_t)bf16_bits(src[i]);
 }
 
+// Transposed bf16 copies of conv/FC weights for the data gradient:
+// dst[off + (c * RS + rs) * K + k] = bf16(src[off + (k * RS + rs) * C + c]) for
+// every layer of the table.  A workgroup transposes one 64 (k) x 64 (c) tile
+// of one tap through LDS, so that both the reads (along c) and the writes
+// (along k) are contiguous; it finds its layer by binary search over the
+// layers' first tile numbers.
+constexpr int WT_T = WT_TILE;
+
+__global__ void __launch_bounds__(256) cast_bf16_t_kernel(const float* __restrict__ src,
+                                                          uint16_t* __restrict__ dst,
+                                                          const WtLayer* __restrict__ table,
+                                                          int nlayers) {
+    __shared__ float tile[WT_T][WT_T + 1];
+    const int b = blockIdx.x;
+    int lo = 0, hi = nlayers - 1;      // last layer whose first tile is <= b
+    while (lo < hi) {
+        const int mid = (lo + hi + 1) / 2;
+        if (table[mid].tile0 <= b) lo = mid;
+        else hi = mid - 1;
+    }
+    const WtLayer L = table[lo];
+    const int tkn = (L.K + WT_T - 1) / WT_T, tcn = (L.C + WT_T - 1) / WT_T;
+    int tl = b - L.tile0;
+    const int c0 = (tl % tcn) * WT_T;
+    tl /= tcn;
+    const int k0 = (tl % tkn) * WT_T;
+    const int rs = tl / tkn;
+    for (int e = threadIdx.x; e < WT_T * WT_T; e += 256) {
+        const int kk = e / WT_T, cc = e % WT_T;
+        const int k = k0 + kk, c = c0 + cc;
+        tile[kk][cc] = (k < L.K && c < L.C) ? src[L.off + ((long)k * L.RS + rs) * L.C + c] : 0.f;
+    }
+    __syncthreads();
+    for (int e = threadIdx.x; e < WT_T * WT_T; e += 256) {
+        const int cc = e / WT_T, kk = e % WT_T;
+        const int k = k0 + kk, c = c0 + cc;
+        if (k < L.K && c < L.C)
+            dst[L.off + ((long)c * L.RS + rs) * L.K + k] = (uint16_t)bf16_bits(tile[kk][cc]);
+    }
+}
+
 // softmax cross-entropy: one workgroup per row
 __global__ void softmax_ce_kernel(const float* __restrict__ z, const int32_t* __restrict__ labels,
                                   int B, int K, float* __restrict__ row_loss,
@@ -879,6 +920,14 @@ hipError_t launch_cast_bf16(const float* src, uint16_t* dst, size_t n, hipStream
     const int vec = ((((uintptr_t)src) & 15) | (((uintptr_t)dst) & 7)) == 0;
     hipLaunchKernelGGL(cast_bf16_kernel, dim3(ew_blocks(vec ? (n + 3) / 4 : n)), dim3(EW_THREADS), 0,
                        s, src, dst, n, vec);
+    return hipGetLastError();
+}
+
+hipError_t launch_cast_bf16_t(const float* src, uint16_t* dst, const WtLayer* table,
+                              int nlayers, int tiles, hipStream_t s) {
+    if (nlayers <= 0 || tiles <= 0) return hipSuccess;
+    hipLaunchKernelGGL(cast_bf16_t_kernel, dim3(tiles), dim3(256), 0, s, src, dst, table,
+                       nlayers);
     return hipGetLastError();
 }
 

@@ -132,6 +132,11 @@ struct hp_stage {
     // bf16 mode with bf16 operands in memory: copies of the weights, of the
     // stage input and (scratch, one conv at a time) of a conv's output gradient
     uint16_t* w16 = nullptr;
+    // transposed copies [C][R][S][K] of the weights of the convs whose data
+    // gradient runs on k-major operands, and the device table that makes them
+    uint16_t* w16t = nullptr;
+    WtLayer* wt_table = nullptr;
+    int wt_layers = 0, wt_tiles_total = 0;
     uint16_t* x16 = nullptr;
     bool x16_ready = false;
     // the weight gradients run on a second stream beside the data-gradient
@@ -388,6 +393,25 @@ int build_stage(hp_stage* st, const hp_layer* layers, int n_layers) {
     if (any16) {
         int rc = dev_alloc16(st, &st->w16, st->P);
         if (rc) return rc;
+        std::vector<WtLayer> tab;
+        int tiles = 0;
+        for (int i = 0; i < n_layers; ++i) {
+            const Node& nd = st->nodes[i];
+            if ((nd.L.kind != HP_CONV && nd.L.kind != HP_FC) || !nd.dgrad.h16k) continue;
+            const ConvGeo& g = nd.geo;
+            tab.push_back(WtLayer{(long)nd.w_off, g.K, g.R * g.S, g.C, tiles});
+            tiles += wt_tiles(g.K, g.R * g.S, g.C);
+        }
+        if (!tab.empty()) {
+            if ((rc = dev_alloc16(st, &st->w16t, st->P))) return rc;
+            float* t = nullptr;
+            const size_t tb = tab.size() * sizeof(WtLayer);
+            if ((rc = dev_alloc(st, &t, (tb + 3) / 4))) return rc;
+            HP_HIP(hipMemcpy(t, tab.data(), tb, hipMemcpyHostToDevice));
+            st->wt_table = reinterpret_cast<WtLayer*>(t);
+            st->wt_layers = (int)tab.size();
+            st->wt_tiles_total = tiles;
+        }
     }
     int rc = dev_alloc(st, &st->ws2, std::max<size_t>(st->ws2_floats, 64));
     if (rc) return rc;
@@ -520,6 +544,9 @@ extern "C" int hp_stage_forward(hp_stage* st, const float* w, const float* x, fl
     if (st->w16) {
         st->timer.begin(1, s);
         hipError_t e = launch_cast_bf16(w, st->w16, st->P, s);
+        if (e == hipSuccess && st->w16t)
+            e = launch_cast_bf16_t(w, st->w16t, st->wt_table, st->wt_layers,
+                                   st->wt_tiles_total, s);
         st->timer.end(s);
         int rc = launch_ok(e, "weight cast", -1);
         if (rc) return rc;
@@ -709,7 +736,8 @@ extern "C" int hp_stage_backward(hp_stage* st, const float* w, const float* dy, 
                     }
                     tm.begin(0, s);
                     e = launch_gemm(nd.dgrad, nd.geo, gin, w + nd.w_off, d, dep, st->ws, s, g16,
-                                    g16 ? st->w16 + nd.w_off : nullptr);
+                                    g16 ? st->w16 + nd.w_off : nullptr,
+                                    g16 && st->w16t ? st->w16t + nd.w_off : nullptr);
                     tm.end(s);
                 }
                 break;

@@ -23,6 +23,8 @@
 // fan-in) are cut into chunks; each chunk writes a partial tile to a
 // workspace and a second kernel adds the partials in a fixed order, so results
 // are deterministic.
+#include <type_traits>
+
 #include "kernels.h"
 
 namespace hp {
@@ -38,19 +40,22 @@ namespace {
 constexpr int PAD_T = 2;
 constexpr int PAD_V = 4;
 
-// Tile configurations: workgroup tile BM x BN, reduction tile BK, wave tile
-// WM x WN (a grid of (WM/32) x (WN/32) MFMA 32x32 tiles per wave); the
-// workgroup has (BM/WM) * (BN/WN) waves.
-struct TileCfg { int bm, bn, bk, wm, wn; };
+// Tile configurations: workgroup tile BM x BN, reduction tile BK of the
+// kernels that stage from fp32 and BKH of the kernels on bf16 operands in
+// memory, wave tile WM x WN (a grid of (WM/32) x (WN/32) MFMA 32x32 tiles per
+// wave); the workgroup has (BM/WM) * (BN/WN) waves.  BKH = 64 halves the
+// barriers per MFMA; the 128x64 tile keeps 32, where the second register set
+// of a 64-wide k tile would cost it occupancy.
+struct TileCfg { int bm, bn, bk, wm, wn, bkh; };
 // Waves of 32x64 (eight in the general tile, four in the 128x64 and 64x128
 // ones) hide the staging latency better than fewer waves of 64x64, at the
 // cost of more LDS reads per MFMA.
 constexpr TileCfg kCfgs[] = {
-    {128, 128, 16, 32, 64},    // 0: general (8 waves)
-    {128, 64, 16, 32, 64},     // 1: narrow N (at most 64 output columns, 4 waves)
-    {64, 256, 16, 64, 64},     // 2: narrow M, N a multiple of 256 or large
-    {64, 128, 16, 32, 64},     // 3: narrow M otherwise (4 waves)
-    {64, 64, 16, 32, 32},      // 4: small M and N (4 waves of 32x32)
+    {128, 128, 16, 32, 64, 64},    // 0: general (8 waves)
+    {128, 64, 16, 32, 64, 32},     // 1: narrow N (at most 64 output columns, 4 waves)
+    {64, 256, 16, 64, 64, 32},     // 2: narrow M, N a multiple of 256 or large
+    {64, 128, 16, 32, 64, 64},     // 3: narrow M otherwise (4 waves)
+    {64, 64, 16, 32, 32, 64},      // 4: small M and N (4 waves of 32x32)
 };
 
 struct KArgs {
@@ -871,29 +876,41 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_bf16_kern
 
 // ---- bf16 kernel on bf16 operands -------------------------------------------
 // The bf16 contractions when both operands are already rounded to bf16 in
-// memory (a16 / b16): same LDS layout and MFMA loop as igemm_bf16_kernel, but
-// the staging moves bf16 bits straight to LDS.  k-major operands load 8
-// consecutive k (16 bytes) of a row and store them with one 16-byte LDS
-// write; m-major operands load 4 x 4 blocks (4 reduction rows of 4 columns, 8
-// bytes each) and transpose them in registers.  Used only when every
-// contiguous axis is a multiple of 8 elements and the operands are 16-byte
-// aligned, so there is no scalar path and no bias column.
-template <int OP, int BM, int BN, int WM, int WN>
+// memory (a16 / b16), on the same MFMA and the same LDS row layout as
+// igemm_bf16_kernel, with BKX k per tile (rows padded by 8 bf16, so 16-byte
+// fragment reads of 8 consecutive rows still cover all banks once).  k-major
+// operands load 8 consecutive k (16 bytes) of a row and store them with one
+// 16-byte LDS write; m-major operands load 4 x 4 blocks (4 reduction rows of
+// 4 columns, 8 bytes each) and transpose them in registers.
+//
+// Staging runs two tiles ahead: while the MFMAs consume tile kt from LDS,
+// the loads of tile kt+2 are in flight into one register set and tile kt+1,
+// loaded one step earlier into the other set, is written to the second LDS
+// buffer.  Every load is issued unconditionally (masked lanes read the
+// operand's first element) and the mask is applied when the registers are
+// written to LDS, so the wait before that write covers only the older loads.
+// Used only when every contiguous axis is a multiple of 8 elements and the
+// operands are 16-byte aligned, so there is no scalar path and no bias column.
+template <int OP, int BM, int BN, int WM, int WN, int BKX>
 __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_h16_kernel(KArgs args) {
     constexpr int NT = 64 * (BM / WM) * (BN / WN);
     constexpr int TM = WM / 32, TN = WN / 32;
+    constexpr int LDX = BKX + 8;
     constexpr bool A_KMAJ = (OP != OP_WGRAD);
     constexpr bool B_KMAJ = (OP == OP_FWD);
     constexpr int WAVES_N = BN / WN;
-    constexpr int KG = BKH / 8;                  // 8-k groups per k-major row
+    constexpr int KG = BKX / 8;                  // 8-k groups per k-major row
     constexpr int GA = BM * KG / NT;             // k-major groups per thread
     constexpr int GB = BN * KG / NT;
     constexpr int CGA = BM / 4, CGB = BN / 4;    // column groups of an m-major operand
-    constexpr int PA = (2 * BM + NT - 1) / NT;   // m-major 4x4 blocks per thread
-    constexpr int PB = (2 * BN + NT - 1) / NT;
-    static_assert(GA >= 1 && GB >= 1 && NT % KG == 0 && NT % CGA == 0 && NT % CGB == 0,
-                  "tile shape");
-    __shared__ __attribute__((aligned(16))) unsigned short smem[2 * (BM + BN) * LDH];
+    constexpr int NBA = (BKX / 4) * CGA;         // 4x4 blocks of an m-major tile
+    constexpr int NBB = (BKX / 4) * CGB;
+    constexpr int PA = (NBA + NT - 1) / NT;      // m-major blocks per thread
+    constexpr int PB = (NBB + NT - 1) / NT;
+    static_assert(BKX % 16 == 0 && GA >= 1 && GB >= 1 && NT % KG == 0 &&
+                  (BM * KG) % NT == 0 && (BN * KG) % NT == 0 && NT % CGA == 0 &&
+                  NT % CGB == 0, "tile shape");
+    __shared__ __attribute__((aligned(16))) unsigned short smem[2 * (BM + BN) * LDX];
 
     const ConvGeo& g = args.g;
     const int t = threadIdx.x;
@@ -902,10 +919,8 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_h16_kerne
     const int wm = (wave / WAVES_N) * WM;
     const int wn = (wave % WAVES_N) * WN;
     const Work wk = decode_work<BM, BN>(args);
-    const int ktiles = (int)((wk.kend - wk.kbeg + BKH - 1) / BKH);
+    const int ktiles = (int)((wk.kend - wk.kbeg + BKX - 1) / BKX);
     const int kg = (t % KG) * 8;
-    const bool a_act = A_KMAJ || 2 * BM >= NT || t < 2 * BM;
-    const bool b_act = B_KMAJ || 2 * BN >= NT || t < 2 * BN;
     const unsigned short* A = args.a16;
     const unsigned short* Bm = args.b16;
 
@@ -959,18 +974,22 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_h16_kerne
         }
     }
 
-    uintx4 areg_k[A_KMAJ ? GA : 1], breg_k[B_KMAJ ? GB : 1];
-    uintx2 areg_m[A_KMAJ ? 1 : 4 * PA], breg_m[B_KMAJ ? 1 : 4 * PB];
+    // two register sets of staged operands and their masks
+    uintx4 ra_k[2][A_KMAJ ? GA : 1], rb_k[2][B_KMAJ ? GB : 1];
+    uintx2 ra_m[2][A_KMAJ ? 1 : 4 * PA], rb_m[2][B_KMAJ ? 1 : 4 * PB];
+    bool ma_k[2][A_KMAJ ? GA : 1], mb_k[2][B_KMAJ ? GB : 1];
+    bool ma_m[2][A_KMAJ ? 1 : 4 * PA], mb_m[2][B_KMAJ ? 1 : 4 * PB];
 
-    auto ld16 = [](const unsigned short* p, bool ok) -> uintx4 {
-        return ok ? *reinterpret_cast<const uintx4*>(p) : uintx4{0u, 0u, 0u, 0u};
+    auto ld16 = [](const unsigned short* p) -> uintx4 {
+        return *reinterpret_cast<const uintx4*>(p);
     };
-    auto ld8 = [](const unsigned short* p, bool ok) -> uintx2 {
-        return ok ? *reinterpret_cast<const uintx2*>(p) : uintx2{0u, 0u};
+    auto ld8 = [](const unsigned short* p) -> uintx2 {
+        return *reinterpret_cast<const uintx2*>(p);
     };
 
-    auto gload = [&](int kt) {
-        const int k0 = (int)(wk.kbeg + (long)kt * BKH);
+    auto gload = [&](int kt, auto S) {
+        constexpr int s = decltype(S)::value;
+        const int k0 = (int)(wk.kbeg + (long)kt * BKX);
         const int kend_i = (int)wk.kend;
         if constexpr (OP == OP_FWD || OP == OP_DGRAD) {
             const int CC = (OP == OP_FWD) ? g.C : g.K;
@@ -1004,7 +1023,8 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_h16_kerne
                              q < g.Q;
                         off = arow_base[i] + ((long)p * g.Q + q) * g.K + c;
                     }
-                    areg_k[i] = ld16(A + (ok ? off : 0), ok);
+                    ra_k[s][i] = ld16(A + (ok ? off : 0));
+                    ma_k[s][i] = ok;
                 }
             }
             if constexpr (OP == OP_FWD) {
@@ -1012,56 +1032,60 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_h16_kerne
 #pragma unroll
                 for (int i = 0; i < GB; ++i) {
                     const bool ok = brow_ok[i] && kk < kend_i;
-                    breg_k[i] = ld16(Bm + (ok ? (brow_n[i] * args.Kred + kk) : 0), ok);
+                    rb_k[s][i] = ld16(Bm + (ok ? (brow_n[i] * args.Kred + kk) : 0));
+                    mb_k[s][i] = ok;
                 }
-            } else if (b_act) {     // B[kk = (r,s,k)][c] = w[k][r][s][c]
+            } else {                // B[kk = (r,s,k)][c] = w[k][r][s][c]
 #pragma unroll
                 for (int i = 0; i < PB; ++i) {
-                    const int kq = ((t + i * NT) / CGB) * 4;
+                    const int b = t + i * NT;
+                    const int kq = (b / CGB) * 4;
                     int k = c0 + kq, r = r0, sx = s0;
                     while (k >= CC) { k -= CC; if (++sx == g.S) { sx = 0; ++r; } }
 #pragma unroll
                     for (int jr = 0; jr < 4; ++jr) {
                         if (jr > 0 && ++k == CC) { k = 0; if (++sx == g.S) { sx = 0; ++r; } }
-                        const bool ok = bcol_ok && k0 + kq + jr < kend_i;
+                        const bool ok = b < NBB && bcol_ok && k0 + kq + jr < kend_i;
                         const long off = (((long)k * g.R + r) * g.S + sx) * g.C + bcol_c;
-                        breg_m[4 * i + jr] = ld8(Bm + (ok ? off : 0), ok);
+                        rb_m[s][4 * i + jr] = ld8(Bm + (ok ? off : 0));
+                        mb_m[s][4 * i + jr] = ok;
                     }
                 }
             }
         } else {
-            if (a_act) {            // A[kk][m] = dy[kk][m]
 #pragma unroll
-                for (int i = 0; i < PA; ++i) {
-                    const int kq = ((t + i * NT) / CGA) * 4;
+            for (int i = 0; i < PA; ++i) {  // A[kk][m] = dy[kk][m]
+                const int b = t + i * NT;
+                const int kq = (b / CGA) * 4;
 #pragma unroll
-                    for (int jr = 0; jr < 4; ++jr) {
-                        const int kk = k0 + kq + jr;
-                        const bool ok = kk < kend_i && acol < args.M;
-                        areg_m[4 * i + jr] = ld8(Bm + (ok ? (long)kk * g.K + acol : 0), ok);
-                    }
+                for (int jr = 0; jr < 4; ++jr) {
+                    const int kk = k0 + kq + jr;
+                    const bool ok = b < NBA && kk < kend_i && acol < args.M;
+                    ra_m[s][4 * i + jr] = ld8(Bm + (ok ? (long)kk * g.K + acol : 0));
+                    ma_m[s][4 * i + jr] = ok;
                 }
             }
-            if (b_act) {            // B[kk = (n,p,q)][j = (r,s,c)] = x[n, p*st-pad+r, q*st-pad+s, c]
-                const int q0 = k0 % g.Q;
-                const int t0 = k0 / g.Q;
-                const int p0 = t0 % g.P;
-                const int n0i = t0 / g.P;
+            // B[kk = (n,p,q)][j = (r,s,c)] = x[n, p*st-pad+r, q*st-pad+s, c]
+            const int q0 = k0 % g.Q;
+            const int t0 = k0 / g.Q;
+            const int p0 = t0 % g.P;
+            const int n0i = t0 / g.P;
 #pragma unroll
-                for (int i = 0; i < PB; ++i) {
-                    const int kq = ((t + i * NT) / CGB) * 4;
-                    int q = q0 + kq, p = p0, n = n0i;
-                    while (q >= g.Q) { q -= g.Q; if (++p == g.P) { p = 0; ++n; } }
+            for (int i = 0; i < PB; ++i) {
+                const int b = t + i * NT;
+                const int kq = (b / CGB) * 4;
+                int q = q0 + kq, p = p0, n = n0i;
+                while (q >= g.Q) { q -= g.Q; if (++p == g.P) { p = 0; ++n; } }
 #pragma unroll
-                    for (int jr = 0; jr < 4; ++jr) {
-                        if (jr > 0 && ++q == g.Q) { q = 0; if (++p == g.P) { p = 0; ++n; } }
-                        const int h = p * g.st - g.pad + bcol_r;
-                        const int w = q * g.st - g.pad + bcol_s;
-                        const bool ok = bcol_ok && k0 + kq + jr < kend_i &&
-                                        (unsigned)h < (unsigned)g.H && (unsigned)w < (unsigned)g.W;
-                        const long off = (((long)n * g.H + h) * g.W + w) * g.C + bcol_c;
-                        breg_m[4 * i + jr] = ld8(A + (ok ? off : 0), ok);
-                    }
+                for (int jr = 0; jr < 4; ++jr) {
+                    if (jr > 0 && ++q == g.Q) { q = 0; if (++p == g.P) { p = 0; ++n; } }
+                    const int h = p * g.st - g.pad + bcol_r;
+                    const int w = q * g.st - g.pad + bcol_s;
+                    const bool ok = b < NBB && bcol_ok && k0 + kq + jr < kend_i &&
+                                    (unsigned)h < (unsigned)g.H && (unsigned)w < (unsigned)g.W;
+                    const long off = (((long)n * g.H + h) * g.W + w) * g.C + bcol_c;
+                    rb_m[s][4 * i + jr] = ld8(A + (ok ? off : 0));
+                    mb_m[s][4 * i + jr] = ok;
                 }
             }
         }
@@ -1076,23 +1100,32 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_h16_kerne
         return uintx2{el(0) | (el(1) << 16), el(2) | (el(3) << 16)};
     };
 
-    auto sstore = [&](int buf) {
-        unsigned short* As = smem + buf * (BM + BN) * LDH;
-        unsigned short* Bs = As + BM * LDH;
+    auto sstore = [&](auto S) {
+        constexpr int s = decltype(S)::value;
+        unsigned short* As = smem + s * (BM + BN) * LDX;
+        unsigned short* Bs = As + BM * LDX;
+        const uintx4 z4{0u, 0u, 0u, 0u};
+        const uintx2 z2{0u, 0u};
         if constexpr (A_KMAJ) {
 #pragma unroll
             for (int i = 0; i < GA; ++i) {
                 const int row = t / KG + i * (NT / KG);
-                *reinterpret_cast<uintx4*>(As + row * LDH + kg) = areg_k[i];
+                *reinterpret_cast<uintx4*>(As + row * LDX + kg) = ma_k[s][i] ? ra_k[s][i] : z4;
             }
-        } else if (a_act) {
+        } else {
 #pragma unroll
             for (int i = 0; i < PA; ++i) {
-                const int kq = ((t + i * NT) / CGA) * 4;
+                const int b = t + i * NT;
+                if (b >= NBA) continue;
+                const int kq = (b / CGA) * 4;
+                uintx2 rows[4];
+#pragma unroll
+                for (int jr = 0; jr < 4; ++jr)
+                    rows[jr] = ma_m[s][4 * i + jr] ? ra_m[s][4 * i + jr] : z2;
 #pragma unroll
                 for (int c = 0; c < 4; ++c) {
                     const int col = (t % CGA) * 4 + c;
-                    *reinterpret_cast<uintx2*>(As + col * LDH + kq) = col_pairs(&areg_m[4 * i], c);
+                    *reinterpret_cast<uintx2*>(As + col * LDX + kq) = col_pairs(rows, c);
                 }
             }
         }
@@ -1100,16 +1133,22 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_h16_kerne
 #pragma unroll
             for (int i = 0; i < GB; ++i) {
                 const int row = t / KG + i * (NT / KG);
-                *reinterpret_cast<uintx4*>(Bs + row * LDH + kg) = breg_k[i];
+                *reinterpret_cast<uintx4*>(Bs + row * LDX + kg) = mb_k[s][i] ? rb_k[s][i] : z4;
             }
-        } else if (b_act) {
+        } else {
 #pragma unroll
             for (int i = 0; i < PB; ++i) {
-                const int kq = ((t + i * NT) / CGB) * 4;
+                const int b = t + i * NT;
+                if (b >= NBB) continue;
+                const int kq = (b / CGB) * 4;
+                uintx2 rows[4];
+#pragma unroll
+                for (int jr = 0; jr < 4; ++jr)
+                    rows[jr] = mb_m[s][4 * i + jr] ? rb_m[s][4 * i + jr] : z2;
 #pragma unroll
                 for (int c = 0; c < 4; ++c) {
                     const int col = (t % CGB) * 4 + c;
-                    *reinterpret_cast<uintx2*>(Bs + col * LDH + kq) = col_pairs(&breg_m[4 * i], c);
+                    *reinterpret_cast<uintx2*>(Bs + col * LDX + kq) = col_pairs(rows, c);
                 }
             }
         }
@@ -1123,29 +1162,30 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_h16_kerne
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
-    if (ktiles > 0) {
-        gload(0);
-        sstore(0);
-    }
-    __syncthreads();
     const int lr = lane & 31;
     const int lk = lane >> 5;
-    for (int kt = 0; kt < ktiles; ++kt) {
-        const int buf = kt & 1;
-        if (kt + 1 < ktiles) gload(kt + 1);
-        const unsigned short* As = smem + buf * (BM + BN) * LDH;
-        const unsigned short* Bs = As + BM * LDH;
+    // one k tile: prefetch tile kt+2 into register set s, multiply LDS buffer
+    // s, write tile kt+1 (register set s^1) to LDS buffer s^1.  The loads are
+    // unconditional (a tile past the end is all masked): with every load on
+    // one path the compiler's wait before the LDS write counts only the
+    // older set.
+    auto step = [&](int kt, auto S) {
+        constexpr int s = decltype(S)::value;
+        gload(kt + 2, S);
+        const unsigned short* As = smem + s * (BM + BN) * LDX;
+        const unsigned short* Bs = As + BM * LDX;
+        if (kt < ktiles) {
 #pragma unroll
-        for (int kk = 0; kk < BKH; kk += 16) {
+        for (int kk = 0; kk < BKX; kk += 16) {
             bf16x8 av[TM], bv[TN];
 #pragma unroll
             for (int i = 0; i < TM; ++i)
                 av[i] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uintx4*>(
-                                                       As + (wm + 32 * i + lr) * LDH + kk + 8 * lk));
+                                                       As + (wm + 32 * i + lr) * LDX + kk + 8 * lk));
 #pragma unroll
             for (int j = 0; j < TN; ++j)
                 bv[j] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uintx4*>(
-                                                       Bs + (wn + 32 * j + lr) * LDH + kk + 8 * lk));
+                                                       Bs + (wn + 32 * j + lr) * LDX + kk + 8 * lk));
 #pragma unroll
             for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -1153,11 +1193,209 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_h16_kerne
                     acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[i], bv[j], acc[i][j], 0,
                                                                          0, 0);
         }
-        if (kt + 1 < ktiles) sstore(buf ^ 1);
+        }
+        if (kt + 1 < ktiles) sstore(std::integral_constant<int, s ^ 1>{});
         __syncthreads();
+    };
+
+    const std::integral_constant<int, 0> I0{};
+    const std::integral_constant<int, 1> I1{};
+    gload(0, I0);
+    gload(1, I1);
+    if (ktiles > 0) sstore(I0);
+    __syncthreads();
+    for (int kt = 0; kt < ktiles; kt += 2) {
+        step(kt, I0);
+        step(kt + 1, I1);
     }
     store_tile<BM, BN, TM, TN>(args, wk, acc, wm, wn, lane);
 }
+
+// ---- bf16 kernel on k-major bf16 operands -------------------------------------
+// Forward and stride-1 data-gradient contractions whose reduction channel
+// count (C forward, K data gradient) is a multiple of the k tile, so that one
+// k tile is one kernel tap (r, s) and BKX consecutive channels.  Both operands
+// are k-major: A rows are gathered pixels (the implicit im2col of x; for the
+// data gradient, of dy, where the tap enters with the opposite sign), B rows
+// are weight rows (w [K][R][S][C] forward, its transposed copy [C][R][S][K]
+// for the data gradient).  Operands are read with buffer loads, whose range
+// check returns zeros for an offset past the end of the buffer: a lane whose
+// pixel lies in the padding, or whose row lies past the matrix, gets such an
+// offset, so staging needs no masks and a row's byte offset changes per tile
+// only by the tap term.  Same LDS layout, MFMA loop and two-tile-deep staging
+// as igemm_h16_kernel.
+constexpr unsigned BUF_OOB = 0x80000000u;      // buffer offset past any operand here
+constexpr int BUF_CFG = 0x00020000;            // buffer descriptor word 3 (gfx9 family)
+
+__device__ __forceinline__ uintx4 buf_load16(__amdgpu_buffer_rsrc_t rs, unsigned voff,
+                                             unsigned soff) {
+    return __builtin_amdgcn_raw_buffer_load_b128(rs, (int)voff, (int)soff, 0);
+}
+
+template <int OP, int BM, int BN, int WM, int WN, int BKX>
+__global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_h16k_kernel(KArgs args) {
+    static_assert(OP == OP_FWD || OP == OP_DGRAD, "k-major operands");
+    constexpr int NT = 64 * (BM / WM) * (BN / WN);
+    constexpr int TM = WM / 32, TN = WN / 32;
+    constexpr int LDX = BKX + 8;
+    constexpr int WAVES_N = BN / WN;
+    constexpr int KG = BKX / 8;                  // 8-k groups per row
+    constexpr int GA = BM * KG / NT;             // A groups per thread
+    constexpr int GB = BN * KG / NT;
+    static_assert(BKX % 16 == 0 && GA >= 1 && GB >= 1 && NT % KG == 0 &&
+                  (BM * KG) % NT == 0 && (BN * KG) % NT == 0, "tile shape");
+    __shared__ __attribute__((aligned(16))) unsigned short smem[2 * (BM + BN) * LDX];
+
+    const ConvGeo& g = args.g;
+    const int t = threadIdx.x;
+    const int lane = t & 63;
+    const int wave = t >> 6;
+    const int wm = (wave / WAVES_N) * WM;
+    const int wn = (wave % WAVES_N) * WN;
+    const Work wk = decode_work<BM, BN>(args);
+    const int ktiles = (int)((wk.kend - wk.kbeg) / BKX);   // whole tiles by construction
+    const int kg = (t % KG) * 8;
+    // image and channel count of the gathered operand
+    const int IH = (OP == OP_FWD) ? g.H : g.P;
+    const int IW = (OP == OP_FWD) ? g.W : g.Q;
+    const int CC = (OP == OP_FWD) ? g.C : g.K;
+    const unsigned a_bytes = (unsigned)((long)g.N * IH * IW * CC * 2);
+    const unsigned b_bytes = (unsigned)(args.Ncols * args.Kred * 2);
+    const __amdgpu_buffer_rsrc_t rsA = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<unsigned short*>(args.a16), (short)0, (int)a_bytes, BUF_CFG);
+    const __amdgpu_buffer_rsrc_t rsB = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<unsigned short*>(args.b16), (short)0, (int)b_bytes, BUF_CFG);
+
+    // A row i: pixel of tap (0, 0) and its element offset (channel kg)
+    int a_h[GA], a_w[GA], a_off[GA];
+    bool a_ok[GA];
+#pragma unroll
+    for (int i = 0; i < GA; ++i) {
+        const long m = wk.m0 + t / KG + i * (NT / KG);
+        a_ok[i] = m < args.M;
+        const long mm = a_ok[i] ? m : 0;
+        int n, h0, w0;
+        if constexpr (OP == OP_FWD) {
+            const int q = (int)(mm % g.Q); const long tt = mm / g.Q;
+            const int p = (int)(tt % g.P); n = (int)(tt / g.P);
+            h0 = p * g.st - g.pad;
+            w0 = q * g.st - g.pad;
+        } else {
+            const int w = (int)(mm % g.W); const long tt = mm / g.W;
+            const int h = (int)(tt % g.H); n = (int)(tt / g.H);
+            h0 = h + g.pad;
+            w0 = w + g.pad;
+        }
+        a_h[i] = h0;
+        a_w[i] = w0;
+        a_off[i] = ((n * IH + h0) * IW + w0) * CC + kg;
+    }
+    // B row i: byte offset of its first k (the tile's k enters as soffset)
+    unsigned b_off[GB];
+#pragma unroll
+    for (int i = 0; i < GB; ++i) {
+        const long n = wk.n0 + t / KG + i * (NT / KG);
+        b_off[i] = n < args.Ncols ? (unsigned)((n * args.Kred + kg) * 2) : BUF_OOB;
+    }
+
+    uintx4 ra[2][GA], rb[2][GB];
+    // tap (tr, ts), channel base tc and reduction index of the next tile to load
+    int kload = (int)wk.kbeg;
+    int tc = kload % CC;
+    int tr, ts;
+    {
+        const int rs = kload / CC;
+        tr = rs / g.S;
+        ts = rs - tr * g.S;
+    }
+
+    // Loads of tiles past the end are harmless: every offset is range-checked
+    // and such a tile is never written to LDS.
+    auto gload = [&](auto S) {
+        constexpr int s = decltype(S)::value;
+        const int dr = (OP == OP_FWD) ? tr : -tr;
+        const int ds = (OP == OP_FWD) ? ts : -ts;
+        const int sk = (dr * IW + ds) * CC + tc;
+#pragma unroll
+        for (int i = 0; i < GA; ++i) {
+            const int h = a_h[i] + dr, w = a_w[i] + ds;
+            const bool ok = a_ok[i] && (unsigned)h < (unsigned)IH && (unsigned)w < (unsigned)IW;
+            ra[s][i] = buf_load16(rsA, ok ? (unsigned)(a_off[i] + sk) * 2u : BUF_OOB, 0u);
+        }
+#pragma unroll
+        for (int i = 0; i < GB; ++i) rb[s][i] = buf_load16(rsB, b_off[i], (unsigned)kload * 2u);
+        kload += BKX;
+        tc += BKX;
+        if (tc == CC) {
+            tc = 0;
+            if (++ts == g.S) { ts = 0; ++tr; }
+        }
+    };
+
+    auto sstore = [&](auto S) {
+        constexpr int s = decltype(S)::value;
+        unsigned short* As = smem + s * (BM + BN) * LDX;
+        unsigned short* Bs = As + BM * LDX;
+#pragma unroll
+        for (int i = 0; i < GA; ++i)
+            *reinterpret_cast<uintx4*>(As + (t / KG + i * (NT / KG)) * LDX + kg) = ra[s][i];
+#pragma unroll
+        for (int i = 0; i < GB; ++i)
+            *reinterpret_cast<uintx4*>(Bs + (t / KG + i * (NT / KG)) * LDX + kg) = rb[s][i];
+    };
+
+    floatx16 acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+
+    const int lr = lane & 31;
+    const int lk = lane >> 5;
+    auto step = [&](int kt, auto S) {
+        constexpr int s = decltype(S)::value;
+        gload(S);                                  // tile kt + 2
+        const unsigned short* As = smem + s * (BM + BN) * LDX;
+        const unsigned short* Bs = As + BM * LDX;
+        if (kt < ktiles) {
+#pragma unroll
+            for (int kk = 0; kk < BKX; kk += 16) {
+                bf16x8 av[TM], bv[TN];
+#pragma unroll
+                for (int i = 0; i < TM; ++i)
+                    av[i] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uintx4*>(
+                                                           As + (wm + 32 * i + lr) * LDX + kk + 8 * lk));
+#pragma unroll
+                for (int j = 0; j < TN; ++j)
+                    bv[j] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const uintx4*>(
+                                                           Bs + (wn + 32 * j + lr) * LDX + kk + 8 * lk));
+#pragma unroll
+                for (int i = 0; i < TM; ++i)
+#pragma unroll
+                    for (int j = 0; j < TN; ++j)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[i], bv[j],
+                                                                             acc[i][j], 0, 0, 0);
+            }
+        }
+        if (kt + 1 < ktiles) sstore(std::integral_constant<int, s ^ 1>{});
+        __syncthreads();
+    };
+
+    const std::integral_constant<int, 0> I0{};
+    const std::integral_constant<int, 1> I1{};
+    gload(I0);
+    gload(I1);
+    if (ktiles > 0) sstore(I0);
+    __syncthreads();
+    for (int kt = 0; kt < ktiles; kt += 2) {
+        step(kt, I0);
+        step(kt + 1, I1);
+    }
+    store_tile<BM, BN, TM, TN>(args, wk, acc, wm, wn, lane);
+}
+
 
 
 // Reduction of the cut tiles: workgroup = 64 elements of one tile x 16 split
@@ -1256,46 +1494,57 @@ struct KernelRef {
     int nt;
 };
 
-template <int OP, int CFG, int VW, bool BF>
+// Kernel families: fp32 operands staged from fp32 (vector width 1 or 4),
+// bf16 rounded while staging from fp32 (1 or 4), bf16 operands in memory
+// (general gather), bf16 operands in memory, both k-major (FWD and stride-1
+// DGRAD with a reduction channel count that is a multiple of the k tile).
+enum { KF_F32_1, KF_F32_4, KF_BF_1, KF_BF_4, KF_H16, KF_H16K };
+
+template <int OP, int CFG, int KF>
 KernelRef kref() {
     constexpr TileCfg c = kCfgs[CFG];
     constexpr int nt = 64 * (c.bm / c.wm) * (c.bn / c.wn);
-    if constexpr (VW == 8)
-        return {reinterpret_cast<const void*>(&igemm_h16_kernel<OP, c.bm, c.bn, c.wm, c.wn>), nt};
-    else if constexpr (BF)
-        return {reinterpret_cast<const void*>(&igemm_bf16_kernel<OP, c.bm, c.bn, c.wm, c.wn, VW>),
-                nt};
+    if constexpr (KF == KF_H16K && OP != OP_WGRAD)
+        return {reinterpret_cast<const void*>(
+                    &igemm_h16k_kernel<OP, c.bm, c.bn, c.wm, c.wn, c.bkh>), nt};
+    else if constexpr (KF == KF_H16 || KF == KF_H16K)
+        return {reinterpret_cast<const void*>(
+                    &igemm_h16_kernel<OP, c.bm, c.bn, c.wm, c.wn, c.bkh>), nt};
+    else if constexpr (KF == KF_BF_1 || KF == KF_BF_4)
+        return {reinterpret_cast<const void*>(
+                    &igemm_bf16_kernel<OP, c.bm, c.bn, c.wm, c.wn, KF == KF_BF_4 ? 4 : 1>), nt};
     else
-        return {reinterpret_cast<const void*>(&igemm_kernel<OP, c.bm, c.bn, c.bk, c.wm, c.wn, VW>),
-                nt};
+        return {reinterpret_cast<const void*>(
+                    &igemm_kernel<OP, c.bm, c.bn, c.bk, c.wm, c.wn, KF == KF_F32_4 ? 4 : 1>), nt};
 }
 
-// Every configuration is instantiated with vector width 4 (channel counts
-// divisible by 4, aligned operands) and 1 (everything else); bf16 also with
-// bf16 operands in memory ("vector width" 8).
-template <int OP, int VW, bool BF>
+template <int OP, int KF>
 KernelRef kref_cfg(int cfg) {
     switch (cfg) {
-        case 1: return kref<OP, 1, VW, BF>();
-        case 2: return kref<OP, 2, VW, BF>();
-        case 3: return kref<OP, 3, VW, BF>();
-        case 4: return kref<OP, 4, VW, BF>();
-        default: return kref<OP, 0, VW, BF>();
+        case 1: return kref<OP, 1, KF>();
+        case 2: return kref<OP, 2, KF>();
+        case 3: return kref<OP, 3, KF>();
+        case 4: return kref<OP, 4, KF>();
+        default: return kref<OP, 0, KF>();
     }
 }
 
-// vw: 1, 4, or 8 (bf16 only: operands already bf16 in memory)
 template <int OP>
-KernelRef kref_op(int cfg, int vw, bool bf) {
-    if (bf && vw == 8) return kref_cfg<OP, 8, true>(cfg);
-    if (vw == 4) return bf ? kref_cfg<OP, 4, true>(cfg) : kref_cfg<OP, 4, false>(cfg);
-    return bf ? kref_cfg<OP, 1, true>(cfg) : kref_cfg<OP, 1, false>(cfg);
+KernelRef kref_op(int cfg, int kf) {
+    switch (kf) {
+        case KF_F32_4: return kref_cfg<OP, KF_F32_4>(cfg);
+        case KF_BF_1: return kref_cfg<OP, KF_BF_1>(cfg);
+        case KF_BF_4: return kref_cfg<OP, KF_BF_4>(cfg);
+        case KF_H16: return kref_cfg<OP, KF_H16>(cfg);
+        case KF_H16K: return kref_cfg<OP, KF_H16K>(cfg);
+        default: return kref_cfg<OP, KF_F32_1>(cfg);
+    }
 }
 
-KernelRef kernel_for(int op, int cfg, int vw, bool bf) {
-    if (op == OP_FWD) return kref_op<OP_FWD>(cfg, vw, bf);
-    if (op == OP_DGRAD) return kref_op<OP_DGRAD>(cfg, vw, bf);
-    return kref_op<OP_WGRAD>(cfg, vw, bf);
+KernelRef kernel_for(int op, int cfg, int kf) {
+    if (op == OP_FWD) return kref_op<OP_FWD>(cfg, kf);
+    if (op == OP_DGRAD) return kref_op<OP_DGRAD>(cfg, kf);
+    return kref_op<OP_WGRAD>(cfg, kf);
 }
 
 // Tile configuration for a contraction of M x N (x Kred): the 128x128 tile
@@ -1344,10 +1593,22 @@ GemmPlan plan_gemm(int op, const ConvGeo& g, int bf16, int num_cus, int bias_col
     }
     const TileCfg& c = kCfgs[p.cfg];
     const long tiles = ((p.M + c.bm - 1) / c.bm) * ((p.Ncols + c.bn - 1) / c.bn);
-    const int bk = bf16 ? BKH : c.bk;
+    const int bk = p.h16 ? c.bkh : (bf16 ? BKH : c.bk);
     const long ktiles = (p.Kred + bk - 1) / bk;
+    // both operands k-major: one tap per k tile, 32-bit buffer offsets
+    if (p.h16 && (op == OP_FWD || (op == OP_DGRAD && g.st == 1))) {
+        const long cc = (op == OP_FWD) ? g.C : g.K;
+        const long a_el = (op == OP_FWD) ? (long)g.N * g.H * g.W * g.C
+                                         : (long)g.N * g.P * g.Q * g.K;
+        const long lim = (1L << 30) - (1L << 20);     // elements of a bf16 operand (< 2 GB)
+        p.h16k = (cc % bk == 0 && a_el < lim && p.Ncols * p.Kred < lim) ? 1 : 0;
+    }
     // workgroups resident at once
-    KernelRef kr = kernel_for(op, p.cfg, p.h16 ? 8 : (v4 ? 4 : 1), bf16 != 0);
+    KernelRef kr = kernel_for(op, p.cfg,
+                              p.h16k ? KF_H16K
+                                     : p.h16 ? KF_H16
+                                             : bf16 ? (v4 ? KF_BF_4 : KF_BF_1)
+                                                    : (v4 ? KF_F32_4 : KF_F32_1));
     int occ = 0;
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, kr.fn, kr.nt, 0) != hipSuccess || occ < 1)
         occ = 1;
@@ -1384,7 +1645,7 @@ GemmPlan plan_gemm(int op, const ConvGeo& g, int bf16, int num_cus, int bias_col
 
 hipError_t launch_gemm(const GemmPlan& plan, const ConvGeo& g, const float* a, const float* b,
                        float* out, const Epilogue& ep, float* ws, hipStream_t s,
-                       const uint16_t* a16, const uint16_t* b16) {
+                       const uint16_t* a16, const uint16_t* b16, const uint16_t* b16t) {
     KArgs k{};
     k.g = g;
     k.a = a;
@@ -1410,9 +1671,16 @@ hipError_t launch_gemm(const GemmPlan& plan, const ConvGeo& g, const float* a, c
     // operand bases 16-byte aligned
     bool v4 = (plan.op == OP_FWD) ? (g.C % 4 == 0) : (g.C % 4 == 0 && g.K % 4 == 0);
     v4 = v4 && ((((uintptr_t)a) | ((uintptr_t)b)) & 15) == 0;
-    const bool h16 = plan.h16 && plan.bf16 && !plan.bias_col && a16 && b16 &&
+    // DGRAD on k-major operands takes the transposed weights b16t
+    const uint16_t* bk16 = plan.op == OP_DGRAD ? b16t : b16;
+    const bool h16k = plan.h16k && a16 && bk16 && ((((uintptr_t)a16) | ((uintptr_t)bk16)) & 15) == 0;
+    const bool h16 = !h16k && plan.h16 && plan.bf16 && !plan.bias_col && a16 && b16 &&
                      ((((uintptr_t)a16) | ((uintptr_t)b16)) & 15) == 0;
-    KernelRef kr = kernel_for(plan.op, plan.cfg, h16 ? 8 : (v4 ? 4 : 1), plan.bf16 != 0);
+    if (h16k) k.b16 = bk16;
+    const int kf = h16k ? KF_H16K
+                        : h16 ? KF_H16
+                              : plan.bf16 ? (v4 ? KF_BF_4 : KF_BF_1) : (v4 ? KF_F32_4 : KF_F32_1);
+    KernelRef kr = kernel_for(plan.op, plan.cfg, kf);
     void* kargs[] = {&k};
     hipError_t e = hipLaunchKernel(kr.fn, dim3(plan.nwg), dim3(kr.nt), kargs, 0, s);
     const int cut = k.tiles_m * k.tiles_n - plan.tfull;

@@ -25,6 +25,7 @@ struct GemmPlan {
     int op;
     int bf16;          // round operands to bf16 (RNE) when staging
     int h16;           // bf16: the geometry allows bf16 operands in memory (launch_gemm a16/b16)
+    int h16k;          // h16 and both operands k-major (FWD; DGRAD with stride 1 and b16t)
     int bias_col;      // OP_WGRAD: Ncols includes the bias-gradient column
     int cfg;           // tile configuration
     int tfull;         // tiles computed whole (one workgroup each)
@@ -58,13 +59,30 @@ struct Epilogue {
 
 // a16 / b16 (bf16 plans with plan.h16, optional): the same operands already
 // rounded to bf16, 16-byte aligned; when given, the kernel stages them directly.
+// b16t (OP_DGRAD, optional): the weights transposed to [C][R][S][K] in bf16;
+// with it a plan with h16k runs on k-major operands.
 hipError_t launch_gemm(const GemmPlan& plan, const ConvGeo& g, const float* a,
                        const float* b, float* out, const Epilogue& ep, float* ws,
                        hipStream_t s, const uint16_t* a16 = nullptr,
-                       const uint16_t* b16 = nullptr);
+                       const uint16_t* b16 = nullptr, const uint16_t* b16t = nullptr);
 
 // dst[i] = bf16(src[i]) (round to nearest even), n elements
 hipError_t launch_cast_bf16(const float* src, uint16_t* dst, size_t n, hipStream_t s);
+
+// Transposed bf16 weight copies for the data gradient on k-major operands:
+// for each table layer, dst[off + (c*RS + rs)*K + k] = bf16(src[off + (k*RS + rs)*C + c]).
+// tile0 = the layer's first WT_TILE x WT_TILE tile number (prefix sums of wt_tiles, in
+// table order); `tiles` = the total.  The table lives in device memory.
+struct WtLayer {
+    long off;
+    int K, RS, C, tile0;
+};
+constexpr int WT_TILE = 64;
+inline int wt_tiles(int K, int RS, int C) {
+    return RS * ((K + WT_TILE - 1) / WT_TILE) * ((C + WT_TILE - 1) / WT_TILE);
+}
+hipError_t launch_cast_bf16_t(const float* src, uint16_t* dst, const WtLayer* table,
+                              int nlayers, int tiles, hipStream_t s);
 
 // ---- element-wise / reduction kernels (elementwise.hip) -------------------
 // y = max(x, 0)

@@ -29,6 +29,12 @@ def test_library_exports_every_declared_symbol():
     assert sorted(hetpipe.EXPORTS) == declared_functions()
 
 
+def test_library_resolves_every_symbol_at_load():
+    # immediate binding: a reference the library makes but does not define
+    # fails here instead of at its first call on a GPU
+    ctypes.CDLL(hetpipe.LIB_PATH, mode=os.RTLD_NOW | os.RTLD_LOCAL)
+
+
 def test_layer_struct_matches_header():
     # 10 int32 fields and one float: 44 bytes, no padding
     assert ctypes.sizeof(hetpipe.hp_layer) == 44

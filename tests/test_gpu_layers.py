@@ -24,6 +24,11 @@ CONV = [
     (4, 20, 18, 64, 136, 3, 1, 1, True),   # several 128x128 tiles, ragged N
     (2, 30, 30, 32, 64, 3, 1, 1, True),    # 256x64 tile configuration
     (16, 4, 4, 256, 40, 3, 1, 1, False),   # long reduction, split-K in wgrad
+    # bf16 on k-major operands (reduction channels a multiple of the k tile)
+    (2, 15, 13, 64, 72, 3, 2, 1, False),   # strided, padded forward
+    (2, 11, 9, 72, 128, 3, 1, 1, False),   # data gradient, 3x3 taps, ragged N
+    (3, 7, 7, 64, 64, 1, 1, 0, False),     # 1x1 both ways, ragged M
+    (8, 14, 14, 256, 256, 3, 1, 1, False), # split reduction both ways
 ]
 
 
