@@ -75,6 +75,10 @@ struct KArgs {
     int epi;
     const unsigned short* a16;   // bf16 copies of a and b (16-bit operand kernel only)
     const unsigned short* b16;
+    // weight gradient on bf16 operands: floor(i / Q) = (i * mq) >> sq and
+    // floor(i / P) = (i * mp) >> sp for 0 <= i < 2^31
+    unsigned mq, mp;
+    int sq, sp;
 };
 
 // Destination of output element (row, col): the bias-gradient column of a
@@ -1397,6 +1401,182 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_h16k_kern
 }
 
 
+// ---- bf16 weight-gradient kernel on m-major LDS tiles --------------------------
+// out[k][(r,s,c)] = sum over output pixels (n,p,q) of dy[(n,p,q)][k] *
+// x[n, p*st-pad+r, q*st-pad+s, c].  Both operands have the reduction index
+// (the pixel) as their memory row, so both are staged m-major: a k tile is
+// BKX pixel rows of BM output channels of dy and BN im2col columns of x, each
+// row segment copied with 16-byte buffer loads as it lies in memory (8
+// consecutive channels; C % 8 == 0 keeps them within one tap).  The MFMA
+// operand of a lane (8 consecutive k of one row) is read with two LDS
+// transpose reads (ds_read_b64_tr_b16): in every group of 16 lanes, lane i
+// receives element i mod 4 of the 8 bytes read by lane 4e + i/4 as its value
+// e, so when source lane S reads k row k0 + S/4 at columns m0 + 4 (S mod 4),
+// lane i holds k0..k0+3 of column m0 + i.  Rows are padded by 16 elements,
+// which puts the four rows a 16-lane group reads in disjoint banks.  The
+// output pixel of a k row is divided into (n, p, q) by multiply-high with
+// constants computed on the host.
+template <int BM, int BN, int WM, int WN, int BKX>
+__global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_h16w_kernel(KArgs args) {
+    constexpr int NT = 64 * (BM / WM) * (BN / WN);
+    constexpr int TM = WM / 32, TN = WN / 32;
+    constexpr int PA = BM + 16, PB = BN + 16;    // LDS row pitch (bf16)
+    constexpr int WAVES_N = BN / WN;
+    constexpr int CGA = BM / 8, CGB = BN / 8;    // 16-byte groups per row
+    constexpr int LA = BKX * CGA / NT;           // loads per thread per tile
+    constexpr int LB = BKX * CGB / NT;
+    static_assert(BKX % 16 == 0 && LA >= 1 && LB >= 1 && (BKX * CGA) % NT == 0 &&
+                  (BKX * CGB) % NT == 0 && NT % CGA == 0 && NT % CGB == 0, "tile shape");
+    __shared__ __attribute__((aligned(16))) unsigned short smem[2 * BKX * (PA + PB)];
+
+    const ConvGeo& g = args.g;
+    const int t = threadIdx.x;
+    const int lane = t & 63;
+    const int wave = t >> 6;
+    const int wm = (wave / WAVES_N) * WM;
+    const int wn = (wave % WAVES_N) * WN;
+    const Work wk = decode_work<BM, BN>(args);
+    const int ktiles = (int)((wk.kend - wk.kbeg + BKX - 1) / BKX);
+    const int kend = (int)wk.kend;
+    const unsigned x_bytes = (unsigned)((long)g.N * g.H * g.W * g.C * 2);
+    const unsigned dy_bytes = (unsigned)((long)g.N * g.P * g.Q * g.K * 2);
+    const __amdgpu_buffer_rsrc_t rsX = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<unsigned short*>(args.a16), (short)0, (int)x_bytes, BUF_CFG);
+    const __amdgpu_buffer_rsrc_t rsD = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<unsigned short*>(args.b16), (short)0, (int)dy_bytes, BUF_CFG);
+
+    // dy: this thread's column group and row of each load
+    const int acol = (t % CGA) * 8;
+    const bool acol_ok = wk.m0 + acol < args.M;
+    const unsigned a_voff = (unsigned)(wk.m0 + acol) * 2u;
+    int arow[LA];
+#pragma unroll
+    for (int i = 0; i < LA; ++i) arow[i] = (t + i * NT) / CGA;
+    // x: this thread's column group = one tap (r, s) and 8 channels from c
+    const int bcol = (t % CGB) * 8;
+    const long jb = wk.n0 + bcol;
+    const bool bcol_ok = jb < args.Ncols;
+    int bc, br, bs;
+    {
+        const long jj = bcol_ok ? jb : 0;
+        bc = (int)(jj % g.C);
+        const int rs = (int)(jj / g.C);
+        br = rs / g.S;
+        bs = rs - br * g.S;
+    }
+    int brow[LB];
+#pragma unroll
+    for (int i = 0; i < LB; ++i) brow[i] = (t + i * NT) / CGB;
+
+    uintx4 ra[2][LA], rb[2][LB];
+
+    // loads of tile kt (rows past kend, including whole tiles past the end,
+    // read zeros through the range check)
+    auto gload = [&](int kt, auto S) {
+        constexpr int s = decltype(S)::value;
+        const int k0 = (int)wk.kbeg + kt * BKX;
+#pragma unroll
+        for (int i = 0; i < LA; ++i) {
+            const int pix = k0 + arow[i];
+            const bool ok = acol_ok && pix < kend;
+            ra[s][i] = buf_load16(rsD, ok ? (unsigned)pix * (unsigned)(g.K * 2) + a_voff : BUF_OOB, 0u);
+        }
+#pragma unroll
+        for (int i = 0; i < LB; ++i) {
+            const unsigned pix = (unsigned)(k0 + brow[i]);
+            const unsigned t2 = (unsigned)(((unsigned long long)pix * args.mq) >> args.sq);
+            const int q = (int)(pix - t2 * (unsigned)g.Q);
+            const unsigned n = (unsigned)(((unsigned long long)t2 * args.mp) >> args.sp);
+            const int p = (int)(t2 - n * (unsigned)g.P);
+            const int h = p * g.st - g.pad + br;
+            const int w = q * g.st - g.pad + bs;
+            const bool ok = bcol_ok && (int)pix < kend && (unsigned)h < (unsigned)g.H &&
+                            (unsigned)w < (unsigned)g.W;
+            const int off = (((int)n * g.H + h) * g.W + w) * g.C + bc;
+            rb[s][i] = buf_load16(rsX, ok ? (unsigned)off * 2u : BUF_OOB, 0u);
+        }
+    };
+
+    auto sstore = [&](auto S) {
+        constexpr int s = decltype(S)::value;
+        unsigned short* As = smem + s * BKX * (PA + PB);
+        unsigned short* Bs = As + BKX * PA;
+#pragma unroll
+        for (int i = 0; i < LA; ++i)
+            *reinterpret_cast<uintx4*>(As + arow[i] * PA + acol) = ra[s][i];
+#pragma unroll
+        for (int i = 0; i < LB; ++i)
+            *reinterpret_cast<uintx4*>(Bs + brow[i] * PB + bcol) = rb[s][i];
+    };
+
+    floatx16 acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+
+    // transpose-read addressing: source lane S = lane % 16 of group gq = lane / 16
+    // reads k row 8 (gq / 2) + S / 4 (+4 for the second half) at column
+    // 16 (gq % 2) + 4 (S % 4) of a 32-column fragment
+    const int gq = lane >> 4, sl = lane & 15;
+    const int tr_row = 8 * (gq >> 1) + (sl >> 2);
+    const int tr_col = 16 * (gq & 1) + 4 * (sl & 3);
+    typedef short v4s __attribute__((ext_vector_type(4)));
+    auto tr_read = [](const unsigned short* p) -> v4s {
+        return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (__attribute__((address_space(3))) v4s*)(
+                (__attribute__((address_space(3))) unsigned short*)(p)));
+    };
+    auto frag = [&](const unsigned short* base, int pitch, int kk, int col) -> bf16x8 {
+        const unsigned short* p = base + (kk + tr_row) * pitch + col + tr_col;
+        const v4s lo = tr_read(p);
+        const v4s hi = tr_read(p + 4 * pitch);
+        typedef short v8s __attribute__((ext_vector_type(8)));
+        const v8s v = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+        return __builtin_bit_cast(bf16x8, v);
+    };
+
+    auto step = [&](int kt, auto S) {
+        constexpr int s = decltype(S)::value;
+        gload(kt + 2, S);
+        const unsigned short* As = smem + s * BKX * (PA + PB);
+        const unsigned short* Bs = As + BKX * PA;
+        if (kt < ktiles) {
+#pragma unroll
+            for (int kk = 0; kk < BKX; kk += 16) {
+                bf16x8 av[TM], bv[TN];
+#pragma unroll
+                for (int i = 0; i < TM; ++i) av[i] = frag(As, PA, kk, wm + 32 * i);
+#pragma unroll
+                for (int j = 0; j < TN; ++j) bv[j] = frag(Bs, PB, kk, wn + 32 * j);
+#pragma unroll
+                for (int i = 0; i < TM; ++i)
+#pragma unroll
+                    for (int j = 0; j < TN; ++j)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[i], bv[j],
+                                                                             acc[i][j], 0, 0, 0);
+            }
+        }
+        if (kt + 1 < ktiles) sstore(std::integral_constant<int, s ^ 1>{});
+        __syncthreads();
+    };
+
+    const std::integral_constant<int, 0> I0{};
+    const std::integral_constant<int, 1> I1{};
+    gload(0, I0);
+    gload(1, I1);
+    if (ktiles > 0) sstore(I0);
+    __syncthreads();
+    for (int kt = 0; kt < ktiles; kt += 2) {
+        step(kt, I0);
+        step(kt + 1, I1);
+    }
+    store_tile<BM, BN, TM, TN>(args, wk, acc, wm, wn, lane);
+}
+
+
 
 // Reduction of the cut tiles: workgroup = 64 elements of one tile x 16 split
 // lanes; lane l adds splits l, l+16, ... (eight loads in flight at a time,
@@ -1507,6 +1687,9 @@ KernelRef kref() {
     if constexpr (KF == KF_H16K && OP != OP_WGRAD)
         return {reinterpret_cast<const void*>(
                     &igemm_h16k_kernel<OP, c.bm, c.bn, c.wm, c.wn, c.bkh>), nt};
+    else if constexpr (KF == KF_H16K)
+        return {reinterpret_cast<const void*>(
+                    &igemm_h16w_kernel<c.bm, c.bn, c.wm, c.wn, c.bkh>), nt};
     else if constexpr (KF == KF_H16 || KF == KF_H16K)
         return {reinterpret_cast<const void*>(
                     &igemm_h16_kernel<OP, c.bm, c.bn, c.wm, c.wn, c.bkh>), nt};
@@ -1595,13 +1778,16 @@ GemmPlan plan_gemm(int op, const ConvGeo& g, int bf16, int num_cus, int bias_col
     const long tiles = ((p.M + c.bm - 1) / c.bm) * ((p.Ncols + c.bn - 1) / c.bn);
     const int bk = p.h16 ? c.bkh : (bf16 ? BKH : c.bk);
     const long ktiles = (p.Kred + bk - 1) / bk;
-    // both operands k-major: one tap per k tile, 32-bit buffer offsets
+    // buffer-load kernels (32-bit offsets): FWD and stride-1 DGRAD with both
+    // operands k-major and one tap per k tile; WGRAD on m-major LDS tiles
+    const long lim = (1L << 30) - (1L << 20);         // elements of a bf16 operand (< 2 GB)
+    const long x_el = (long)g.N * g.H * g.W * g.C, dy_el = (long)g.N * g.P * g.Q * g.K;
     if (p.h16 && (op == OP_FWD || (op == OP_DGRAD && g.st == 1))) {
         const long cc = (op == OP_FWD) ? g.C : g.K;
-        const long a_el = (op == OP_FWD) ? (long)g.N * g.H * g.W * g.C
-                                         : (long)g.N * g.P * g.Q * g.K;
-        const long lim = (1L << 30) - (1L << 20);     // elements of a bf16 operand (< 2 GB)
+        const long a_el = (op == OP_FWD) ? x_el : dy_el;
         p.h16k = (cc % bk == 0 && a_el < lim && p.Ncols * p.Kred < lim) ? 1 : 0;
+    } else if (p.h16 && op == OP_WGRAD && !p.bias_col) {
+        p.h16k = (x_el < lim && dy_el < lim) ? 1 : 0;
     }
     // workgroups resident at once
     KernelRef kr = kernel_for(op, p.cfg,
@@ -1643,6 +1829,19 @@ GemmPlan plan_gemm(int op, const ConvGeo& g, int bf16, int num_cus, int bias_col
     return p;
 }
 
+namespace {
+// Division by a constant d >= 1 for numerators below 2^31 (Granlund and
+// Montgomery, round-up method): with l = ceil(log2 d) and m = ceil(2^(31+l)/d),
+// m d - 2^(31+l) < d <= 2^l, hence floor(i m / 2^(31+l)) = floor(i / d).
+void div_magic(int d, unsigned* m, int* sh) {
+    int l = 0;
+    while ((1L << l) < d) ++l;
+    const unsigned long long num = 1ULL << (31 + l);
+    *m = (unsigned)((num + (unsigned long long)d - 1) / (unsigned long long)d);
+    *sh = 31 + l;
+}
+}  // namespace
+
 hipError_t launch_gemm(const GemmPlan& plan, const ConvGeo& g, const float* a, const float* b,
                        float* out, const Epilogue& ep, float* ws, hipStream_t s,
                        const uint16_t* a16, const uint16_t* b16, const uint16_t* b16t) {
@@ -1673,6 +1872,10 @@ hipError_t launch_gemm(const GemmPlan& plan, const ConvGeo& g, const float* a, c
     v4 = v4 && ((((uintptr_t)a) | ((uintptr_t)b)) & 15) == 0;
     // DGRAD on k-major operands takes the transposed weights b16t
     const uint16_t* bk16 = plan.op == OP_DGRAD ? b16t : b16;
+    if (plan.op == OP_WGRAD) {
+        div_magic(g.Q, &k.mq, &k.sq);
+        div_magic(g.P, &k.mp, &k.sp);
+    }
     const bool h16k = plan.h16k && a16 && bk16 && ((((uintptr_t)a16) | ((uintptr_t)bk16)) & 15) == 0;
     const bool h16 = !h16k && plan.h16 && plan.bf16 && !plan.bias_col && a16 && b16 &&
                      ((((uintptr_t)a16) | ((uintptr_t)b16)) & 15) == 0;
