@@ -136,8 +136,9 @@ def cpu_baseline(wl, layers, out_shape, images):
 
 def run_pipeline(args, wl, dev):
     """Throughput of one virtual worker run as a K-partition pipeline (K HIP
-    streams, up to W = s_local + 1 minibatches in flight, partitions balanced
-    by nominal work at block boundaries), against K = 1 in the same process.
+    streams, up to W = s_local + 1 minibatches in flight, cut at block
+    boundaries by nominal work or by the partitioner on measured per-layer
+    times and memory), against K = 1 in the same process.
     A step is one minibatch; the timed region covers whole waves after one
     warm-up wave, so pipeline fill and drain are included once."""
     import torch
@@ -160,9 +161,23 @@ def run_pipeline(args, wl, dev):
     W = wl.s_local + 1
     waves = max(1, -(-args.steps // W))
     result = {}
+    plan_info = None
     for k in (1, args.pipeline):
-        cuts = balanced_cuts(layers, k, layer_costs(layers, wl.H, wl.W, wl.C, wl.batch)) \
-            if k > 1 else []
+        if k == 1:
+            cuts = []
+        elif args.partition == "measured":
+            # the partitioner on this GPU's measured per-layer times and memory,
+            # K partitions on K GPUs of this type (288 GB each)
+            from paper_2005_14038_amd import partitioner as pt
+            prof = pt.profile(layers, wl.batch, wl.H, wl.W, wl.C, dtype=wl.dtype, steps=3)
+            plan = pt.partition(layers, prof, [pt.GPUSpec("MI355X", 1.0, 288e9)] * k, W)
+            cuts = plan.cuts
+            plan_info = {"predicted_bottleneck_ms": round(plan.bottleneck_ms, 4),
+                         "parts": [{"layers": [a, b], "ms": round(ms, 4),
+                                    "GB": round(mem / 1e9, 3), "stashes": nst}
+                                   for a, b, _, ms, mem, nst in plan.parts]}
+        else:
+            cuts = balanced_cuts(layers, k, layer_costs(layers, wl.H, wl.W, wl.C, wl.batch))
         pv = PipelinedVW(layers, wl.batch, wl.H, wl.W, wl.C, w0, wl.s_local, wl.lr, data, cuts,
                          dtype=wl.dtype)
         pv.run(1)
@@ -188,7 +203,10 @@ def run_pipeline(args, wl, dev):
                                f"worker, N_m = {W}, {K} partitions cut after layers {cuts}",
                    "global_batch": wl.batch, "parallelism": f"pipeline {K} streams, one GPU"},
         "one_partition": {"value": round(result[1][0], 3), "ms_per_step": round(result[1][1], 4)},
+        "partition": args.partition,
     }
+    if plan_info:
+        out["partition_plan"] = plan_info
     print(json.dumps(out), flush=True)
 
 
@@ -205,6 +223,9 @@ def main():
     ap.add_argument("--dtype", choices=["fp32", "bf16"], default=None,
                     help="contraction mode (default: the workload's); bf16 rounds the "
                          "contraction operands and keeps fp32 master weights")
+    ap.add_argument("--partition", choices=["work", "measured"], default="work",
+                    help="with --pipeline: cut by nominal work, or by the partitioner on "
+                         "per-layer times and memory measured on this GPU")
     ap.add_argument("--pipeline", type=int, default=0, metavar="K",
                     help="run one virtual worker as a K-partition pipeline on K streams "
                          "(workloads with a loss head) instead of the stage step")

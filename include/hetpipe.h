@@ -101,6 +101,12 @@ int hp_stage_param_layout(const hp_stage *st, int layer, size_t *offset, size_t 
 int hp_stage_output_shape(const hp_stage *st, int layer, int dims[3]);
 /* Bytes of device memory the stage holds. */
 int hp_stage_device_bytes(const hp_stage *st, size_t *bytes);
+/* The same bytes by owner, for the model partitioner's memory model (HetPipe
+ * Sec. 4, model partitioning): bytes[i] = buffers of layer i's value, its
+ * gradient, its statistics and its bf16 copies; bytes[n_layers] = stage-level
+ * buffers (contraction workspaces, bf16 weight copies, the input's bf16
+ * copy).  n must be n_layers + 1; the entries sum to hp_stage_device_bytes. */
+int hp_stage_layer_bytes(const hp_stage *st, size_t *bytes, int n);
 
 /* Device timing of the stage's own kernels, for profiling.  While enabled,
  * every kernel the stage enqueues is bracketed by HIP events on the stage's
@@ -110,6 +116,15 @@ int hp_stage_device_bytes(const hp_stage *st, size_t *bytes);
  * reductions), [1] every other stage kernel -- and resets the sums. */
 int hp_stage_set_timing(hp_stage *st, int enable);
 int hp_stage_read_timing(hp_stage *st, double ms[2], int64_t launches[2]);
+/* The same records per layer, for the model partitioner's per-layer profile
+ * (HetPipe Sec. 4, model partitioning; Sec. 6, partitioning algorithm):
+ * fwd_ms[i] / bwd_ms[i] receive the summed device time of the kernels that
+ * the forward / backward pass enqueued for layer i (the weight gradient
+ * included, whichever stream ran it); slot n_layers holds stage-level work
+ * (the bf16 weight copies).  n must be n_layers + 1.  Synchronises the stream
+ * and resets the records, like hp_stage_read_timing (either call consumes
+ * them). */
+int hp_stage_read_layer_timing(hp_stage *st, double *fwd_ms, double *bwd_ms, int n);
 
 /* Forward pass of one minibatch (HetPipe Sec. 3: the layers of the stage in
  * order) at weights `w` (flat fp32, length P).  `x` is the stage input

@@ -86,7 +86,10 @@ size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
 struct StageTimer {
     bool on = false;
-    struct Rec { hipEvent_t a, b; int cat; };
+    // layer (node index, -1 for stage-level work) and pass (0 forward, 1
+    // backward) that the next records belong to
+    int node = -1, phase = 0;
+    struct Rec { hipEvent_t a, b; int cat, node, phase; };
     std::vector<Rec> recs;          // recorded, not yet read
     std::vector<hipEvent_t> pool;   // free events
     hipEvent_t take() {
@@ -108,7 +111,7 @@ struct StageTimer {
         hipEvent_t b = take();
         if (!b) return;
         (void)hipEventRecord(b, s);
-        recs.push_back({cur_a, b, cur});
+        recs.push_back({cur_a, b, cur, node, phase});
         cur_a = nullptr;
     }
     ~StageTimer() {
@@ -128,6 +131,12 @@ struct hp_stage {
     float* ws = nullptr;
     std::vector<void*> allocs;
     size_t bytes = 0;
+    // device bytes per layer (buffers that belong to one layer's value,
+    // gradient or statistics) and the stage-level rest (workspaces, weight
+    // copies, the input copy); dev_alloc charges cur_node (-1: stage level)
+    std::vector<size_t> node_bytes;
+    size_t shared_bytes = 0;
+    int cur_node = -1;
     bool has_loss = false;
     // bf16 mode with bf16 operands in memory: copies of the weights, of the
     // stage input and (scratch, one conv at a time) of a conv's output gradient
@@ -194,6 +203,10 @@ int dev_alloc(hp_stage* st, float** p, size_t floats) {
                     "hipMalloc(%zu bytes): %s", floats * sizeof(float), hipGetErrorString(e));
     st->allocs.push_back(q);
     st->bytes += floats * sizeof(float);
+    if (st->cur_node >= 0 && st->cur_node < (int)st->node_bytes.size())
+        st->node_bytes[st->cur_node] += floats * sizeof(float);
+    else
+        st->shared_bytes += floats * sizeof(float);
     *p = (float*)q;
     return HP_OK;
 }
@@ -360,8 +373,10 @@ int build_stage(hp_stage* st, const hp_layer* layers, int n_layers) {
         r.bwd_by_consumer = true;
     }
     // device buffers
+    st->node_bytes.assign(n_layers, 0);
     for (int i = 0; i < n_layers; ++i) {
         Node& nd = st->nodes[i];
+        st->cur_node = i;
         if (nd.L.kind == HP_SOFTMAX_CE) continue;
         if (nd.relu_fused) {
             nd.y = st->nodes[nd.L.in0].y;
@@ -383,13 +398,16 @@ int build_stage(hp_stage* st, const hp_layer* layers, int n_layers) {
         if ((nd.L.kind != HP_CONV && nd.L.kind != HP_FC) || !nd.fwd.h16) continue;
         any16 = true;
         const int j = nd.L.in0;
+        st->cur_node = i;
         int rc = dev_alloc16(st, &nd.g16, nd.out_elems);
+        st->cur_node = j;
         if (!rc && j < 0 && !st->x16)
             rc = dev_alloc16(st, &st->x16, (size_t)st->batch * st->H * st->W * st->C);
         else if (!rc && j >= 0 && !st->nodes[j].y16)
             rc = dev_alloc16(st, &st->nodes[j].y16, st->nodes[j].out_elems);
         if (rc) return rc;
     }
+    st->cur_node = -1;
     if (any16) {
         int rc = dev_alloc16(st, &st->w16, st->P);
         if (rc) return rc;
@@ -529,6 +547,36 @@ extern "C" int hp_stage_read_timing(hp_stage* st, double ms[2], int64_t launches
     return read_timer(st->timer, st->stream, 2, ms, launches);
 }
 
+extern "C" int hp_stage_layer_bytes(const hp_stage* st, size_t* bytes, int n) {
+    if (!st || !bytes) return fail(HP_ERR_ARG, "hp_stage_layer_bytes: NULL argument");
+    const int nl = (int)st->nodes.size();
+    if (n != nl + 1)
+        return fail(HP_ERR_ARG, "hp_stage_layer_bytes: n = %d, the stage needs %d", n, nl + 1);
+    for (int i = 0; i < nl; ++i) bytes[i] = st->node_bytes[i];
+    bytes[nl] = st->shared_bytes;
+    return HP_OK;
+}
+
+extern "C" int hp_stage_read_layer_timing(hp_stage* st, double* fwd_ms, double* bwd_ms, int n) {
+    if (!st || !fwd_ms || !bwd_ms) return fail(HP_ERR_ARG, "hp_stage_read_layer_timing: NULL argument");
+    const int nl = (int)st->nodes.size();
+    if (n != nl + 1)
+        return fail(HP_ERR_ARG, "hp_stage_read_layer_timing: n = %d, the stage needs %d", n, nl + 1);
+    HP_HIP(hipStreamSynchronize(st->stream));
+    for (int i = 0; i < n; ++i) fwd_ms[i] = bwd_ms[i] = 0.0;
+    StageTimer& tm = st->timer;
+    for (auto& r : tm.recs) {
+        float t = 0.f;
+        HP_HIP(hipEventElapsedTime(&t, r.a, r.b));
+        const int slot = (r.node >= 0 && r.node < nl) ? r.node : nl;
+        (r.phase ? bwd_ms : fwd_ms)[slot] += t;
+        tm.pool.push_back(r.a);
+        tm.pool.push_back(r.b);
+    }
+    tm.recs.clear();
+    return HP_OK;
+}
+
 extern "C" int hp_stage_forward(hp_stage* st, const float* w, const float* x, float* y,
                                 const int32_t* labels, float* loss) {
     if (!st || !x || (!w && st->P)) return fail(HP_ERR_ARG, "hp_stage_forward: NULL argument");
@@ -541,6 +589,8 @@ extern "C" int hp_stage_forward(hp_stage* st, const float* w, const float* x, fl
     const int B = st->batch;
     st->x16_ready = false;
     for (Node& nd : st->nodes) nd.y16_ready = false;
+    st->timer.node = -1;
+    st->timer.phase = 0;
     if (st->w16) {
         st->timer.begin(1, s);
         hipError_t e = launch_cast_bf16(w, st->w16, st->P, s);
@@ -555,6 +605,7 @@ extern "C" int hp_stage_forward(hp_stage* st, const float* w, const float* x, fl
         Node& nd = st->nodes[i];
         const hp_layer& L = nd.L;
         const float* in = L.in0 < 0 ? x : st->nodes[L.in0].y;
+        st->timer.node = (int)i;
         hipError_t e = hipSuccess;
         StageTimer& tm = st->timer;
         const uint16_t* in16 = nullptr;
@@ -679,9 +730,11 @@ extern "C" int hp_stage_backward(hp_stage* st, const float* w, const float* dy, 
         return true;
     };
 
+    st->timer.phase = 1;
     for (int i = n - 1; i >= 0; --i) {
         Node& nd = st->nodes[i];
         const hp_layer& L = nd.L;
+        st->timer.node = i;
         if (L.kind == HP_SOFTMAX_CE) continue;
         const float* gin;
         if (i == n - 1 && !st->has_loss) gin = dy;

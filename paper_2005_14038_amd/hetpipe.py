@@ -23,8 +23,10 @@ HP_FP32, HP_BF16 = 0, 1
 
 EXPORTS = [
     "hp_stage_create", "hp_stage_destroy", "hp_stage_param_count", "hp_stage_param_layout",
-    "hp_stage_output_shape", "hp_stage_device_bytes", "hp_stage_set_timing",
-    "hp_stage_read_timing", "hp_stage_forward", "hp_stage_backward",
+    "hp_stage_output_shape", "hp_stage_device_bytes", "hp_stage_layer_bytes",
+    "hp_stage_set_timing",
+    "hp_stage_read_timing", "hp_stage_read_layer_timing", "hp_stage_forward",
+    "hp_stage_backward",
     "hp_ps_create", "hp_ps_destroy", "hp_ps_weights", "hp_ps_clock", "hp_ps_set_timing",
     "hp_ps_read_timing",
     "hp_vw_create", "hp_vw_destroy", "hp_vw_set_momentum", "hp_wsp_weights",
@@ -78,6 +80,8 @@ def lib():
     L.hp_stage_set_timing.argtypes = [_vp, i32]
     L.hp_stage_read_timing.argtypes = [_vp, ctypes.POINTER(ctypes.c_double * 2),
                                        ctypes.POINTER(ctypes.c_int64 * 2)]
+    L.hp_stage_read_layer_timing.argtypes = [_vp, _vp, _vp, i32]
+    L.hp_stage_layer_bytes.argtypes = [_vp, _vp, i32]
     L.hp_stage_forward.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp]
     L.hp_stage_backward.argtypes = [_vp, _vp, _vp, _vp, _vp]
     L.hp_ps_create.argtypes = [sz, _vp, i32, i32, _vp, _pp]
@@ -196,6 +200,23 @@ class Stage:
         _check(self._L.hp_stage_read_timing(self.h, ctypes.byref(ms), ctypes.byref(n)))
         return ({"contraction": ms[0], "other": ms[1]},
                 {"contraction": int(n[0]), "other": int(n[1])})
+
+    def layer_bytes(self):
+        """(per-layer device bytes, stage-level bytes)."""
+        n = len(self.layers) + 1
+        b = (ctypes.c_size_t * n)()
+        _check(self._L.hp_stage_layer_bytes(self.h, ctypes.byref(b), n))
+        return list(b)[:-1], b[n - 1]
+
+    def read_layer_timing(self):
+        """(fwd_ms, bwd_ms): per-layer device time of the timed passes since the
+        last read, lists of n_layers + 1 (the last entry: stage-level work such
+        as the bf16 weight copies); resets."""
+        n = len(self.layers) + 1
+        f = (ctypes.c_double * n)()
+        b = (ctypes.c_double * n)()
+        _check(self._L.hp_stage_read_layer_timing(self.h, ctypes.byref(f), ctypes.byref(b), n))
+        return list(f), list(b)
 
     def forward(self, w, x, y=None, labels=None, loss=None):
         _check(self._L.hp_stage_forward(self.h, _ptr(w), _ptr(x), _ptr(y), _ptr(labels),

@@ -5,9 +5,9 @@ HetPipe runs a virtual worker (VW) as pipelined model parallelism over k GPUs
 minibatches are in the pipeline at once, and a new minibatch enters as soon as
 an earlier one completes.  Here the k partitions share one GPU: partition q
 runs on its own HIP stream, cross-partition order is carried by HIP events,
-and every partition keeps one activation stash per in-flight minibatch (one
-stage object per pipeline slot), as each minibatch's forward activations and
-weight version must survive until its backward pass (Sec. 4).
+and every partition keeps one activation stash (stage object) per minibatch
+it holds at once, as each minibatch's forward activations and weight version
+must survive until its backward pass (Sec. 4).
 
 Scheduling follows the rules of Sec. 4 (partition scheduling): on every
 partition the forward tasks run in minibatch order, the backward tasks run in
@@ -262,6 +262,27 @@ def schedule(k, W, total, d_fwd=None, d_bwd=None, d_upd=0.0):
     return out
 
 
+def stash_counts(k, W, d_fwd=None, d_bwd=None):
+    """Largest number of minibatches that partition q holds at once between
+    the start of their forward and the end of their backward pass, under the
+    schedule above (Sec. 4: the first partition holds the most, the last one
+    only the minibatch it is processing).  On one partition the forward and
+    the backward tasks each run in minibatch order, so the minibatches held
+    form a contiguous range and minibatch m can use stash m mod count."""
+    total = 3 * W + 2 * k
+    held = [0] * k
+    most = [0] * k
+    for t in schedule(k, W, total, d_fwd, d_bwd):
+        if t.kind == "F":
+            held[t.q] += 1
+            most[t.q] = max(most[t.q], held[t.q])
+        elif t.kind == "FB":
+            most[t.q] = max(most[t.q], held[t.q] + 1)
+        elif t.kind == "B":
+            held[t.q] -= 1
+    return most
+
+
 # ----------------------------------------------------------------- driver
 
 class PipelinedVW:
@@ -283,9 +304,12 @@ class PipelinedVW:
         self.P = sum(p.p_cnt for p in self.parts)
         self.streams = [torch.cuda.Stream(device=dev) for _ in range(self.k)]
         self.ps_stream = torch.cuda.Stream(device=dev)
-        # one stage object (activation stash) per partition and pipeline slot
+        # one stage object (activation stash) per minibatch a partition holds
+        # at once: minibatch m uses stash (m - 1) mod slots[q]
+        self.slots = stash_counts(self.k, self.W, d_fwd, d_bwd)
         self.stages = [[Stage(p.layers, batch, *p.in_shape, dtype=dtype, stream=s)
-                        for _ in range(self.W)] for p, s in zip(self.parts, self.streams)]
+                        for _ in range(n)]
+                       for p, s, n in zip(self.parts, self.streams, self.slots)]
         for p, st in zip(self.parts, self.stages):
             assert st[0].P == p.p_cnt, (st[0].P, p.p_cnt)
         self.acts = [[torch.empty((batch,) + tuple(p.out_shape), dtype=torch.float32, device=dev)
@@ -345,7 +369,8 @@ class PipelinedVW:
             if t.kind == "U":
                 self._complete(m, slot, total)
                 continue
-            part, st, s = self.parts[q], self.stages[q][slot], self.streams[q]
+            part, s = self.parts[q], self.streams[q]
+            st = self.stages[q][(m - 1) % self.slots[q]]
             w = self.wptr[m] + 4 * part.p_off
             grad = self.grads[slot][part.p_off:]
             x, labels, _ = self.inputs[m]
