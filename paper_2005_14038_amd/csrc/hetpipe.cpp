@@ -59,7 +59,7 @@ struct Node {
     float* y = nullptr;                 // forward output (a fused ReLU aliases its producer)
     float* g = nullptr;                 // gradient of the output
     bool g_written = false;
-    const float* g_alias = nullptr;     // gradient handed over without a copy (ReLU -> BN)
+    const float* g_alias = nullptr;     // gradient handed over without a copy (ReLU -> BN, add -> sole-consumer input)
     int mask_into = -1;                 // data gradient goes to this producer, ReLU-masked
     bool bias_in_wgrad = false;         // bias gradient computed by the weight-gradient GEMM
     bool bwd_by_consumer = false;       // (ReLU) its backward is fused into its consumer
@@ -837,9 +837,22 @@ extern "C" int hp_stage_backward(hp_stage* st, const float* w, const float* dy, 
                 break;
             }
             case HP_ADD: {
-                if (dest(L.in0, &d, &acc)) e = launch_copy_or_acc(gin, d, nd.out_elems, acc, s);
-                if (e == hipSuccess && dest(L.in1, &d, &acc))
-                    e = launch_copy_or_acc(gin, d, nd.out_elems, acc, s);
+                // both inputs receive this gradient unchanged.  An input that
+                // nothing else reads takes it as its own without a copy (its
+                // backward only reads it; the layers that wrote it are done),
+                // unless it is the caller's dy.
+                auto route = [&](int j) -> hipError_t {
+                    if (j >= 0 && gin != dy && st->nodes[j].consumers == 1 &&
+                        !st->nodes[j].g_written) {
+                        st->nodes[j].g_alias = gin;
+                        st->nodes[j].g_written = true;
+                        return hipSuccess;
+                    }
+                    if (dest(j, &d, &acc)) return launch_copy_or_acc(gin, d, nd.out_elems, acc, s);
+                    return hipSuccess;
+                };
+                e = route(L.in0);
+                if (e == hipSuccess) e = route(L.in1);
                 break;
             }
             case HP_GAP:
