@@ -351,14 +351,28 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_kernel(KA
         for (int i = 0; i < BV; ++i) { brow_n[i] = 0; brow_ok[i] = true; }
     }
 
-    float areg[AV][VW];
-    float breg[BV][VW];
+    // two register sets of staged operands (tile kt+2 loads while kt+1 waits
+    // to be written to LDS) and their masks; loads are unconditional (masked
+    // lanes read the operand's first element) and the mask is applied when
+    // the registers are written to LDS
+    float areg[2][AV][VW];
+    float breg[2][BV][VW];
+    bool aok[2][AV], bok[2][BV], bone[2][BV];
+    auto ld = [](const float* p, float* v) {
+        if constexpr (VW == 4) {
+            const float4 t4 = *reinterpret_cast<const float4*>(p);
+            v[0] = t4.x; v[1] = t4.y; v[2] = t4.z; v[3] = t4.w;
+        } else {
+            v[0] = *p;
+        }
+    };
 
     // Staging of one reduction tile [k0, k0 + BK).  The decomposition of k0 into
     // (filter tap, channel) or (image, output row, output column) is uniform
     // across the workgroup (scalar unit); each thread then steps from it by its
     // own small offset instead of dividing per element.
-    auto gload = [&](int kt) {
+    auto gload = [&](int kt, auto S) {
+        constexpr int s = decltype(S)::value;
         const int k0 = (int)(kbeg + (long)kt * BK);
         const int kend_i = (int)kend;
         if constexpr (OP == OP_FWD || OP == OP_DGRAD) {
@@ -380,7 +394,8 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_kernel(KA
                                   (unsigned)w < (unsigned)g.W;
                         const float* ptr =
                             args.a + (ok ? (arow_base[i] + ((long)h * g.W + w) * g.C + c) : 0);
-                        load_vec<VW>(ptr, ok, areg[i]);
+                        ld(ptr, areg[s][i]);
+                        aok[s][i] = ok;
                     } else {
                         int tp = arow_h[i] - r, tq = arow_w[i] - sx;
                         int p = tp, q = tq;
@@ -394,7 +409,8 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_kernel(KA
                                   p < g.P && q < g.Q;
                         const float* ptr =
                             args.a + (ok ? (arow_base[i] + ((long)p * g.Q + q) * g.K + c) : 0);
-                        load_vec<VW>(ptr, ok, areg[i]);
+                        ld(ptr, areg[s][i]);
+                        aok[s][i] = ok;
                     }
                 }
             }
@@ -405,7 +421,8 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_kernel(KA
                     const int kk = k0 + bkv;
                     bool ok = brow_ok[i] && kk < kend_i;
                     const float* ptr = args.b + (ok ? (brow_n[i] * args.Kred + kk) : 0);
-                    load_vec<VW>(ptr, ok, breg[i]);
+                    ld(ptr, breg[s][i]);
+                    bok[s][i] = ok;
                 } else {   // B[kk = (r,s,k)][c] = w[k][r][s][c]
                     const int kr = (t + i * NT) / BVPR;
                     int k = c0 + kr, r = r0, sx = s0;
@@ -413,7 +430,8 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_kernel(KA
                     bool ok = bcol_ok && k0 + kr < kend_i;
                     const float* ptr =
                         args.b + (ok ? ((((long)k * g.R + r) * g.S + sx) * g.C + bcol_c) : 0);
-                    load_vec<VW>(ptr, ok, breg[i]);
+                    ld(ptr, breg[s][i]);
+                    bok[s][i] = ok;
                 }
             }
         } else {
@@ -423,7 +441,8 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_kernel(KA
                 const int kk = k0 + (t + i * NT) / AVPR;
                 bool ok = arow_ok[i] && kk < kend_i;
                 const float* ptr = args.b + (ok ? ((long)kk * g.K + arow_base[i]) : 0);
-                load_vec<VW>(ptr, ok, areg[i]);
+                ld(ptr, areg[s][i]);
+                aok[s][i] = ok;
             }
             // ---- B: B[kk = (n,p,q)][j = (r,s,c)] = x[n, p*st-pad+r, q*st-pad+s, c] ----
             const int q0 = k0 % g.Q;
@@ -441,30 +460,30 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_kernel(KA
                           (unsigned)w < (unsigned)g.W;
                 const float* ptr =
                     args.a + (ok ? ((((long)n * g.H + h) * g.W + w) * g.C + bcol_c) : 0);
-                load_vec<VW>(ptr, ok, breg[i]);
-                if (bcol_ones) {
-                    breg[i][0] = kin ? 1.f : 0.f;
-#pragma unroll
-                    for (int j = 1; j < VW; ++j) breg[i][j] = 0.f;
-                }
+                ld(ptr, breg[s][i]);
+                bok[s][i] = ok;
+                bone[s][i] = bcol_ones && kin;
             }
         }
     };
 
-    auto sstore = [&](int buf) {
-        float* As = smem + buf * BK * (LDA + LDB);
+    auto sstore = [&](auto S) {
+        constexpr int s = decltype(S)::value;
+        float* As = smem + s * BK * (LDA + LDB);
         float* Bs = As + BK * LDA;
 #pragma unroll
         for (int i = 0; i < AV; ++i) {
             if constexpr (A_KMAJ) {
                 int row = (t + i * NT) / KVPR;
 #pragma unroll
-                for (int j = 0; j < VW; ++j) As[(akv + j) * LDA + row] = areg[i][j];
+                for (int j = 0; j < VW; ++j)
+                    As[(akv + j) * LDA + row] = aok[s][i] ? areg[s][i][j] : 0.f;
             } else {
                 int kr = (t + i * NT) / AVPR;
                 int col = ((t + i * NT) % AVPR) * VW;
 #pragma unroll
-                for (int j = 0; j < VW; ++j) As[kr * LDA + col + j] = areg[i][j];
+                for (int j = 0; j < VW; ++j)
+                    As[kr * LDA + col + j] = aok[s][i] ? areg[s][i][j] : 0.f;
             }
         }
 #pragma unroll
@@ -472,12 +491,17 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_kernel(KA
             if constexpr (B_KMAJ) {
                 int row = (t + i * NT) / KVPR;
 #pragma unroll
-                for (int j = 0; j < VW; ++j) Bs[(bkv + j) * LDB + row] = breg[i][j];
+                for (int j = 0; j < VW; ++j)
+                    Bs[(bkv + j) * LDB + row] = bok[s][i] ? breg[s][i][j] : 0.f;
             } else {
                 int kr = (t + i * NT) / BVPR;
                 int col = ((t + i * NT) % BVPR) * VW;
 #pragma unroll
-                for (int j = 0; j < VW; ++j) Bs[kr * LDB + col + j] = breg[i][j];
+                for (int j = 0; j < VW; ++j) {
+                    // the appended column of ones (bias gradient) in lane 0
+                    const float one = (j == 0 && bone[s][i]) ? 1.f : 0.f;
+                    Bs[kr * LDB + col + j] = bok[s][i] ? breg[s][i][j] : one;
+                }
             }
         }
     };
@@ -490,35 +514,48 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_kernel(KA
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
-    if (ktiles > 0) {
-        gload(0);
-        sstore(0);
-    }
-    __syncthreads();
     const int lr = lane & 31;
     const int lk = lane >> 5;
-    for (int kt = 0; kt < ktiles; ++kt) {
-        const int buf = kt & 1;
-        if (kt + 1 < ktiles) gload(kt + 1);
-        const float* As = smem + buf * BK * (LDA + LDB);
+    // one k tile: prefetch tile kt+2 into register set s, multiply LDS buffer
+    // s, write tile kt+1 (register set s^1) to LDS buffer s^1; loads of tiles
+    // past the end are fully masked, so every load is on one path and the
+    // wait before the LDS write counts only the older set
+    auto step = [&](int kt, auto S) {
+        constexpr int s = decltype(S)::value;
+        gload(kt + 2, S);
+        const float* As = smem + s * BK * (LDA + LDB);
         const float* Bs = As + BK * LDA;
+        if (kt < ktiles) {
 #pragma unroll
-        for (int kk = 0; kk < BK; kk += 2) {
-            const float* ar = As + (kk + lk) * LDA + wm + lr;
-            const float* br = Bs + (kk + lk) * LDB + wn + lr;
-            float av[TM], bv[TN];
+            for (int kk = 0; kk < BK; kk += 2) {
+                const float* ar = As + (kk + lk) * LDA + wm + lr;
+                const float* br = Bs + (kk + lk) * LDB + wn + lr;
+                float av[TM], bv[TN];
 #pragma unroll
-            for (int i = 0; i < TM; ++i) av[i] = ar[32 * i];
+                for (int i = 0; i < TM; ++i) av[i] = ar[32 * i];
 #pragma unroll
-            for (int j = 0; j < TN; ++j) bv[j] = br[32 * j];
+                for (int j = 0; j < TN; ++j) bv[j] = br[32 * j];
 #pragma unroll
-            for (int i = 0; i < TM; ++i)
+                for (int i = 0; i < TM; ++i)
 #pragma unroll
-                for (int j = 0; j < TN; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[i], bv[j], acc[i][j], 0, 0, 0);
+                    for (int j = 0; j < TN; ++j)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[i], bv[j], acc[i][j],
+                                                                        0, 0, 0);
+            }
         }
-        if (kt + 1 < ktiles) sstore(buf ^ 1);
+        if (kt + 1 < ktiles) sstore(std::integral_constant<int, s ^ 1>{});
         __syncthreads();
+    };
+
+    const std::integral_constant<int, 0> I0{};
+    const std::integral_constant<int, 1> I1{};
+    gload(0, I0);
+    gload(1, I1);
+    if (ktiles > 0) sstore(I0);
+    __syncthreads();
+    for (int kt = 0; kt < ktiles; kt += 2) {
+        step(kt, I0);
+        step(kt + 1, I1);
     }
 
     store_tile<BM, BN, TM, TN>(args, wk, acc, wm, wn, lane);
