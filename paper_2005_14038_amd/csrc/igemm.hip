@@ -229,6 +229,134 @@ __device__ __forceinline__ void store_tile(const KArgs& args, const Work& w,
     }
 }
 
+// The same writes through the wave's private 4 KB LDS slot (the k loop's
+// buffers are free once its last barrier has passed): each 32x32 block is
+// staged in LDS and read back with every lane holding 4 consecutive columns of
+// one row (8 rows per pass, 4 passes, two at a time), so the epilogue's loads and stores are
+// 16 bytes wide instead of 4.  Used when the output, the bias and the mask
+// allow 16-byte access and there is no bias-gradient column; a group of 4
+// columns that crosses the last column is written element by element.
+constexpr int SLOT_FLOATS = 32 * 32;
+
+template <int BM, int BN, int TM, int TN>
+__device__ __forceinline__ void store_tile_wide(const KArgs& args, const Work& w,
+                                                const floatx16 (&acc)[TM][TN], int wm, int wn,
+                                                int lane, float* slot) {
+    const int lr = lane & 31, lk = lane >> 5;
+    const int rq = lane >> 3, cq = (lane & 7) * 4;
+    const int epi = args.epi;
+    const long N = args.Ncols;
+    float* pslot =
+        w.partial ? args.ws + ((long)(w.tile - args.tfull) * args.splits + w.z) * (BM * BN)
+                  : nullptr;
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+#pragma unroll
+        for (int i = 0; i < TM; ++i) {
+#pragma unroll
+            for (int v = 0; v < 16; ++v)
+                slot[(8 * (v >> 2) + 4 * lk + (v & 3)) * 32 + lr] = acc[i][j][v];
+            const int lcol = wn + 32 * j + cq;
+            const long col = w.n0 + lcol;
+            const bool full = col + 3 < N;
+            float4 bias = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (!w.partial && (epi & EPI_BIAS) && col < N) {
+                if (full) {
+                    bias = *reinterpret_cast<const float4*>(args.bias + col);
+                } else {
+                    bias.x = args.bias[col];
+                    if (col + 1 < N) bias.y = args.bias[col + 1];
+                    if (col + 2 < N) bias.z = args.bias[col + 2];
+                }
+            }
+            // two passes (rows 8q + rq) at a time: their epilogue reads first,
+            // then the stores
+#pragma unroll
+            for (int q0 = 0; q0 < 4; q0 += 2) {
+                float4 val[2];
+#pragma unroll
+                for (int h = 0; h < 2; ++h)
+                    val[h] = *reinterpret_cast<const float4*>(slot + (8 * (q0 + h) + rq) * 32 + cq);
+                if (w.partial) {
+#pragma unroll
+                    for (int h = 0; h < 2; ++h) {
+                        const int lrow = wm + 32 * i + 8 * (q0 + h) + rq;
+                        if (w.m0 + lrow < args.M && col < N)
+                            *reinterpret_cast<float4*>(pslot + lrow * BN + lcol) = val[h];
+                    }
+                    continue;
+                }
+                if (col >= N) continue;
+                float4 prev[2], msk[2];
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    const long row = w.m0 + wm + 32 * i + 8 * (q0 + h) + rq;
+                    prev[h] = make_float4(0.f, 0.f, 0.f, 0.f);
+                    msk[h] = make_float4(1.f, 1.f, 1.f, 1.f);
+                    if (row >= args.M) continue;
+                    const long off = row * N + col;
+                    if (full) {
+                        if (epi & EPI_ACCUM) prev[h] = *reinterpret_cast<const float4*>(args.out + off);
+                        if (epi & EPI_MASK) msk[h] = *reinterpret_cast<const float4*>(args.mask + off);
+                    } else {
+                        float* pp = &prev[h].x;
+                        float* mm = &msk[h].x;
+                        for (int e = 0; e < 4 && col + e < N; ++e) {
+                            if (epi & EPI_ACCUM) pp[e] = args.out[off + e];
+                            if (epi & EPI_MASK) mm[e] = args.mask[off + e];
+                        }
+                    }
+                }
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    const long row = w.m0 + wm + 32 * i + 8 * (q0 + h) + rq;
+                    if (row >= args.M) continue;
+                    float o[4] = {val[h].x, val[h].y, val[h].z, val[h].w};
+                    const float b4[4] = {bias.x, bias.y, bias.z, bias.w};
+                    const float p4[4] = {prev[h].x, prev[h].y, prev[h].z, prev[h].w};
+                    const float m4[4] = {msk[h].x, msk[h].y, msk[h].z, msk[h].w};
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        if (epi & EPI_BIAS) o[e] += b4[e];
+                        if (epi & EPI_RELU) o[e] = fmaxf(o[e], 0.f);
+                        if ((epi & EPI_MASK) && !(m4[e] > 0.f)) o[e] = 0.f;
+                        if (epi & EPI_ACCUM) o[e] += p4[e];
+                    }
+                    const long off = row * N + col;
+                    if (full) {
+                        *reinterpret_cast<float4*>(args.out + off) =
+                            make_float4(o[0], o[1], o[2], o[3]);
+                    } else {
+                        for (int e = 0; e < 4 && col + e < N; ++e) args.out[off + e] = o[e];
+                    }
+                }
+            }
+        }
+    }
+}
+
+// Writes a wave's tile: the wide path when the kernel was built with it
+// (WIDE) and its conditions hold (uniform).  The wide path costs registers,
+// which the fp32 kernels on long reductions, where the epilogue is a small
+// part of the time, keep for occupancy.
+template <int BM, int BN, int TM, int TN, bool WIDE = true>
+__device__ __forceinline__ void write_tile(const KArgs& args, const Work& w,
+                                           const floatx16 (&acc)[TM][TN], int wm, int wn,
+                                           int lane, float* slot) {
+    if constexpr (WIDE) {
+        auto a16 = [](const void* p) { return (((uintptr_t)p) & 15) == 0; };
+        const int epi = args.epi;
+        const bool wide = !(epi & EPI_BIASCOL) && (args.Ncols & 3) == 0 && a16(args.out) &&
+                          (!(epi & EPI_BIAS) || a16(args.bias)) &&
+                          (!(epi & EPI_MASK) || a16(args.mask)) && a16(args.ws);
+        if (wide) {
+            store_tile_wide<BM, BN, TM, TN>(args, w, acc, wm, wn, lane, slot);
+            return;
+        }
+    }
+    store_tile<BM, BN, TM, TN>(args, w, acc, wm, wn, lane);
+}
+
 // ---- operand gathers -------------------------------------------------------
 // Each returns VW consecutive elements along the operand's contiguous axis
 // (zero where the element lies outside the problem or in the padding).
@@ -247,7 +375,7 @@ __device__ __forceinline__ void load_vec(const float* p, bool ok, float* v) {
     }
 }
 
-template <int OP, int BM, int BN, int BK, int WM, int WN, int VW>
+template <int OP, int BM, int BN, int BK, int WM, int WN, int VW, bool WIDE = false>
 __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_kernel(KArgs args) {
     constexpr int NT = 64 * (BM / WM) * (BN / WN);
     constexpr int TM = WM / 32, TN = WN / 32;  // MFMA tiles per wave
@@ -558,7 +686,9 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_kernel(KA
         step(kt + 1, I1);
     }
 
-    store_tile<BM, BN, TM, TN>(args, wk, acc, wm, wn, lane);
+    static_assert(sizeof(smem) >= (NT / 64) * SLOT_FLOATS * sizeof(float), "epilogue slots");
+    write_tile<BM, BN, TM, TN, WIDE>(args, wk, acc, wm, wn, lane,
+                               reinterpret_cast<float*>(smem) + wave * SLOT_FLOATS);
 }
 
 // ---- bf16 kernel ------------------------------------------------------------
@@ -911,7 +1041,9 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_bf16_kern
         if (kt + 1 < ktiles) sstore(buf ^ 1);
         __syncthreads();
     }
-    store_tile<BM, BN, TM, TN>(args, wk, acc, wm, wn, lane);
+    static_assert(sizeof(smem) >= (NT / 64) * SLOT_FLOATS * sizeof(float), "epilogue slots");
+    write_tile<BM, BN, TM, TN>(args, wk, acc, wm, wn, lane,
+                               reinterpret_cast<float*>(smem) + wave * SLOT_FLOATS);
 }
 
 
@@ -1249,7 +1381,9 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_h16_kerne
         step(kt, I0);
         step(kt + 1, I1);
     }
-    store_tile<BM, BN, TM, TN>(args, wk, acc, wm, wn, lane);
+    static_assert(sizeof(smem) >= (NT / 64) * SLOT_FLOATS * sizeof(float), "epilogue slots");
+    write_tile<BM, BN, TM, TN>(args, wk, acc, wm, wn, lane,
+                               reinterpret_cast<float*>(smem) + wave * SLOT_FLOATS);
 }
 
 // ---- bf16 kernel on k-major bf16 operands -------------------------------------
@@ -1434,7 +1568,9 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_h16k_kern
         step(kt, I0);
         step(kt + 1, I1);
     }
-    store_tile<BM, BN, TM, TN>(args, wk, acc, wm, wn, lane);
+    static_assert(sizeof(smem) >= (NT / 64) * SLOT_FLOATS * sizeof(float), "epilogue slots");
+    write_tile<BM, BN, TM, TN>(args, wk, acc, wm, wn, lane,
+                               reinterpret_cast<float*>(smem) + wave * SLOT_FLOATS);
 }
 
 
@@ -1610,7 +1746,9 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_h16w_kern
         step(kt, I0);
         step(kt + 1, I1);
     }
-    store_tile<BM, BN, TM, TN>(args, wk, acc, wm, wn, lane);
+    static_assert(sizeof(smem) >= (NT / 64) * SLOT_FLOATS * sizeof(float), "epilogue slots");
+    write_tile<BM, BN, TM, TN>(args, wk, acc, wm, wn, lane,
+                               reinterpret_cast<float*>(smem) + wave * SLOT_FLOATS);
 }
 
 
@@ -1714,8 +1852,9 @@ struct KernelRef {
 // Kernel families: fp32 operands staged from fp32 (vector width 1 or 4),
 // bf16 rounded while staging from fp32 (1 or 4), bf16 operands in memory
 // (general gather), bf16 operands in memory, both k-major (FWD and stride-1
-// DGRAD with a reduction channel count that is a multiple of the k tile).
-enum { KF_F32_1, KF_F32_4, KF_BF_1, KF_BF_4, KF_H16, KF_H16K };
+// DGRAD with a reduction channel count that is a multiple of the k tile), and
+// fp32 vector width 4 with the wide epilogue (short reductions).
+enum { KF_F32_1, KF_F32_4, KF_BF_1, KF_BF_4, KF_H16, KF_H16K, KF_F32_4W };
 
 template <int OP, int CFG, int KF>
 KernelRef kref() {
@@ -1733,6 +1872,9 @@ KernelRef kref() {
     else if constexpr (KF == KF_BF_1 || KF == KF_BF_4)
         return {reinterpret_cast<const void*>(
                     &igemm_bf16_kernel<OP, c.bm, c.bn, c.wm, c.wn, KF == KF_BF_4 ? 4 : 1>), nt};
+    else if constexpr (KF == KF_F32_4W)
+        return {reinterpret_cast<const void*>(
+                    &igemm_kernel<OP, c.bm, c.bn, c.bk, c.wm, c.wn, 4, true>), nt};
     else
         return {reinterpret_cast<const void*>(
                     &igemm_kernel<OP, c.bm, c.bn, c.bk, c.wm, c.wn, KF == KF_F32_4 ? 4 : 1>), nt};
@@ -1757,6 +1899,7 @@ KernelRef kref_op(int cfg, int kf) {
         case KF_BF_4: return kref_cfg<OP, KF_BF_4>(cfg);
         case KF_H16: return kref_cfg<OP, KF_H16>(cfg);
         case KF_H16K: return kref_cfg<OP, KF_H16K>(cfg);
+        case KF_F32_4W: return kref_cfg<OP, KF_F32_4W>(cfg);
         default: return kref_cfg<OP, KF_F32_1>(cfg);
     }
 }
@@ -1815,6 +1958,20 @@ GemmPlan plan_gemm(int op, const ConvGeo& g, int bf16, int num_cus, int bias_col
     const long tiles = ((p.M + c.bm - 1) / c.bm) * ((p.Ncols + c.bn - 1) / c.bn);
     const int bk = p.h16 ? c.bkh : (bf16 ? BKH : c.bk);
     const long ktiles = (p.Kred + bk - 1) / bk;
+    // fp32: the wide epilogue where the epilogue weighs: a short reduction
+    // (writes much relative to what it computes), or a moderate reduction over
+    // so few tiles that it is cut into eight or more chunks (the partial tiles
+    // written outweigh occupancy).  Long reductions (the weight gradients of
+    // large images) and larger tile counts keep the narrow kernel: its
+    // occupancy gives them more resident workgroups and reduction chunks.
+    if (!bf16 && v4) {
+        int occ_n = 0;
+        const KernelRef kn = kernel_for(op, p.cfg, KF_F32_4);
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ_n, kn.fn, kn.nt, 0) != hipSuccess ||
+            occ_n < 1)
+            occ_n = 1;
+        p.wide = (p.Kred <= 1024 || (p.Kred <= 32768 && 8 * tiles <= (long)num_cus * occ_n)) ? 1 : 0;
+    }
     // buffer-load kernels (32-bit offsets): FWD and stride-1 DGRAD with both
     // operands k-major and one tap per k tile; WGRAD on m-major LDS tiles
     const long lim = (1L << 30) - (1L << 20);         // elements of a bf16 operand (< 2 GB)
@@ -1831,7 +1988,8 @@ GemmPlan plan_gemm(int op, const ConvGeo& g, int bf16, int num_cus, int bias_col
                               p.h16k ? KF_H16K
                                      : p.h16 ? KF_H16
                                              : bf16 ? (v4 ? KF_BF_4 : KF_BF_1)
-                                                    : (v4 ? KF_F32_4 : KF_F32_1));
+                                                    : (v4 ? (p.wide ? KF_F32_4W : KF_F32_4)
+                                                          : KF_F32_1));
     int occ = 0;
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, kr.fn, kr.nt, 0) != hipSuccess || occ < 1)
         occ = 1;
@@ -1919,7 +2077,8 @@ hipError_t launch_gemm(const GemmPlan& plan, const ConvGeo& g, const float* a, c
     if (h16k) k.b16 = bk16;
     const int kf = h16k ? KF_H16K
                         : h16 ? KF_H16
-                              : plan.bf16 ? (v4 ? KF_BF_4 : KF_BF_1) : (v4 ? KF_F32_4 : KF_F32_1);
+                              : plan.bf16 ? (v4 ? KF_BF_4 : KF_BF_1)
+                                          : (v4 ? (plan.wide ? KF_F32_4W : KF_F32_4) : KF_F32_1);
     KernelRef kr = kernel_for(plan.op, plan.cfg, kf);
     void* kargs[] = {&k};
     hipError_t e = hipLaunchKernel(kr.fn, dim3(plan.nwg), dim3(kr.nt), kargs, 0, s);

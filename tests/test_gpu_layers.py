@@ -29,6 +29,7 @@ CONV = [
     (2, 11, 9, 72, 128, 3, 1, 1, False),   # data gradient, 3x3 taps, ragged N
     (3, 7, 7, 64, 64, 1, 1, 0, False),     # 1x1 both ways, ragged M
     (8, 14, 14, 256, 256, 3, 1, 1, False), # split reduction both ways
+    (4, 9, 7, 64, 128, 1, 1, 0, False),    # weight gradient on the 128x64 tile (N = 64)
 ]
 
 
