@@ -1387,9 +1387,10 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_h16_kerne
 }
 
 // ---- bf16 kernel on k-major bf16 operands -------------------------------------
-// Forward and stride-1 data-gradient contractions whose reduction channel
-// count (C forward, K data gradient) is a multiple of the k tile, so that one
-// k tile is one kernel tap (r, s) and BKX consecutive channels.  Both operands
+// Forward and stride-1 or stride-2 data-gradient contractions whose
+// reduction channel count (C forward, K data gradient) is a multiple of the
+// k tile, so that one k tile is one kernel tap (r, s) and BKX consecutive
+// channels.  Both operands
 // are k-major: A rows are gathered pixels (the implicit im2col of x; for the
 // data gradient, of dy, where the tap enters with the opposite sign), B rows
 // are weight rows (w [K][R][S][C] forward, its transposed copy [C][R][S][K]
@@ -1397,8 +1398,10 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_h16_kerne
 // check returns zeros for an offset past the end of the buffer: a lane whose
 // pixel lies in the padding, or whose row lies past the matrix, gets such an
 // offset, so staging needs no masks and a row's byte offset changes per tile
-// only by the tap term.  Same LDS layout, MFMA loop and two-tile-deep staging
-// as igemm_h16_kernel.
+// only by the tap term.  A stride-2 data gradient reads dy pixel (h/2, w/2)
+// of x pixel (h, w) shifted by the tap when both are even, and nothing
+// otherwise.  Same LDS layout, MFMA loop and two-tile-deep staging as
+// igemm_h16_kernel.
 constexpr unsigned BUF_OOB = 0x80000000u;      // buffer offset past any operand here
 constexpr int BUF_CFG = 0x00020000;            // buffer descriptor word 3 (gfx9 family)
 
@@ -1441,7 +1444,9 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_h16k_kern
     const __amdgpu_buffer_rsrc_t rsB = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<unsigned short*>(args.b16), (short)0, (int)b_bytes, BUF_CFG);
 
-    // A row i: pixel of tap (0, 0) and its element offset (channel kg)
+    // A row i: pixel of tap (0, 0) and its element offset (channel kg); for
+    // a stride-2 data gradient the offset of the image's first pixel instead
+    const bool st2 = (OP == OP_DGRAD) && g.st == 2;
     int a_h[GA], a_w[GA], a_off[GA];
     bool a_ok[GA];
 #pragma unroll
@@ -1463,7 +1468,7 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_h16k_kern
         }
         a_h[i] = h0;
         a_w[i] = w0;
-        a_off[i] = ((n * IH + h0) * IW + w0) * CC + kg;
+        a_off[i] = st2 ? n * IH * IW * CC + kg : ((n * IH + h0) * IW + w0) * CC + kg;
     }
     // B row i: byte offset of its first k (the tile's k enters as soffset)
     unsigned b_off[GB];
@@ -1494,8 +1499,16 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_h16k_kern
 #pragma unroll
         for (int i = 0; i < GA; ++i) {
             const int h = a_h[i] + dr, w = a_w[i] + ds;
-            const bool ok = a_ok[i] && (unsigned)h < (unsigned)IH && (unsigned)w < (unsigned)IW;
-            ra[s][i] = buf_load16(rsA, ok ? (unsigned)(a_off[i] + sk) * 2u : BUF_OOB, 0u);
+            if (st2) {
+                // dy pixel (h / 2, w / 2) when both are even (a tap on the stride grid)
+                const bool ok = a_ok[i] && ((h | w) & 1) == 0 && h >= 0 && w >= 0 &&
+                                (h >> 1) < IH && (w >> 1) < IW;
+                const int off = a_off[i] + ((h >> 1) * IW + (w >> 1)) * CC + tc;
+                ra[s][i] = buf_load16(rsA, ok ? (unsigned)off * 2u : BUF_OOB, 0u);
+            } else {
+                const bool ok = a_ok[i] && (unsigned)h < (unsigned)IH && (unsigned)w < (unsigned)IW;
+                ra[s][i] = buf_load16(rsA, ok ? (unsigned)(a_off[i] + sk) * 2u : BUF_OOB, 0u);
+            }
         }
 #pragma unroll
         for (int i = 0; i < GB; ++i) rb[s][i] = buf_load16(rsB, b_off[i], (unsigned)kload * 2u);
@@ -1976,7 +1989,7 @@ GemmPlan plan_gemm(int op, const ConvGeo& g, int bf16, int num_cus, int bias_col
     // operands k-major and one tap per k tile; WGRAD on m-major LDS tiles
     const long lim = (1L << 30) - (1L << 20);         // elements of a bf16 operand (< 2 GB)
     const long x_el = (long)g.N * g.H * g.W * g.C, dy_el = (long)g.N * g.P * g.Q * g.K;
-    if (p.h16 && (op == OP_FWD || (op == OP_DGRAD && g.st == 1))) {
+    if (p.h16 && (op == OP_FWD || (op == OP_DGRAD && (g.st == 1 || g.st == 2)))) {
         const long cc = (op == OP_FWD) ? g.C : g.K;
         const long a_el = (op == OP_FWD) ? x_el : dy_el;
         p.h16k = (cc % bk == 0 && a_el < lim && p.Ncols * p.Kred < lim) ? 1 : 0;

@@ -25,7 +25,7 @@ struct GemmPlan {
     int op;
     int bf16;          // round operands to bf16 (RNE) when staging
     int h16;           // bf16: the geometry allows bf16 operands in memory (launch_gemm a16/b16)
-    int h16k;          // h16 and both operands k-major (FWD; DGRAD with stride 1 and b16t)
+    int h16k;          // h16 and both operands k-major (FWD; DGRAD with stride 1 or 2 and b16t)
     int wide;          // fp32 with the wide (LDS-staged, 16-byte) epilogue: short reductions
     int bias_col;      // OP_WGRAD: Ncols includes the bias-gradient column
     int cfg;           // tile configuration

@@ -30,6 +30,9 @@ CONV = [
     (3, 7, 7, 64, 64, 1, 1, 0, False),     # 1x1 both ways, ragged M
     (8, 14, 14, 256, 256, 3, 1, 1, False), # split reduction both ways
     (4, 9, 7, 64, 128, 1, 1, 0, False),    # weight gradient on the 128x64 tile (N = 64)
+    (2, 15, 13, 32, 64, 3, 2, 1, False),   # stride-2 data gradient, 128x64 tile, odd sizes
+    (2, 14, 14, 64, 128, 1, 2, 0, False),  # stride-2 1x1 projection shape
+    (2, 16, 12, 128, 128, 3, 2, 1, False), # stride-2 data gradient, 128x128 tile
 ]
 
 
