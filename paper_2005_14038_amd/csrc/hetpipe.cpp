@@ -60,6 +60,8 @@ struct Node {
     float* g = nullptr;                 // gradient of the output
     bool g_written = false;
     const float* g_alias = nullptr;     // gradient handed over without a copy (ReLU -> BN, add -> sole-consumer input)
+    bool g_shared = false;              // g_alias is a buffer this value's other consumers accumulate into
+    bool add_share[2] = {false, false}; // (add) input 0 / 1 may take this gradient buffer as its own
     int mask_into = -1;                 // data gradient goes to this producer, ReLU-masked
     bool bias_in_wgrad = false;         // bias gradient computed by the weight-gradient GEMM
     bool bwd_by_consumer = false;       // (ReLU) its backward is fused into its consumer
@@ -347,6 +349,30 @@ int build_stage(hp_stage* st, const hp_layer* layers, int n_layers) {
         nd.out_elems = (size_t)B * nd.H * nd.W * nd.C;
     }
     st->P = off;
+    // A residual add may hand its gradient buffer to an input that has other
+    // consumers (the identity shortcut): that input's gradient then starts as
+    // the add's gradient and its other consumers accumulate into the same
+    // buffer.  Safe when the add's other input is a batch norm (its backward
+    // only reads the buffer, on the stage stream) that every other consumer of
+    // the shared input precedes: in reverse order the batch norm has read the
+    // buffer before the first accumulation.
+    for (int a = 0; a < n_layers; ++a) {
+        Node& nd = st->nodes[a];
+        if (nd.L.kind != HP_ADD) continue;
+        for (int side = 0; side < 2; ++side) {
+            const int j = side ? nd.L.in1 : nd.L.in0, k = side ? nd.L.in0 : nd.L.in1;
+            if (j < 0 || k < 0 || j == k || st->nodes[j].consumers < 2 ||
+                st->nodes[k].L.kind != HP_BN)
+                continue;
+            bool ok = true;
+            for (int c = 0; c < n_layers && ok; ++c) {
+                if (c == a) continue;
+                const hp_layer& Lc = st->nodes[c].L;
+                if (Lc.in0 == j || (Lc.kind == HP_ADD && Lc.in1 == j)) ok = c < k;
+            }
+            nd.add_share[side] = ok;
+        }
+    }
     // ReLU fusion: a ReLU reading a conv / FC / BN / add that has no other consumer
     for (int i = 0; i < n_layers; ++i) {
         Node& nd = st->nodes[i];
@@ -704,6 +730,7 @@ extern "C" int hp_stage_backward(hp_stage* st, const float* w, const float* dy, 
     for (Node& nd : st->nodes) {
         nd.g_written = false;
         nd.g_alias = nullptr;
+        nd.g_shared = false;
     }
     bool dx_written = false;
     for (Node& nd : st->nodes) nd.g16_ready = false;
@@ -722,6 +749,11 @@ extern "C" int hp_stage_backward(hp_stage* st, const float* w, const float* dy, 
             *p = dx;
             *acc = dx_written ? 1 : 0;
             dx_written = true;
+            return true;
+        }
+        if (st->nodes[j].g_shared) {           // accumulate into the shared buffer
+            *p = const_cast<float*>(st->nodes[j].g_alias);
+            *acc = 1;
             return true;
         }
         *p = st->nodes[j].g;
@@ -841,18 +873,24 @@ extern "C" int hp_stage_backward(hp_stage* st, const float* w, const float* dy, 
                 // nothing else reads takes it as its own without a copy (its
                 // backward only reads it; the layers that wrote it are done),
                 // unless it is the caller's dy.
-                auto route = [&](int j) -> hipError_t {
+                auto route = [&](int j, int side) -> hipError_t {
                     if (j >= 0 && gin != dy && st->nodes[j].consumers == 1 &&
                         !st->nodes[j].g_written) {
                         st->nodes[j].g_alias = gin;
                         st->nodes[j].g_written = true;
                         return hipSuccess;
                     }
+                    if (j >= 0 && nd.add_share[side] && gin == nd.g && !st->nodes[j].g_written) {
+                        st->nodes[j].g_alias = gin;       // the identity shortcut's gradient
+                        st->nodes[j].g_written = true;
+                        st->nodes[j].g_shared = true;
+                        return hipSuccess;
+                    }
                     if (dest(j, &d, &acc)) return launch_copy_or_acc(gin, d, nd.out_elems, acc, s);
                     return hipSuccess;
                 };
-                e = route(L.in0);
-                if (e == hipSuccess) e = route(L.in1);
+                e = route(L.in0, 0);
+                if (e == hipSuccess) e = route(L.in1, 1);
                 break;
             }
             case HP_GAP:
