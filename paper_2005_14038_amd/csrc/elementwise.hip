@@ -129,10 +129,12 @@ __global__ void copy_or_acc_kernel(const float* __restrict__ v, float* __restric
 // max-pool forward: padded taps never win; the first maximum in row-major
 // window order is kept (strict '>' comparison).
 // max-pool forward: VEC consecutive channels of one output pixel per thread
+// arg (optional): the window tap r * S + s of the first maximum, one byte per
+// output element (255: none), for the backward pass of overlapping windows.
 template <int VEC>
 __global__ void maxpool_fwd_kernel(const float* __restrict__ x, float* __restrict__ y, int N, int H,
                                    int W, int C, int R, int S, int st, int pad, int P, int Q,
-                                   uint16_t* __restrict__ y16) {
+                                   uint16_t* __restrict__ y16, uint8_t* __restrict__ arg) {
     const size_t total = (size_t)N * P * Q * C;
     for (size_t i = ((size_t)blockIdx.x * blockDim.x + threadIdx.x) * VEC; i < total;
          i += (size_t)gridDim.x * blockDim.x * VEC) {
@@ -142,6 +144,9 @@ __global__ void maxpool_fwd_kernel(const float* __restrict__ x, float* __restric
         const int p = (int)(t % P);
         const int n = (int)(t / P);
         float m[VEC];
+        int best[VEC];
+#pragma unroll
+        for (int j = 0; j < VEC; ++j) best[j] = 255;     // no tap (a window of padding)
         bool any = false;
         for (int r = 0; r < R; ++r) {
             const int h = p * st - pad + r;
@@ -153,12 +158,16 @@ __global__ void maxpool_fwd_kernel(const float* __restrict__ x, float* __restric
                 ldv<VEC>(x + (((size_t)n * H + h) * W + w) * C + c, v);
 #pragma unroll
                 for (int j = 0; j < VEC; ++j)
-                    if (!any || v[j] > m[j]) m[j] = v[j];
+                    if (!any || v[j] > m[j]) { m[j] = v[j]; best[j] = r * S + s; }
                 any = true;
             }
         }
         stv<VEC>(y + i, m);
         if (y16) st16v<VEC>(y16 + i, m);
+        if (arg) {
+#pragma unroll
+            for (int j = 0; j < VEC; ++j) arg[i + j] = (uint8_t)best[j];
+        }
     }
 }
 
@@ -214,6 +223,60 @@ __global__ void maxpool_bwd_kernel(const float* __restrict__ x, const float* __r
 #pragma unroll
                 for (int j = 0; j < VEC; ++j)
                     if (best[j] == r * S + s) sum[j] += g[j];
+            }
+        }
+        if (mask) {
+            float mk[VEC];
+            ldv<VEC>(mask + i, mk);
+#pragma unroll
+            for (int j = 0; j < VEC; ++j)
+                if (!(mk[j] > 0.f)) sum[j] = 0.f;
+        }
+        if (acc) {
+            float d[VEC];
+            ldv<VEC>(dx + i, d);
+#pragma unroll
+            for (int j = 0; j < VEC; ++j) sum[j] = d[j] + sum[j];
+        }
+        stv<VEC>(dx + i, sum);
+    }
+}
+
+// max-pool backward as a gather with the taps the forward pass recorded:
+// each input element sums dy over the windows whose first maximum it is, in
+// window order, reading one byte per candidate window instead of the window.
+template <int VEC>
+__global__ void maxpool_bwd_arg_kernel(const uint8_t* __restrict__ arg,
+                                       const float* __restrict__ dy, float* __restrict__ dx,
+                                       int N, int H, int W, int C, int R, int S, int st, int pad,
+                                       int P, int Q, int acc, const float* __restrict__ mask) {
+    const size_t total = (size_t)N * H * W * C;
+    for (size_t i = ((size_t)blockIdx.x * blockDim.x + threadIdx.x) * VEC; i < total;
+         i += (size_t)gridDim.x * blockDim.x * VEC) {
+        const int c = (int)(i % C);
+        size_t t = i / C;
+        const int w0 = (int)(t % W); t /= W;
+        const int h0 = (int)(t % H);
+        const int n = (int)(t / H);
+        float sum[VEC];
+#pragma unroll
+        for (int j = 0; j < VEC; ++j) sum[j] = 0.f;
+        for (int r = 0; r < R; ++r) {
+            const int tp = h0 + pad - r;
+            if (tp < 0 || tp % st) continue;
+            const int p = tp / st;
+            if (p >= P) continue;
+            for (int s = 0; s < S; ++s) {
+                const int tq = w0 + pad - s;
+                if (tq < 0 || tq % st) continue;
+                const int q = tq / st;
+                if (q >= Q) continue;
+                const size_t o = (((size_t)n * P + p) * Q + q) * C + c;
+                float g[VEC];
+                ldv<VEC>(dy + o, g);
+#pragma unroll
+                for (int j = 0; j < VEC; ++j)
+                    if (arg[o + j] == r * S + s) sum[j] += g[j];
             }
         }
         if (mask) {
@@ -746,22 +809,27 @@ hipError_t launch_copy_or_acc(const float* v, float* out, size_t n, int accumula
 }
 
 hipError_t launch_maxpool_fwd(const float* x, float* y, int N, int H, int W, int C, int R, int S,
-                              int st, int pad, int P, int Q, hipStream_t s, uint16_t* y16) {
+                              int st, int pad, int P, int Q, hipStream_t s, uint16_t* y16,
+                              uint8_t* arg) {
     size_t n = (size_t)N * P * Q * C;
     if (C % 4 == 0 && aligned16({x, y}) && ((uintptr_t)y16 & 7) == 0)
         hipLaunchKernelGGL(maxpool_fwd_kernel<4>, dim3(ew_blocks(n / 4)), dim3(EW_THREADS), 0, s, x,
-                           y, N, H, W, C, R, S, st, pad, P, Q, y16);
+                           y, N, H, W, C, R, S, st, pad, P, Q, y16, arg);
     else
         hipLaunchKernelGGL(maxpool_fwd_kernel<1>, dim3(ew_blocks(n)), dim3(EW_THREADS), 0, s, x, y,
-                           N, H, W, C, R, S, st, pad, P, Q, y16);
+                           N, H, W, C, R, S, st, pad, P, Q, y16, arg);
     return hipGetLastError();
+}
+
+bool maxpool_tiled(int H, int W, int R, int S, int st, int pad, int P, int Q) {
+    return R == S && R == st && pad == 0 && P * st == H && Q * st == W;
 }
 
 hipError_t launch_maxpool_bwd(const float* x, const float* dy, float* dx, int N, int H, int W,
                               int C, int R, int S, int st, int pad, int P, int Q, int accumulate,
-                              const float* mask, hipStream_t s) {
+                              const float* mask, hipStream_t s, const uint8_t* arg) {
     const bool v4 = C % 4 == 0 && aligned16({x, dy, dx, mask});
-    if (R == S && R == st && pad == 0 && P * st == H && Q * st == W) {
+    if (maxpool_tiled(H, W, R, S, st, pad, P, Q)) {
         size_t n = (size_t)N * P * Q * C;
         const dim3 g(ew_blocks(v4 ? n / 4 : n)), b(EW_THREADS);
         if (R == 2 && v4)
@@ -779,7 +847,13 @@ hipError_t launch_maxpool_bwd(const float* x, const float* dy, float* dx, int N,
         return hipGetLastError();
     }
     size_t n = (size_t)N * H * W * C;
-    if (v4)
+    if (arg && v4)
+        hipLaunchKernelGGL(maxpool_bwd_arg_kernel<4>, dim3(ew_blocks(n / 4)), dim3(EW_THREADS), 0, s,
+                           arg, dy, dx, N, H, W, C, R, S, st, pad, P, Q, accumulate, mask);
+    else if (arg)
+        hipLaunchKernelGGL(maxpool_bwd_arg_kernel<1>, dim3(ew_blocks(n)), dim3(EW_THREADS), 0, s,
+                           arg, dy, dx, N, H, W, C, R, S, st, pad, P, Q, accumulate, mask);
+    else if (v4)
         hipLaunchKernelGGL(maxpool_bwd_kernel<4>, dim3(ew_blocks(n / 4)), dim3(EW_THREADS), 0, s, x,
                            dy, dx, N, H, W, C, R, S, st, pad, P, Q, accumulate, mask);
     else

@@ -80,6 +80,9 @@ struct Node {
     // the BN backward that produces it, else cast before the weight gradient)
     uint16_t* g16 = nullptr;
     bool g16_ready = false;
+    // max-pool with overlapping windows: the tap of each window's first
+    // maximum, recorded by the forward pass for the backward pass
+    uint8_t* arg = nullptr;
 };
 
 size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
@@ -412,6 +415,12 @@ int build_stage(hp_stage* st, const hp_layer* layers, int n_layers) {
         }
         int rc = dev_alloc(st, &nd.g, nd.out_elems);
         if (rc) return rc;
+        if (nd.L.kind == HP_MAXPOOL && nd.L.R * nd.L.S < 256 &&
+            !maxpool_tiled(nd.inH, nd.inW, nd.L.R, nd.L.S, nd.L.stride, nd.L.pad, nd.H, nd.W)) {
+            float* q = nullptr;
+            if ((rc = dev_alloc(st, &q, (nd.out_elems + 3) / 4))) return rc;
+            nd.arg = reinterpret_cast<uint8_t*>(q);
+        }
         if (nd.L.kind == HP_BN) {
             if ((rc = dev_alloc(st, &nd.mean, nd.C))) return rc;
             if ((rc = dev_alloc(st, &nd.invstd, nd.C))) return rc;
@@ -676,7 +685,7 @@ extern "C" int hp_stage_forward(hp_stage* st, const float* w, const float* x, fl
                 break;
             case HP_MAXPOOL:
                 e = launch_maxpool_fwd(in, nd.y, B, nd.inH, nd.inW, nd.inC, L.R, L.S, L.stride,
-                                       L.pad, nd.H, nd.W, s, out16);
+                                       L.pad, nd.H, nd.W, s, out16, nd.arg);
                 break;
             case HP_BN:
                 e = launch_bn_fwd(in, (long)B * nd.H * nd.W, nd.C, w + nd.w_off, w + nd.b_off,
@@ -846,7 +855,7 @@ extern "C" int hp_stage_backward(hp_stage* st, const float* w, const float* dy, 
                 const float* mask = nd.mask_into >= 0 ? st->nodes[L.in0].y : nullptr;
                 if (dest(tgt, &d, &acc))
                     e = launch_maxpool_bwd(in, gin, d, B, nd.inH, nd.inW, nd.inC, L.R, L.S,
-                                           L.stride, L.pad, nd.H, nd.W, acc, mask, s);
+                                           L.stride, L.pad, nd.H, nd.W, acc, mask, s, nd.arg);
                 break;
             }
             case HP_BN: {

@@ -98,14 +98,21 @@ hipError_t launch_add_fwd(const float* a, const float* b, float* y, size_t n, in
 // out = v (accumulate = 0) or out += v
 hipError_t launch_copy_or_acc(const float* v, float* out, size_t n, int accumulate,
                               hipStream_t s);
+// arg (optional, one byte per output element, R * S < 256): records the
+// window tap of every first maximum for the backward pass
 hipError_t launch_maxpool_fwd(const float* x, float* y, int N, int H, int W, int C, int R,
                               int S, int st, int pad, int P, int Q, hipStream_t s,
-                              uint16_t* y16 = nullptr);
+                              uint16_t* y16 = nullptr, uint8_t* arg = nullptr);
+// windows that tile the input exactly (the backward needs no recorded taps)
+bool maxpool_tiled(int H, int W, int R, int S, int st, int pad, int P, int Q);
 // mask (optional, layout of dx): the pooled input is a ReLU output; dx is
-// zeroed where mask <= 0 (ReLU backward fused)
+// zeroed where mask <= 0 (ReLU backward fused).  arg (optional): the taps the
+// forward pass recorded, used for overlapping windows instead of recomputing
+// each window's maximum from x.
 hipError_t launch_maxpool_bwd(const float* x, const float* dy, float* dx, int N, int H, int W,
                               int C, int R, int S, int st, int pad, int P, int Q,
-                              int accumulate, const float* mask, hipStream_t s);
+                              int accumulate, const float* mask, hipStream_t s,
+                              const uint8_t* arg = nullptr);
 hipError_t launch_gap_fwd(const float* x, float* y, int N, int HW, int C, hipStream_t s);
 hipError_t launch_gap_bwd(const float* dy, float* dx, int N, int HW, int C, int accumulate,
                           hipStream_t s);
