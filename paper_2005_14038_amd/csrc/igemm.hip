@@ -1866,8 +1866,8 @@ struct KernelRef {
 // bf16 rounded while staging from fp32 (1 or 4), bf16 operands in memory
 // (general gather), bf16 operands in memory, both k-major (FWD and stride-1
 // DGRAD with a reduction channel count that is a multiple of the k tile), and
-// fp32 vector width 4 with the wide epilogue (short reductions).
-enum { KF_F32_1, KF_F32_4, KF_BF_1, KF_BF_4, KF_H16, KF_H16K, KF_F32_4W };
+// fp32 (vector width 4 or 1) with the wide epilogue.
+enum { KF_F32_1, KF_F32_4, KF_BF_1, KF_BF_4, KF_H16, KF_H16K, KF_F32_4W, KF_F32_1W };
 
 template <int OP, int CFG, int KF>
 KernelRef kref() {
@@ -1885,9 +1885,10 @@ KernelRef kref() {
     else if constexpr (KF == KF_BF_1 || KF == KF_BF_4)
         return {reinterpret_cast<const void*>(
                     &igemm_bf16_kernel<OP, c.bm, c.bn, c.wm, c.wn, KF == KF_BF_4 ? 4 : 1>), nt};
-    else if constexpr (KF == KF_F32_4W)
+    else if constexpr (KF == KF_F32_4W || KF == KF_F32_1W)
         return {reinterpret_cast<const void*>(
-                    &igemm_kernel<OP, c.bm, c.bn, c.bk, c.wm, c.wn, 4, true>), nt};
+                    &igemm_kernel<OP, c.bm, c.bn, c.bk, c.wm, c.wn, KF == KF_F32_4W ? 4 : 1, true>),
+                nt};
     else
         return {reinterpret_cast<const void*>(
                     &igemm_kernel<OP, c.bm, c.bn, c.bk, c.wm, c.wn, KF == KF_F32_4 ? 4 : 1>), nt};
@@ -1913,6 +1914,7 @@ KernelRef kref_op(int cfg, int kf) {
         case KF_H16: return kref_cfg<OP, KF_H16>(cfg);
         case KF_H16K: return kref_cfg<OP, KF_H16K>(cfg);
         case KF_F32_4W: return kref_cfg<OP, KF_F32_4W>(cfg);
+        case KF_F32_1W: return kref_cfg<OP, KF_F32_1W>(cfg);
         default: return kref_cfg<OP, KF_F32_1>(cfg);
     }
 }
@@ -1977,9 +1979,9 @@ GemmPlan plan_gemm(int op, const ConvGeo& g, int bf16, int num_cus, int bias_col
     // written outweigh occupancy).  Long reductions (the weight gradients of
     // large images) and larger tile counts keep the narrow kernel: its
     // occupancy gives them more resident workgroups and reduction chunks.
-    if (!bf16 && v4) {
+    if (!bf16) {
         int occ_n = 0;
-        const KernelRef kn = kernel_for(op, p.cfg, KF_F32_4);
+        const KernelRef kn = kernel_for(op, p.cfg, v4 ? KF_F32_4 : KF_F32_1);
         if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ_n, kn.fn, kn.nt, 0) != hipSuccess ||
             occ_n < 1)
             occ_n = 1;
@@ -2002,7 +2004,7 @@ GemmPlan plan_gemm(int op, const ConvGeo& g, int bf16, int num_cus, int bias_col
                                      : p.h16 ? KF_H16
                                              : bf16 ? (v4 ? KF_BF_4 : KF_BF_1)
                                                     : (v4 ? (p.wide ? KF_F32_4W : KF_F32_4)
-                                                          : KF_F32_1));
+                                                          : (p.wide ? KF_F32_1W : KF_F32_1)));
     int occ = 0;
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, kr.fn, kr.nt, 0) != hipSuccess || occ < 1)
         occ = 1;
@@ -2091,7 +2093,8 @@ hipError_t launch_gemm(const GemmPlan& plan, const ConvGeo& g, const float* a, c
     const int kf = h16k ? KF_H16K
                         : h16 ? KF_H16
                               : plan.bf16 ? (v4 ? KF_BF_4 : KF_BF_1)
-                                          : (v4 ? (plan.wide ? KF_F32_4W : KF_F32_4) : KF_F32_1);
+                                          : (v4 ? (plan.wide ? KF_F32_4W : KF_F32_4)
+                                                : (plan.wide ? KF_F32_1W : KF_F32_1));
     KernelRef kr = kernel_for(plan.op, plan.cfg, kf);
     void* kargs[] = {&k};
     hipError_t e = hipLaunchKernel(kr.fn, dim3(plan.nwg), dim3(kr.nt), kargs, 0, s);
