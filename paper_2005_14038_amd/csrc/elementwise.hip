@@ -682,6 +682,33 @@ __global__ void cast_bf16_kernel(const float* __restrict__ src, uint16_t* __rest
         dst[i] = (uint16_t)bf16_bits(src[i]);
 }
 
+// Channel padding of a conv whose input channel count is not a multiple of
+// the contraction's vector width: dst[r][c] = src[r][c] for c < C, 0 up to Cp
+// (fp32, or bf16 rounded to nearest even); and the reverse for the weight
+// gradient computed on the padded geometry.
+__global__ void pad_channels_kernel(const float* __restrict__ src, float* __restrict__ dst,
+                                    uint16_t* __restrict__ dst16, size_t rows, int C, int Cp) {
+    const size_t n = rows * (size_t)Cp;
+    for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+         i += (size_t)gridDim.x * blockDim.x) {
+        const size_t r = i / Cp;
+        const int c = (int)(i - r * Cp);
+        const float v = c < C ? src[r * C + c] : 0.f;
+        if (dst16) dst16[i] = (uint16_t)bf16_bits(v);
+        else dst[i] = v;
+    }
+}
+
+__global__ void unpad_channels_kernel(const float* __restrict__ src, float* __restrict__ dst,
+                                      size_t rows, int C, int Cp) {
+    const size_t n = rows * (size_t)C;
+    for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n;
+         i += (size_t)gridDim.x * blockDim.x) {
+        const size_t r = i / C;
+        dst[i] = src[r * Cp + (i - r * C)];
+    }
+}
+
 // Transposed bf16 copies of conv/FC weights for the data gradient:
 // dst[off + (c * RS + rs) * K + k] = bf16(src[off + (k * RS + rs) * C + c]) for
 // every layer of the table.  A workgroup transposes one 64 (k) x 64 (c) tile
@@ -994,6 +1021,20 @@ hipError_t launch_cast_bf16(const float* src, uint16_t* dst, size_t n, hipStream
     const int vec = ((((uintptr_t)src) & 15) | (((uintptr_t)dst) & 7)) == 0;
     hipLaunchKernelGGL(cast_bf16_kernel, dim3(ew_blocks(vec ? (n + 3) / 4 : n)), dim3(EW_THREADS), 0,
                        s, src, dst, n, vec);
+    return hipGetLastError();
+}
+
+hipError_t launch_pad_channels(const float* src, float* dst, uint16_t* dst16, size_t rows, int C,
+                               int Cp, hipStream_t s) {
+    hipLaunchKernelGGL(pad_channels_kernel, dim3(ew_blocks(rows * Cp)), dim3(EW_THREADS), 0, s, src,
+                       dst, dst16, rows, C, Cp);
+    return hipGetLastError();
+}
+
+hipError_t launch_unpad_channels(const float* src, float* dst, size_t rows, int C, int Cp,
+                                 hipStream_t s) {
+    hipLaunchKernelGGL(unpad_channels_kernel, dim3(ew_blocks(rows * C)), dim3(EW_THREADS), 0, s, src,
+                       dst, rows, C, Cp);
     return hipGetLastError();
 }
 

@@ -83,6 +83,17 @@ struct Node {
     // max-pool with overlapping windows: the tap of each window's first
     // maximum, recorded by the forward pass for the backward pass
     uint8_t* arg = nullptr;
+    // conv whose input channel count is not a multiple of the contraction's
+    // vector width (the image layer, C = 3): forward and weight gradient run
+    // on copies padded with zero channels to padC (input, weights; bf16 mode:
+    // their bf16 copies), the padded weight gradient is compacted into grad
+    int padC = 0;
+    ConvGeo geo_p{};
+    float* xp = nullptr;
+    float* wp = nullptr;
+    float* dwp = nullptr;
+    uint16_t* xp16 = nullptr;
+    uint16_t* wp16 = nullptr;
 };
 
 size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
@@ -281,11 +292,20 @@ int build_stage(hp_stage* st, const hp_layer* layers, int n_layers) {
                 off += (size_t)L.K * R * S * inC;
                 if (L.bias) { nd.b_off = off; off += L.K; }
                 nd.p_cnt = off - nd.p_off;
-                nd.fwd = plan_gemm(OP_FWD, nd.geo, st->dtype, cus);
+                {
+                    const int vw = st->dtype == HP_BF16 ? 8 : 4;
+                    if (L.kind == HP_CONV && inC % vw != 0 && L.K % vw == 0) {
+                        nd.padC = (inC + vw - 1) / vw * vw;
+                        nd.geo_p = nd.geo;
+                        nd.geo_p.C = nd.padC;
+                    }
+                }
+                const ConvGeo& gfw = nd.padC ? nd.geo_p : nd.geo;
+                nd.fwd = plan_gemm(OP_FWD, gfw, st->dtype, cus);
                 nd.dgrad = plan_gemm(OP_DGRAD, nd.geo, st->dtype, cus);
                 // fp32: the bias gradient rides along as a column of ones in the weight
                 // gradient; bf16 would round dy there, so it is a separate fp32 sum
-                nd.wgrad = plan_gemm(OP_WGRAD, nd.geo, st->dtype, cus,
+                nd.wgrad = plan_gemm(OP_WGRAD, gfw, st->dtype, cus,
                                      (L.bias && st->dtype == HP_FP32) ? 1 : 0);
                 nd.bias_in_wgrad = nd.wgrad.bias_col != 0;
                 // a small weight gradient (under 20 GFLOP) leaves most of the GPU
@@ -415,6 +435,17 @@ int build_stage(hp_stage* st, const hp_layer* layers, int n_layers) {
         }
         int rc = dev_alloc(st, &nd.g, nd.out_elems);
         if (rc) return rc;
+        if (nd.padC) {
+            const size_t xn = (size_t)st->batch * nd.inH * nd.inW * nd.padC;
+            const size_t wn = (size_t)nd.L.K * nd.L.R * nd.L.S * nd.padC;
+            if (st->dtype == HP_BF16) {
+                if ((rc = dev_alloc16(st, &nd.xp16, xn)) || (rc = dev_alloc16(st, &nd.wp16, wn)))
+                    return rc;
+            } else if ((rc = dev_alloc(st, &nd.xp, xn)) || (rc = dev_alloc(st, &nd.wp, wn))) {
+                return rc;
+            }
+            if ((rc = dev_alloc(st, &nd.dwp, wn))) return rc;
+        }
         if (nd.L.kind == HP_MAXPOOL && nd.L.R * nd.L.S < 256 &&
             !maxpool_tiled(nd.inH, nd.inW, nd.L.R, nd.L.S, nd.L.stride, nd.L.pad, nd.H, nd.W)) {
             float* q = nullptr;
@@ -644,7 +675,7 @@ extern "C" int hp_stage_forward(hp_stage* st, const float* w, const float* x, fl
         hipError_t e = hipSuccess;
         StageTimer& tm = st->timer;
         const uint16_t* in16 = nullptr;
-        if ((L.kind == HP_CONV || L.kind == HP_FC) && nd.fwd.h16 && st->w16) {
+        if ((L.kind == HP_CONV || L.kind == HP_FC) && nd.fwd.h16 && st->w16 && !nd.padC) {
             // bf16 copy of the input value, made by its first contraction consumer
             in16 = L.in0 < 0 ? st->x16 : st->nodes[L.in0].y16;
             bool& ready = L.in0 < 0 ? st->x16_ready : st->nodes[L.in0].y16_ready;
@@ -676,6 +707,20 @@ extern "C" int hp_stage_forward(hp_stage* st, const float* w, const float* x, fl
                 Epilogue ep;
                 ep.flags = (L.bias ? EPI_BIAS : 0) | (nd.fuses_relu ? EPI_RELU : 0);
                 ep.bias = L.bias ? w + nd.b_off : nullptr;
+                if (nd.padC) {
+                    // zero-padded copies of the input and the weights, then the
+                    // contraction on the padded geometry
+                    const int C0 = nd.geo.C, Cp = nd.padC;
+                    const size_t xr = (size_t)B * nd.inH * nd.inW;
+                    const size_t wr = (size_t)L.K * L.R * L.S;
+                    e = launch_pad_channels(in, nd.xp, nd.xp16, xr, C0, Cp, s);
+                    if (e == hipSuccess)
+                        e = launch_pad_channels(w + nd.w_off, nd.wp, nd.wp16, wr, C0, Cp, s);
+                    if (e == hipSuccess)
+                        e = launch_gemm(nd.fwd, nd.geo_p, nd.xp ? nd.xp : in, nd.wp ? nd.wp : w,
+                                        nd.y, ep, st->ws, s, nd.xp16, nd.wp16);
+                    break;
+                }
                 e = launch_gemm(nd.fwd, nd.geo, in, w + nd.w_off, nd.y, ep, st->ws, s, in16,
                                 in16 ? st->w16 + nd.w_off : nullptr);
                 break;
@@ -795,7 +840,7 @@ extern "C" int hp_stage_backward(hp_stage* st, const float* w, const float* dy, 
                 const uint16_t* in16 = nullptr;
                 const uint16_t* g16 = nullptr;
                 if (nd.fwd.h16 && st->w16) {
-                    in16 = L.in0 < 0 ? st->x16 : st->nodes[L.in0].y16;
+                    in16 = nd.padC ? nd.xp16 : L.in0 < 0 ? st->x16 : st->nodes[L.in0].y16;
                     if (!nd.g16_ready) {
                         tm.begin(1, s);
                         e = launch_cast_bf16(gin, nd.g16, nd.out_elems, s);
@@ -811,9 +856,17 @@ extern "C" int hp_stage_backward(hp_stage* st, const float* w, const float* dy, 
                 tm.begin(0, sd);
                 Epilogue wep;                     // bias gradient = appended column
                 wep.bias_out = nd.bias_in_wgrad ? grad + nd.b_off : nullptr;
-                if (e == hipSuccess)
+                if (e == hipSuccess && nd.padC) {
+                    // on the padded geometry, then compacted into grad
+                    e = launch_gemm(nd.wgrad, nd.geo_p, nd.xp ? nd.xp : in, gin, nd.dwp, wep, wsw,
+                                    sd, in16, g16);
+                    if (e == hipSuccess)
+                        e = launch_unpad_channels(nd.dwp, grad + nd.w_off,
+                                                  (size_t)L.K * L.R * L.S, nd.geo.C, nd.padC, sd);
+                } else if (e == hipSuccess) {
                     e = launch_gemm(nd.wgrad, nd.geo, in, gin, grad + nd.w_off, wep, wsw, sd,
                                     in16, g16);
+                }
                 tm.end(sd);
                 if (e == hipSuccess && L.bias && !nd.bias_in_wgrad) {
                     tm.begin(1, sd);

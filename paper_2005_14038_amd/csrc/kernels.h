@@ -70,6 +70,14 @@ hipError_t launch_gemm(const GemmPlan& plan, const ConvGeo& g, const float* a,
 // dst[i] = bf16(src[i]) (round to nearest even), n elements
 hipError_t launch_cast_bf16(const float* src, uint16_t* dst, size_t n, hipStream_t s);
 
+// Channel padding: dst[r][c] = src[r][c] (c < C), 0 (C <= c < Cp), rows x Cp,
+// into dst (fp32) or, when dst16 is given, dst16 (bf16, nearest even).
+hipError_t launch_pad_channels(const float* src, float* dst, uint16_t* dst16, size_t rows, int C,
+                               int Cp, hipStream_t s);
+// The reverse: dst[r][c] = src[r][c] for c < C (src rows of Cp).
+hipError_t launch_unpad_channels(const float* src, float* dst, size_t rows, int C, int Cp,
+                                 hipStream_t s);
+
 // Transposed bf16 weight copies for the data gradient on k-major operands:
 // for each table layer, dst[off + (c*RS + rs)*K + k] = bf16(src[off + (k*RS + rs)*C + c]).
 // tile0 = the layer's first WT_TILE x WT_TILE tile number (prefix sums of wt_tiles, in
