@@ -995,6 +995,24 @@ hipError_t launch_bn_fwd(const float* x, long M, int C, const float* gamma, cons
     return hipGetLastError();
 }
 
+hipError_t launch_bn_fwd_partials(const float* x, long M, int C, const float* gamma,
+                                  const float* beta, float eps, float* y, float* mean,
+                                  float* invstd, int relu, const float* part0, const float* part1,
+                                  int nb, long rb, hipStream_t s, uint16_t* y16) {
+    ColPlan p{};
+    p.nb = nb;
+    p.rb = rb;
+    launch_final<FIN_STATS>(p, part0, part1, M, C, eps, mean, invstd, s);
+    size_t n = (size_t)M * C;
+    if (vec4_ok(C, {x, y, gamma, beta, mean, invstd}) && ((uintptr_t)y16 & 7) == 0)
+        hipLaunchKernelGGL(bn_apply_kernel<4>, dim3(ew_blocks(n / 4)), dim3(EW_THREADS), 0, s, x, M,
+                           C, gamma, beta, mean, invstd, y, relu, y16);
+    else
+        hipLaunchKernelGGL(bn_apply_kernel<1>, dim3(ew_blocks(n)), dim3(EW_THREADS), 0, s, x, M, C,
+                           gamma, beta, mean, invstd, y, relu, y16);
+    return hipGetLastError();
+}
+
 hipError_t launch_bn_bwd(const float* x, const float* dy, const float* relu_y, long M, int C,
                          const float* gamma, const float* mean, const float* invstd, float* dx,
                          float* dgamma, float* dbeta, int accumulate, float* ws, hipStream_t s,

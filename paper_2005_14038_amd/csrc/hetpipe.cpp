@@ -87,6 +87,12 @@ struct Node {
     // vector width (the image layer, C = 3): forward and weight gradient run
     // on copies padded with zero channels to padC (input, weights; bf16 mode:
     // their bf16 copies), the padded weight gradient is compacted into grad
+    // conv whose only consumer is a batch norm: its forward contraction writes
+    // per-tile column statistics (mean, squared deviations; stats_nb row
+    // tiles of stats_rb rows) and the batch norm merges them
+    float* stats = nullptr;
+    int stats_nb = 0;
+    long stats_rb = 0;
     int padC = 0;
     ConvGeo geo_p{};
     float* xp = nullptr;
@@ -435,6 +441,17 @@ int build_stage(hp_stage* st, const hp_layer* layers, int n_layers) {
         }
         int rc = dev_alloc(st, &nd.g, nd.out_elems);
         if (rc) return rc;
+        if (nd.L.kind == HP_CONV && nd.consumers == 1) {
+            int cons = -1;
+            for (int c = i + 1; c < n_layers && cons < 0; ++c)
+                if (st->nodes[c].L.in0 == i) cons = c;
+            if (cons >= 0 && st->nodes[cons].L.kind == HP_BN &&
+                plan_stats(nd.fwd, nd.L.bias ? EPI_BIAS : 0)) {
+                nd.stats_rb = nd.fwd.bm;
+                nd.stats_nb = (int)((nd.fwd.M + nd.fwd.bm - 1) / nd.fwd.bm);
+                if ((rc = dev_alloc(st, &nd.stats, 2 * (size_t)nd.stats_nb * nd.C))) return rc;
+            }
+        }
         if (nd.padC) {
             const size_t xn = (size_t)st->batch * nd.inH * nd.inW * nd.padC;
             const size_t wn = (size_t)nd.L.K * nd.L.R * nd.L.S * nd.padC;
@@ -707,6 +724,7 @@ extern "C" int hp_stage_forward(hp_stage* st, const float* w, const float* x, fl
                 Epilogue ep;
                 ep.flags = (L.bias ? EPI_BIAS : 0) | (nd.fuses_relu ? EPI_RELU : 0);
                 ep.bias = L.bias ? w + nd.b_off : nullptr;
+                ep.stats = nd.stats;
                 if (nd.padC) {
                     // zero-padded copies of the input and the weights, then the
                     // contraction on the padded geometry
@@ -732,11 +750,20 @@ extern "C" int hp_stage_forward(hp_stage* st, const float* w, const float* x, fl
                 e = launch_maxpool_fwd(in, nd.y, B, nd.inH, nd.inW, nd.inC, L.R, L.S, L.stride,
                                        L.pad, nd.H, nd.W, s, out16, nd.arg);
                 break;
-            case HP_BN:
-                e = launch_bn_fwd(in, (long)B * nd.H * nd.W, nd.C, w + nd.w_off, w + nd.b_off,
-                                  L.eps, nd.y, nd.mean, nd.invstd, nd.fuses_relu ? 1 : 0, st->ws, s,
-                                  out16);
+            case HP_BN: {
+                const Node* pc = L.in0 >= 0 ? &st->nodes[L.in0] : nullptr;
+                if (pc && pc->stats)       // statistics from the producing contraction
+                    e = launch_bn_fwd_partials(in, (long)B * nd.H * nd.W, nd.C, w + nd.w_off,
+                                               w + nd.b_off, L.eps, nd.y, nd.mean, nd.invstd,
+                                               nd.fuses_relu ? 1 : 0, pc->stats,
+                                               pc->stats + (size_t)pc->stats_nb * nd.C,
+                                               pc->stats_nb, pc->stats_rb, s, out16);
+                else
+                    e = launch_bn_fwd(in, (long)B * nd.H * nd.W, nd.C, w + nd.w_off, w + nd.b_off,
+                                      L.eps, nd.y, nd.mean, nd.invstd, nd.fuses_relu ? 1 : 0,
+                                      st->ws, s, out16);
                 break;
+            }
             case HP_ADD: {
                 const float* in1 = L.in1 < 0 ? x : st->nodes[L.in1].y;
                 e = launch_add_fwd(in, in1, nd.y, nd.out_elems, nd.fuses_relu ? 1 : 0, s, out16);

@@ -72,6 +72,7 @@ struct KArgs {
     int splits;       // every remaining tile is cut into `splits` reduction chunks
     int kchunk;       // reduction length of a chunk (multiple of the K tile)
     float* ws;        // partial tiles of the cut tiles: [tile - tfull][split][BM * BN]
+    float* stats;     // optional column statistics per row tile (see Epilogue)
     int epi;
     const unsigned short* a16;   // bf16 copies of a and b (16-bit operand kernel only)
     const unsigned short* b16;
@@ -335,6 +336,65 @@ __device__ __forceinline__ void store_tile_wide(const KArgs& args, const Work& w
     }
 }
 
+// Column statistics of a whole tile for a following batch norm: the mean of
+// each column over the tile's rows below M and the sum of squared deviations
+// from it, two passes over the accumulators (values after the bias), lanes l
+// and l + 32 combined by a shuffle, the waves along M through LDS in a fixed
+// order.  Every thread of the workgroup takes part (barriers); lds holds at
+// least (BM / WM + 1) * BN floats.
+template <int BM, int BN, int TM, int TN>
+__device__ __forceinline__ void tile_stats(const KArgs& args, const Work& w,
+                                           const floatx16 (&acc)[TM][TN], int wm, int wn,
+                                           int lane, float* lds) {
+    constexpr int WAVES_M = BM / (32 * TM);
+    const int lr = lane & 31, lk = lane >> 5;
+    const int wave_m = wm / (32 * TM);
+    const long rows = min((long)BM, args.M - w.m0);
+    float* part = lds;                   // [WAVES_M][BN]
+    float* mean = lds + WAVES_M * BN;    // [BN]
+    const int t = threadIdx.x;
+    const int nthreads = blockDim.x;
+    float bias[TN];
+#pragma unroll
+    for (int j = 0; j < TN; ++j) {
+        const long col = w.n0 + wn + 32 * j + lr;
+        bias[j] = ((args.epi & EPI_BIAS) && col < args.Ncols) ? args.bias[col] : 0.f;
+    }
+    for (int pass = 0; pass < 2; ++pass) {
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+            const float mu = pass ? mean[wn + 32 * j + lr] : 0.f;
+            float sum = 0.f;
+#pragma unroll
+            for (int i = 0; i < TM; ++i)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) {
+                    const int r = wm + 32 * i + 8 * (v >> 2) + 4 * lk + (v & 3);
+                    if (r < rows) {
+                        const float d = acc[i][j][v] + bias[j] - mu;
+                        sum += pass ? d * d : d;
+                    }
+                }
+            sum += __shfl_xor(sum, 32);
+            if (lk == 0) part[wave_m * BN + wn + 32 * j + lr] = sum;
+        }
+        __syncthreads();
+        for (int c = t; c < BN; c += nthreads) {
+            float s = 0.f;
+            for (int m = 0; m < WAVES_M; ++m) s += part[m * BN + c];
+            const long col = w.n0 + c;
+            if (pass == 0) {
+                mean[c] = rows > 0 ? s / (float)rows : 0.f;
+            } else if (col < args.Ncols) {
+                const long tm = w.m0 / BM;
+                args.stats[tm * args.Ncols + col] = mean[c];
+                args.stats[((long)args.tiles_m + tm) * args.Ncols + col] = s;
+            }
+        }
+        __syncthreads();
+    }
+}
+
 // Writes a wave's tile: the wide path when the kernel was built with it
 // (WIDE) and its conditions hold (uniform).  The wide path costs registers,
 // which the fp32 kernels on long reductions, where the epilogue is a small
@@ -342,8 +402,13 @@ __device__ __forceinline__ void store_tile_wide(const KArgs& args, const Work& w
 template <int BM, int BN, int TM, int TN, bool WIDE = true>
 __device__ __forceinline__ void write_tile(const KArgs& args, const Work& w,
                                            const floatx16 (&acc)[TM][TN], int wm, int wn,
-                                           int lane, float* slot) {
+                                           int lane, float* slot, float* lds_all) {
     if constexpr (WIDE) {
+        // column statistics of whole tiles (uniform per workgroup: it is either
+        // whole or cut); the LDS slots are reused afterwards.  Built only into
+        // the wide kernels, whose register budget already allows it.
+        if (args.stats && !w.partial)
+            tile_stats<BM, BN, TM, TN>(args, w, acc, wm, wn, lane, lds_all);
         auto a16 = [](const void* p) { return (((uintptr_t)p) & 15) == 0; };
         const int epi = args.epi;
         const bool wide = !(epi & EPI_BIASCOL) && (args.Ncols & 3) == 0 && a16(args.out) &&
@@ -688,7 +753,8 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_kernel(KA
 
     static_assert(sizeof(smem) >= (NT / 64) * SLOT_FLOATS * sizeof(float), "epilogue slots");
     write_tile<BM, BN, TM, TN, WIDE>(args, wk, acc, wm, wn, lane,
-                               reinterpret_cast<float*>(smem) + wave * SLOT_FLOATS);
+                                     reinterpret_cast<float*>(smem) + wave * SLOT_FLOATS,
+                                     reinterpret_cast<float*>(smem));
 }
 
 // ---- bf16 kernel ------------------------------------------------------------
@@ -1043,7 +1109,8 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_bf16_kern
     }
     static_assert(sizeof(smem) >= (NT / 64) * SLOT_FLOATS * sizeof(float), "epilogue slots");
     write_tile<BM, BN, TM, TN>(args, wk, acc, wm, wn, lane,
-                               reinterpret_cast<float*>(smem) + wave * SLOT_FLOATS);
+                               reinterpret_cast<float*>(smem) + wave * SLOT_FLOATS,
+                               reinterpret_cast<float*>(smem));
 }
 
 
@@ -1383,7 +1450,8 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_h16_kerne
     }
     static_assert(sizeof(smem) >= (NT / 64) * SLOT_FLOATS * sizeof(float), "epilogue slots");
     write_tile<BM, BN, TM, TN>(args, wk, acc, wm, wn, lane,
-                               reinterpret_cast<float*>(smem) + wave * SLOT_FLOATS);
+                               reinterpret_cast<float*>(smem) + wave * SLOT_FLOATS,
+                               reinterpret_cast<float*>(smem));
 }
 
 // ---- bf16 kernel on k-major bf16 operands -------------------------------------
@@ -1583,7 +1651,8 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_h16k_kern
     }
     static_assert(sizeof(smem) >= (NT / 64) * SLOT_FLOATS * sizeof(float), "epilogue slots");
     write_tile<BM, BN, TM, TN>(args, wk, acc, wm, wn, lane,
-                               reinterpret_cast<float*>(smem) + wave * SLOT_FLOATS);
+                               reinterpret_cast<float*>(smem) + wave * SLOT_FLOATS,
+                               reinterpret_cast<float*>(smem));
 }
 
 
@@ -1761,7 +1830,8 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_h16w_kern
     }
     static_assert(sizeof(smem) >= (NT / 64) * SLOT_FLOATS * sizeof(float), "epilogue slots");
     write_tile<BM, BN, TM, TN>(args, wk, acc, wm, wn, lane,
-                               reinterpret_cast<float*>(smem) + wave * SLOT_FLOATS);
+                               reinterpret_cast<float*>(smem) + wave * SLOT_FLOATS,
+                               reinterpret_cast<float*>(smem));
 }
 
 
@@ -1854,6 +1924,87 @@ __global__ void __launch_bounds__(256) igemm_cut_reduce_kernel(KArgs args, int B
             if (epi & EPI_ACCUM) v += prev[j];
             *out_ptr(args.out, args.bias_out, row, col, args.Ncols, epi) = v;
         }
+    }
+}
+
+// Reduction of the cut tiles with column statistics (a following batch norm):
+// one workgroup per cut tile; thread = 4 consecutive columns x every RG-th
+// row.  Each output is the sum of its split partials in split order plus the
+// bias; the tile's column means and sums of squared deviations are then
+// formed from the values kept in registers, exactly as tile_stats does for
+// whole tiles.
+constexpr int CRS_THREADS = 256, CRS_ROWS = 16;   // rows per thread at most
+
+__global__ void __launch_bounds__(CRS_THREADS) igemm_cut_reduce_stats_kernel(KArgs args, int BM,
+                                                                             int BN) {
+    __shared__ float part[CRS_THREADS * 4];
+    __shared__ float mean[256];
+    const int CG = BN / 4, RG = CRS_THREADS / CG;
+    const int t = threadIdx.x;
+    const int cg = t % CG, rg = t / CG;
+    const int rt = blockIdx.x;
+    const int tile = args.tfull + rt;
+    const long m0 = (long)(tile / args.tiles_n) * BM, n0 = (long)(tile % args.tiles_n) * BN;
+    const long rows = min((long)BM, args.M - m0);
+    const long col0 = n0 + 4 * cg;
+    const float* src = args.ws + (long)rt * args.splits * BM * BN;
+    float b4[4] = {0.f, 0.f, 0.f, 0.f};
+    if (args.epi & EPI_BIAS)
+        for (int e = 0; e < 4; ++e)
+            if (col0 + e < args.Ncols) b4[e] = args.bias[col0 + e];
+    float val[CRS_ROWS][4];
+    float sum[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int q = 0; q < CRS_ROWS; ++q) {
+        const int r = rg + q * RG;
+        for (int e = 0; e < 4; ++e) val[q][e] = 0.f;
+        if (r >= BM || r >= rows) continue;
+        float4 a = *reinterpret_cast<const float4*>(src + r * BN + 4 * cg);
+        for (int z = 1; z < args.splits; ++z) {
+            const float4 p = *reinterpret_cast<const float4*>(src + (long)z * BM * BN + r * BN + 4 * cg);
+            a.x += p.x; a.y += p.y; a.z += p.z; a.w += p.w;
+        }
+        val[q][0] = a.x + b4[0];
+        val[q][1] = a.y + b4[1];
+        val[q][2] = a.z + b4[2];
+        val[q][3] = a.w + b4[3];
+        float* o = args.out + (m0 + r) * args.Ncols + col0;
+        for (int e = 0; e < 4; ++e) {
+            if (col0 + e < args.Ncols) o[e] = val[q][e];
+            sum[e] += val[q][e];
+        }
+    }
+    const long tm = m0 / BM;
+    for (int pass = 0; pass < 2; ++pass) {
+        if (pass == 1) {
+            float mu[4];
+            for (int e = 0; e < 4; ++e) { mu[e] = mean[4 * cg + e]; sum[e] = 0.f; }
+#pragma unroll
+            for (int q = 0; q < CRS_ROWS; ++q) {
+                const int r = rg + q * RG;
+                if (r >= BM || r >= rows) continue;
+                for (int e = 0; e < 4; ++e) {
+                    const float d = val[q][e] - mu[e];
+                    sum[e] += d * d;
+                }
+            }
+        }
+        for (int e = 0; e < 4; ++e) part[(rg * CG + cg) * 4 + e] = sum[e];
+        __syncthreads();
+        if (rg == 0) {
+            for (int e = 0; e < 4; ++e) {
+                float s = 0.f;
+                for (int g = 0; g < RG; ++g) s += part[(g * CG + cg) * 4 + e];
+                const long col = col0 + e;
+                if (pass == 0) {
+                    mean[4 * cg + e] = rows > 0 ? s / (float)rows : 0.f;
+                } else if (col < args.Ncols) {
+                    args.stats[tm * args.Ncols + col] = mean[4 * cg + e];
+                    args.stats[((long)args.tiles_m + tm) * args.Ncols + col] = s;
+                }
+            }
+        }
+        __syncthreads();
     }
 }
 
@@ -2036,6 +2187,8 @@ GemmPlan plan_gemm(int op, const ConvGeo& g, int bf16, int num_cus, int bias_col
     p.tfull = (int)(p.splits > 1 ? tfull : tiles);
     p.nwg = (int)(p.tfull + (tiles - p.tfull) * p.splits);
     p.ws_floats = (size_t)(tiles - p.tfull) * p.splits * c.bm * c.bn;
+    p.bm = c.bm;
+    p.bn = c.bn;
     return p;
 }
 
@@ -2052,6 +2205,10 @@ void div_magic(int d, unsigned* m, int* sh) {
 }
 }  // namespace
 
+bool plan_stats(const GemmPlan& plan, int flags) {
+    return (flags & ~EPI_BIAS) == 0 && (plan.bf16 || plan.wide);
+}
+
 hipError_t launch_gemm(const GemmPlan& plan, const ConvGeo& g, const float* a, const float* b,
                        float* out, const Epilogue& ep, float* ws, hipStream_t s,
                        const uint16_t* a16, const uint16_t* b16, const uint16_t* b16t) {
@@ -2063,6 +2220,9 @@ hipError_t launch_gemm(const GemmPlan& plan, const ConvGeo& g, const float* a, c
     k.bias = ep.bias;
     k.mask = ep.mask;
     k.bias_out = ep.bias_out;
+    // column statistics: kernels with the wide epilogue only (bf16, or the fp32
+    // wide variant); the caller checks plan_stats() before relying on them
+    k.stats = plan_stats(plan, ep.flags) ? ep.stats : nullptr;
     k.epi = ep.flags | (plan.bias_col ? EPI_BIASCOL : 0);
     k.M = plan.M;
     k.Ncols = plan.Ncols;
@@ -2100,7 +2260,10 @@ hipError_t launch_gemm(const GemmPlan& plan, const ConvGeo& g, const float* a, c
     hipError_t e = hipLaunchKernel(kr.fn, dim3(plan.nwg), dim3(kr.nt), kargs, 0, s);
     const int cut = k.tiles_m * k.tiles_n - plan.tfull;
     if (e != hipSuccess || cut == 0) return e;
-    if (plan.splits <= SK_LANES) {
+    if (k.stats) {
+        hipLaunchKernelGGL(igemm_cut_reduce_stats_kernel, dim3(cut), dim3(CRS_THREADS), 0, s, k,
+                           c.bm, c.bn);
+    } else if (plan.splits <= SK_LANES) {
         const long total = (long)cut * c.bm * c.bn / 4;
         const int blocks = (int)std::min<long>((total + 255) / 256, 16384);
         hipLaunchKernelGGL(igemm_cut_reduce_kernel, dim3(blocks), dim3(256), 0, s, k, c.bm, c.bn);

@@ -33,6 +33,7 @@ struct GemmPlan {
     int splits;        // the other tiles are cut into `splits` reduction chunks
     int kchunk;        // reduction length of a chunk (multiple of the K tile)
     int nwg;           // workgroups launched
+    int bm, bn;        // workgroup tile
     size_t ws_floats;  // workspace for the partial tiles of the cut tiles
     long M, Ncols, Kred;
 };
@@ -56,12 +57,18 @@ struct Epilogue {
     const float* bias = nullptr;
     const float* mask = nullptr;
     float* bias_out = nullptr;
+    // optional (flags within EPI_BIAS): per output column and row tile of
+    // plan.bm rows, the tile's mean and sum of squared deviations from it:
+    // stats[t * Ncols + col] and stats[(tiles_m + t) * Ncols + col]
+    float* stats = nullptr;
 };
 
 // a16 / b16 (bf16 plans with plan.h16, optional): the same operands already
 // rounded to bf16, 16-byte aligned; when given, the kernel stages them directly.
 // b16t (OP_DGRAD, optional): the weights transposed to [C][R][S][K] in bf16;
 // with it a plan with h16k runs on k-major operands.
+// Whether launch_gemm writes Epilogue::stats for this plan and epilogue flags.
+bool plan_stats(const GemmPlan& plan, int flags);
 hipError_t launch_gemm(const GemmPlan& plan, const ConvGeo& g, const float* a,
                        const float* b, float* out, const Epilogue& ep, float* ws,
                        hipStream_t s, const uint16_t* a16 = nullptr,
@@ -137,6 +144,13 @@ size_t bn_ws_floats(long M, int C);
 hipError_t launch_bn_fwd(const float* x, long M, int C, const float* gamma, const float* beta,
                          float eps, float* y, float* mean, float* invstd, int relu, float* ws,
                          hipStream_t s, uint16_t* y16 = nullptr);
+// The same from per-row-block partials computed elsewhere (the producing
+// contraction's tile statistics): part0[b][c] = mean of block b, part1[b][c]
+// = its sum of squared deviations, blocks of rb rows (the last one shorter).
+hipError_t launch_bn_fwd_partials(const float* x, long M, int C, const float* gamma,
+                                  const float* beta, float eps, float* y, float* mean,
+                                  float* invstd, int relu, const float* part0, const float* part1,
+                                  int nb, long rb, hipStream_t s, uint16_t* y16 = nullptr);
 // Backward.  If relu_y != NULL the incoming gradient is first masked by
 // relu_y > 0 (BN followed by ReLU).  Writes dgamma, dbeta and, unless dx is NULL,
 // dx (accumulate optional).

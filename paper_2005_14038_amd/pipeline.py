@@ -48,7 +48,10 @@ def _refs(d):
 def valid_cuts(layers):
     """Indices i such that cutting after layer i leaves exactly one tensor (the
     output of layer i) crossing the cut, and the loss head keeps a layer before
-    it in its partition."""
+    it in its partition.  A conv and the batch norm reading it stay together:
+    the batch norm takes its statistics from the conv's contraction, and a cut
+    between them would change the order of those sums, so the pipeline would
+    no longer reproduce the sequential stage bit for bit."""
     n = len(layers)
     # earliest layer referenced by any later layer
     cuts = []
@@ -60,6 +63,9 @@ def valid_cuts(layers):
         if min_ref_after[i + 1] < i:
             continue
         if layers[-1]["kind"] == HP_SOFTMAX_CE and i == n - 2:
+            continue
+        if layers[i]["kind"] == HP_CONV and any(
+                d["kind"] == HP_BN and d.get("in0", -1) == i for d in layers[i + 1:]):
             continue
         cuts.append(i)
     return cuts

@@ -7,7 +7,7 @@ import pytest
 
 from paper_2005_14038_amd import nets
 from paper_2005_14038_amd import pipeline as pl
-from paper_2005_14038_amd.hetpipe import HP_ADD, HP_RELU
+from paper_2005_14038_amd.hetpipe import HP_ADD, HP_BN, HP_CONV, HP_RELU
 
 
 @pytest.mark.parametrize("name", ["tiny", "vgg19", "resnet152"])
@@ -22,12 +22,19 @@ def test_valid_cuts_leave_one_tensor(name):
                 refs.append(layers[j]["in1"])
             # nothing after the cut reads a tensor from before it, except layer i
             assert all(r >= i for r in refs), (i, j, refs)
-    # every rejected index has some later layer reading across it
+    # every rejected index has some later layer reading across it, or
+    # separates a conv from the batch norm that reads it
     for i in set(range(len(layers) - 1)) - set(cuts):
         crossing = any(min([layers[j].get("in0", -1)] +
                            ([layers[j]["in1"]] if layers[j]["kind"] == HP_ADD else [])) < i
                        for j in range(i + 1, len(layers)))
-        assert crossing or i == len(layers) - 2
+        conv_bn = layers[i]["kind"] == HP_CONV and any(
+            d["kind"] == HP_BN and d.get("in0", -1) == i for d in layers[i + 1:])
+        assert crossing or conv_bn or i == len(layers) - 2
+    # no cut separates a conv from its batch norm
+    for i in cuts:
+        assert not (layers[i]["kind"] == HP_CONV and layers[i + 1]["kind"] == HP_BN
+                    and layers[i + 1].get("in0", -1) == i)
 
 
 def test_resnet_cuts_are_block_boundaries():
