@@ -122,6 +122,28 @@ def test_batchnorm(dev, shape, relu):  # noqa: F811
     assert_close(g["dx"], r["dx"], FP32_TOL, "data gradient")
 
 
+# conv -> batch norm -> ReLU: the batch norm takes its statistics from the
+# conv's contraction (whole tiles in the epilogue, cut tiles in the cut-tile
+# reduction); shapes with whole tiles only, with tiles cut 18 ways, and ragged
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+@pytest.mark.parametrize("case", [(4, 32, 32, 64, 128, 1, 1, 0), (2, 14, 14, 256, 64, 3, 1, 1),
+                                  (3, 9, 7, 64, 96, 3, 1, 1)])
+def test_conv_batchnorm_statistics_from_the_contraction(dev, case, dtype):  # noqa: F811
+    B, H, W, C, K, R, st, pad = case
+
+    def build(n):
+        n.relu(n.bn(n.conv(-1, C, K, R, st, pad), K))
+    net = single(build, H, W, C)
+    w = oracle_weights(net, 81, scale_bn=True)
+    x, _, dy = make_inputs(net, B, 82)
+    g = run_gpu(net, B, w, x, None, dy, True, dtype)
+    r = run_oracle(net, w, x, None, dy, True, bf16=(dtype == "bf16"))
+    tol = FP32_TOL if dtype == "fp32" else BF16_TOL
+    assert_close(g["y"], r["y"], tol, "forward")
+    assert_close(g["grad"], r["grad"], tol, "weight, gamma, beta gradients")
+    assert_close(g["dx"], r["dx"], tol, "data gradient")
+
+
 def test_residual_add_fans_out_to_the_input(dev):  # noqa: F811
     # y = relu(bn(conv(x)) + x): the input gradient sums the branch and the skip
     def build(n):
