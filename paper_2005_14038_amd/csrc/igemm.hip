@@ -712,12 +712,16 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_kernel(KA
     // one k tile: prefetch tile kt+2 into register set s, multiply LDS buffer
     // s, write tile kt+1 (register set s^1) to LDS buffer s^1; loads of tiles
     // past the end are fully masked, so every load is on one path and the
-    // wait before the LDS write counts only the older set
+    // wait before the LDS write counts only the older set.  The wave raises
+    // its issue priority while it multiplies, so that of the waves sharing a
+    // SIMD the ones with MFMAs ready go ahead of those staging operands (the
+    // kernels below do the same).
     auto step = [&](int kt, auto S) {
         constexpr int s = decltype(S)::value;
         gload(kt + 2, S);
         const float* As = smem + s * BK * (LDA + LDB);
         const float* Bs = As + BK * LDA;
+        __builtin_amdgcn_s_setprio(1);
         if (kt < ktiles) {
 #pragma unroll
             for (int kk = 0; kk < BK; kk += 2) {
@@ -736,6 +740,7 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_kernel(KA
                                                                         0, 0, 0);
             }
         }
+        __builtin_amdgcn_s_setprio(0);
         if (kt + 1 < ktiles) sstore(std::integral_constant<int, s ^ 1>{});
         __syncthreads();
     };
@@ -1414,6 +1419,7 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_h16_kerne
         gload(kt + 2, S);
         const unsigned short* As = smem + s * (BM + BN) * LDX;
         const unsigned short* Bs = As + BM * LDX;
+        __builtin_amdgcn_s_setprio(1);
         if (kt < ktiles) {
 #pragma unroll
         for (int kk = 0; kk < BKX; kk += 16) {
@@ -1434,6 +1440,7 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_h16_kerne
                                                                          0, 0);
         }
         }
+        __builtin_amdgcn_s_setprio(0);
         if (kt + 1 < ktiles) sstore(std::integral_constant<int, s ^ 1>{});
         __syncthreads();
     };
@@ -1615,6 +1622,7 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_h16k_kern
         gload(S);                                  // tile kt + 2
         const unsigned short* As = smem + s * (BM + BN) * LDX;
         const unsigned short* Bs = As + BM * LDX;
+        __builtin_amdgcn_s_setprio(1);
         if (kt < ktiles) {
 #pragma unroll
             for (int kk = 0; kk < BKX; kk += 16) {
@@ -1635,6 +1643,7 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_h16k_kern
                                                                              acc[i][j], 0, 0, 0);
             }
         }
+        __builtin_amdgcn_s_setprio(0);
         if (kt + 1 < ktiles) sstore(std::integral_constant<int, s ^ 1>{});
         __syncthreads();
     };
@@ -1667,15 +1676,18 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_h16k_kern
 // transpose reads (ds_read_b64_tr_b16): in every group of 16 lanes, lane i
 // receives element i mod 4 of the 8 bytes read by lane 4e + i/4 as its value
 // e, so when source lane S reads k row k0 + S/4 at columns m0 + 4 (S mod 4),
-// lane i holds k0..k0+3 of column m0 + i.  Rows are padded by 16 elements,
-// which puts the four rows a 16-lane group reads in disjoint banks.  The
+// lane i holds k0..k0+3 of column m0 + i.  The LDS serves an 8-byte read
+// 32 lanes at a time from 64 four-byte banks; those 32 lanes read 16
+// consecutive dwords of each of four rows, so rows are padded by 32 elements
+// (a pitch of 16 mod 64 dwords for BM = 128, 48 for BM = 64), which puts the
+// four rows in disjoint quarters of the banks.  The
 // output pixel of a k row is divided into (n, p, q) by multiply-high with
 // constants computed on the host.
 template <int BM, int BN, int WM, int WN, int BKX>
 __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_h16w_kernel(KArgs args) {
     constexpr int NT = 64 * (BM / WM) * (BN / WN);
     constexpr int TM = WM / 32, TN = WN / 32;
-    constexpr int PA = BM + 16, PB = BN + 16;    // LDS row pitch (bf16)
+    constexpr int PA = BM + 32, PB = BN + 32;    // LDS row pitch (bf16)
     constexpr int WAVES_N = BN / WN;
     constexpr int CGA = BM / 8, CGB = BN / 8;    // 16-byte groups per row
     constexpr int LA = BKX * CGA / NT;           // loads per thread per tile
@@ -1798,6 +1810,7 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_h16w_kern
         gload(kt + 2, S);
         const unsigned short* As = smem + s * BKX * (PA + PB);
         const unsigned short* Bs = As + BKX * PA;
+        __builtin_amdgcn_s_setprio(1);
         if (kt < ktiles) {
 #pragma unroll
             for (int kk = 0; kk < BKX; kk += 16) {
@@ -1814,6 +1827,7 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_h16w_kern
                                                                              acc[i][j], 0, 0, 0);
             }
         }
+        __builtin_amdgcn_s_setprio(0);
         if (kt + 1 < ktiles) sstore(std::integral_constant<int, s ^ 1>{});
         __syncthreads();
     };
