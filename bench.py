@@ -21,6 +21,7 @@ import argparse
 import dataclasses
 import hashlib
 import json
+import statistics
 import os
 import sys
 import time
@@ -276,19 +277,23 @@ def main():
         drv.minibatch(next_vw())
     torch.cuda.synchronize()
 
-    # timed region: K steps exactly as a user runs them (no instrumentation)
-    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    # timed region: K steps exactly as a user runs them (no per-kernel
+    # instrumentation; one event between steps gives the per-wave repeats)
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    start.record()
-    for _ in range(args.steps):
+    evs[0].record()
+    for i in range(args.steps):
         n = next_vw()
         order.append(n)
         drv.minibatch(n)
-    stop.record()
+        evs[i + 1].record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    ev_ms = start.elapsed_time(stop)
+    ev_ms = evs[0].elapsed_time(evs[-1])
+    W = wl.s_local + 1
+    wave_rates = [wl.batch * W / (evs[i].elapsed_time(evs[i + W]) * 1e-3)
+                  for i in range(0, args.steps - W + 1, W)]
 
     # kernel-timing pass: K more steps of the same schedule with HIP events
     # recorded around every launch on the stream it is issued to (the library's
@@ -337,6 +342,11 @@ def main():
                      "flop_per_step": flops_step, "ms_per_step": round(gemm_ms_step, 4),
                      "launches_per_step": launches["contraction"] / args.steps},
         "other_kernels_ms_per_step": round(ms["other"] / args.steps, 4),
+        "repeats": ({"per": f"wave of {W} minibatches (HIP events between timed steps)",
+                     "n": len(wave_rates), "unit": "images/s",
+                     "median": round(statistics.median(wave_rates), 3),
+                     "min": round(min(wave_rates), 3), "max": round(max(wave_rates), 3)}
+                    if wave_rates else None),
         "wsp_update_roofline": update_roofline(st.P, ums, ulaunch),
     }
     drv.close()

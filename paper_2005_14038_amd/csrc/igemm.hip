@@ -1966,6 +1966,31 @@ __global__ void __launch_bounds__(CRS_THREADS) igemm_cut_reduce_stats_kernel(KAr
     if (args.epi & EPI_BIAS)
         for (int e = 0; e < 4; ++e)
             if (col0 + e < args.Ncols) b4[e] = args.bias[col0 + e];
+    // the partials of one split for every row of this thread are loaded
+    // together (CRS_ROWS loads in flight), then added; each element still
+    // sums its splits in split order
+    float4 acc[CRS_ROWS];
+    auto load_split = [&](int z, float4 (&p)[CRS_ROWS]) {
+        const float* sz = src + (long)z * BM * BN + 4 * cg;
+#pragma unroll
+        for (int q = 0; q < CRS_ROWS; ++q) {
+            const int r = rg + q * RG;
+            p[q] = (r < BM && r < rows) ? *reinterpret_cast<const float4*>(sz + r * BN)
+                                        : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+    };
+    load_split(0, acc);
+    for (int z = 1; z < args.splits; ++z) {
+        float4 p[CRS_ROWS];
+        load_split(z, p);
+#pragma unroll
+        for (int q = 0; q < CRS_ROWS; ++q) {
+            acc[q].x += p[q].x; acc[q].y += p[q].y; acc[q].z += p[q].z; acc[q].w += p[q].w;
+        }
+    }
+    // 16-byte stores when the row length keeps them aligned
+    const bool vec_out = (args.Ncols & 3) == 0 && col0 + 3 < args.Ncols &&
+                         (((uintptr_t)args.out) & 15) == 0;
     float val[CRS_ROWS][4];
     float sum[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -1973,20 +1998,18 @@ __global__ void __launch_bounds__(CRS_THREADS) igemm_cut_reduce_stats_kernel(KAr
         const int r = rg + q * RG;
         for (int e = 0; e < 4; ++e) val[q][e] = 0.f;
         if (r >= BM || r >= rows) continue;
-        float4 a = *reinterpret_cast<const float4*>(src + r * BN + 4 * cg);
-        for (int z = 1; z < args.splits; ++z) {
-            const float4 p = *reinterpret_cast<const float4*>(src + (long)z * BM * BN + r * BN + 4 * cg);
-            a.x += p.x; a.y += p.y; a.z += p.z; a.w += p.w;
-        }
-        val[q][0] = a.x + b4[0];
-        val[q][1] = a.y + b4[1];
-        val[q][2] = a.z + b4[2];
-        val[q][3] = a.w + b4[3];
+        val[q][0] = acc[q].x + b4[0];
+        val[q][1] = acc[q].y + b4[1];
+        val[q][2] = acc[q].z + b4[2];
+        val[q][3] = acc[q].w + b4[3];
         float* o = args.out + (m0 + r) * args.Ncols + col0;
-        for (int e = 0; e < 4; ++e) {
-            if (col0 + e < args.Ncols) o[e] = val[q][e];
-            sum[e] += val[q][e];
+        if (vec_out) {
+            *reinterpret_cast<float4*>(o) = make_float4(val[q][0], val[q][1], val[q][2], val[q][3]);
+        } else {
+            for (int e = 0; e < 4; ++e)
+                if (col0 + e < args.Ncols) o[e] = val[q][e];
         }
+        for (int e = 0; e < 4; ++e) sum[e] += val[q][e];
     }
     const long tm = m0 / BM;
     for (int pass = 0; pass < 2; ++pass) {
