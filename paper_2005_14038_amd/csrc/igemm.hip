@@ -14,15 +14,20 @@
 // block of the output as a grid of MFMA 32x32 tiles.
 //
 //   fp32: v_mfma_f32_32x32x2_f32; LDS tiles [BK][rows] (row index contiguous).
-//   bf16: every operand is rounded to bfloat16 (RNE) as it is staged; LDS
-//         tiles [rows][32 k] of bf16 (reduction index contiguous) feed
-//         v_mfma_f32_32x32x16_bf16.  Products of bf16 values are exact in fp32
-//         and the accumulation stays fp32.
+//   bf16: every operand is rounded to bfloat16 (RNE), either as it is staged
+//         from fp32 or once, into a bf16 copy in memory, by the layer that
+//         produces it; v_mfma_f32_32x32x16_bf16 reads LDS tiles of BKH = 32
+//         or 64 reduction indices per row.  Products of bf16 values are exact
+//         in fp32 and the accumulation stays fp32.  Kernels: general gather
+//         (igemm_bf16_kernel from fp32, igemm_h16_kernel from bf16), buffer
+//         loads for k-major operands (igemm_h16k_kernel: forward, data
+//         gradient) and m-major LDS tiles with transpose reads
+//         (igemm_h16w_kernel: weight gradient).
 //
 // Long reductions (weight gradients reduce over N*P*Q, FC layers over their
-// fan-in) are cut into chunks; each chunk writes a partial tile to a
-// workspace and a second kernel adds the partials in a fixed order, so results
-// are deterministic.
+// fan-in) and layers with too few output tiles to fill the chip are cut into
+// chunks; each chunk writes a partial tile to a workspace and a second kernel
+// adds the partials in a fixed order, so results are deterministic.
 #include <type_traits>
 
 #include "kernels.h"

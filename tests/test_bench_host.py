@@ -1,0 +1,53 @@
+"""Host-side checks of bench.py: the one-GPU refusal, and the code hash that
+keys the stored contraction traffic (it must ignore comments and whitespace
+and see every change to the code)."""
+import importlib.util
+import os
+import subprocess
+import sys
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _bench():
+    spec = importlib.util.spec_from_file_location("bench_mod", os.path.join(ROOT, "bench.py"))
+    mod = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(mod)
+    return mod
+
+
+SRC = """// header comment
+template <int N> __global__ void k(float* a) {  /* block
+   comment */
+    a[threadIdx.x] *= 2.f;   // trailing
+}
+"""
+
+
+def test_code_hash_ignores_comments_and_whitespace(tmp_path):
+    b = _bench()
+    p0, p1, p2 = tmp_path / "a.hip", tmp_path / "b.hip", tmp_path / "c.hip"
+    p0.write_text(SRC)
+    p1.write_text(SRC.replace("// trailing", "// another remark")
+                     .replace("block\n   comment", "x").replace("    a[", "\ta["))
+    p2.write_text(SRC.replace("2.f", "3.f"))
+    h0, h1, h2 = (b.kernel_code_hash(str(p)) for p in (p0, p1, p2))
+    assert h0 == h1
+    assert h0 != h2
+
+
+def test_stored_traffic_is_keyed_by_the_code_hash():
+    b = _bench()
+    import json
+    d = json.load(open(os.path.join(ROOT, "profiles", "igemm_vgg19_s1_traffic.json")))
+    assert "igemm_code_sha256_16" in d and d["bytes_per_step"] > 0
+    # reported only while the stored hash matches the current kernel code
+    expect = d["bytes_per_step"] if d["igemm_code_sha256_16"] == b.kernel_code_hash() else None
+    assert b.measured_traffic("vgg19_s1") == expect
+
+
+def test_more_than_one_gpu_is_refused():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=300, cwd=ROOT)
+    assert r.returncode != 0
+    assert "one GPU" in (r.stdout + r.stderr)
