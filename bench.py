@@ -139,8 +139,20 @@ def cpu_baseline(wl, layers, out_shape, images):
     dt = time.perf_counter() - t0
     cores = int(os.environ.get("OMP_NUM_THREADS", "0")) or len(os.sched_getaffinity(0))
     return {"value": round(images / dt, 4), "unit": "images/s", "cores": cores, "kind": "oracle",
+            "cpu": cpu_model(), "affinity_cpus": len(os.sched_getaffinity(0)),
             "sample": f"{images} image(s) of minibatch 1 ({wl.name}): oracle stage forward + "
                       f"backward + local update, {dt:.1f} s"}
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
 
 
 def run_pipeline(args, wl, dev):
