@@ -125,7 +125,8 @@ __device__ __forceinline__ unsigned pack_bf16(float lo, float hi) {
 // as full as the others, and leave partial tiles for the reduce kernels.
 // XCD-aware: consecutive workgroup ids are dealt round-robin to the 8 XCDs;
 // each XCD gets a contiguous run of whole tiles (n fastest), so tiles sharing
-// A rows share that XCD's L2.
+// A rows share that XCD's L2, and likewise a contiguous run of cut-tile items
+// (chunk, tile), so tiles reducing over the same chunk share it.
 struct Work {
     int tile, z;
     bool partial;
@@ -143,8 +144,21 @@ __device__ __forceinline__ Work decode_work(const KArgs& args) {
         w.tile = bid;
     } else {
         const int r = bid - args.tfull;
-        w.tile = args.tfull + r / args.splits;
-        w.z = r - (w.tile - args.tfull) * args.splits;
+        const int ncut = args.tiles_m * args.tiles_n - args.tfull;
+        if ((args.tfull & 7) == 0) {
+            // the workgroups of one XCD (ids congruent mod 8) take a contiguous
+            // run of (chunk, tile) items, tiles fastest: the cut tiles that
+            // reduce over the same chunk (same dy rows, same image rows) share
+            // that XCD's L2
+            const int nparts = ncut * args.splits;
+            const int x = r & 7, q = nparts >> 3, rem = nparts & 7;
+            const int item = x * q + min(x, rem) + (r >> 3);
+            w.z = item / ncut;
+            w.tile = args.tfull + (item - w.z * ncut);
+        } else {
+            w.tile = args.tfull + r / args.splits;
+            w.z = r - (w.tile - args.tfull) * args.splits;
+        }
     }
     w.m0 = (long)(w.tile / args.tiles_n) * BM;
     w.n0 = (long)(w.tile % args.tiles_n) * BN;
