@@ -365,7 +365,8 @@ def main():
         "repeats": ({"per": f"wave of {W} minibatches (HIP events between timed steps)",
                      "n": len(wave_rates), "unit": "images/s",
                      "median": round(statistics.median(wave_rates), 3),
-                     "min": round(min(wave_rates), 3), "max": round(max(wave_rates), 3)}
+                     "min": round(min(wave_rates), 3), "max": round(max(wave_rates), 3),
+                     "rates": [round(v, 1) for v in wave_rates]}
                     if wave_rates else None),
         "wsp_update_roofline": update_roofline(st.P, ums, ulaunch),
     }
