@@ -57,6 +57,42 @@ def test_conv(dev, case, dtype):  # noqa: F811
     assert_close(g["dx"], r["dx"], tol, "data gradient")
 
 
+def random_conv(seed):
+    """A seeded conv geometry: taps 1, 3 or 5, stride 1 or 2, any legal padding,
+    channel counts on and off the vector and k-tile multiples, ragged maps;
+    shrunk until the layer is at most 40 M multiply-adds."""
+    rng = np.random.default_rng(4000 + seed)
+    R = int(rng.choice([1, 3, 3, 5]))
+    st = int(rng.choice([1, 1, 2]))
+    pad = int(rng.integers(0, R // 2 + 1))
+    C = int(rng.choice([3, 5, 8, 16, 24, 64, 72, 128]))
+    K = int(rng.choice([8, 20, 64, 96, 136, 256]))
+    H, W = int(rng.integers(R, 19)), int(rng.integers(R, 19))
+    N = int(rng.integers(1, 5))
+    bias = bool(rng.integers(0, 2))
+
+    def macs():
+        P = (H + 2 * pad - R) // st + 1
+        Q = (W + 2 * pad - R) // st + 1
+        return N * P * Q * K * C * R * R
+
+    while macs() > 40e6 and (N > 1 or H > R or W > R):
+        if N > 1:
+            N -= 1
+        else:
+            H, W = max(R, H - 2), max(R, W - 2)
+    return (N, H, W, C, K, R, st, pad, bias)
+
+
+RANDOM_CONV = [random_conv(s) for s in range(40)]
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+@pytest.mark.parametrize("case", RANDOM_CONV, ids=[f"rnd{i}-{c[:8]}" for i, c in enumerate(RANDOM_CONV)])
+def test_conv_random_geometry(dev, case, dtype):  # noqa: F811
+    test_conv(dev, case, dtype)
+
+
 FC = [(4, 1, 1, 37, 50), (32, 2, 3, 16, 96), (5, 3, 3, 64, 260)]
 
 
