@@ -124,9 +124,45 @@ def test_maxpool_and_unfused_relu(dev, case):  # noqa: F811
     x, _, dy = make_inputs(net, B, 31)
     g = run_gpu(net, B, np.zeros(0, np.float32), x, None, dy, True)
     r = run_oracle(net, np.zeros(0), x, None, dy, True)
-    # max-pool and ReLU select values: the results are exact
+    # max-pool and ReLU select values: the forward is exact
     np.testing.assert_array_equal(g["y"], r["y"].astype(np.float32))
-    assert_close(g["dx"], r["dx"], 1e-6, "data gradient")
+    if st >= R:
+        # each input is in at most one window: its gradient is one dy value
+        np.testing.assert_array_equal(g["dx"], r["dx"].astype(np.float32))
+    else:
+        # an input sums dy over the k <= ceil(R/st)^2 windows whose first
+        # maximum it is; an fp32 sum of k terms in any order is within
+        # (k-1) 2^-24 sum|g| of the exact sum, and the routing depends on x
+        # alone, so the oracle on |dy| gives sum|g| per element
+        k = (-(-R // st)) ** 2
+        s_abs = run_oracle(net, np.zeros(0), x, None, np.abs(dy), True)["dx"]
+        err = np.abs(g["dx"].astype(np.float64) - r["dx"])
+        bound = (k - 1) * 2.0 ** -24 * s_abs * (1 + 1e-6)
+        assert np.all(err <= bound), \
+            f"data gradient: worst excess {np.max(err - bound):.3e} over the fp32 summation bound"
+
+
+def random_pool(seed):
+    """A seeded max-pool geometry: windows 2 or 3, strides 1-3 (overlapping,
+    tiling and gapped windows), padding up to half the window, ragged maps,
+    channel counts on and off the vector width."""
+    rng = np.random.default_rng(5000 + seed)
+    R = int(rng.choice([2, 3]))
+    st = int(rng.integers(1, 4))
+    pad = int(rng.integers(0, R // 2 + 1))
+    H, W = int(rng.integers(R, 21)), int(rng.integers(R, 21))
+    if seed % 4 == 0:                     # windows that tile the map exactly
+        st, pad = R, 0
+        H, W = R * max(1, H // R), R * max(1, W // R)
+    return (int(rng.integers(1, 5)), H, W, int(rng.choice([1, 3, 4, 8, 64, 130])), R, st, pad)
+
+
+RANDOM_POOL = [random_pool(s) for s in range(24)]
+
+
+@pytest.mark.parametrize("case", RANDOM_POOL, ids=[f"rnd{i}-{c}" for i, c in enumerate(RANDOM_POOL)])
+def test_maxpool_random_geometry(dev, case):  # noqa: F811
+    test_maxpool_and_unfused_relu(dev, case)
 
 
 def test_maxpool_ties_route_to_first(dev):  # noqa: F811
@@ -178,6 +214,16 @@ def test_conv_batchnorm_statistics_from_the_contraction(dev, case, dtype):  # no
     assert_close(g["y"], r["y"], tol, "forward")
     assert_close(g["grad"], r["grad"], tol, "weight, gamma, beta gradients")
     assert_close(g["dx"], r["dx"], tol, "data gradient")
+
+
+RANDOM_CONV_BN = [random_conv(100 + s)[:8] for s in range(16)]
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+@pytest.mark.parametrize("case", RANDOM_CONV_BN,
+                         ids=[f"rnd{i}-{c}" for i, c in enumerate(RANDOM_CONV_BN)])
+def test_conv_batchnorm_random_geometry(dev, case, dtype):  # noqa: F811
+    test_conv_batchnorm_statistics_from_the_contraction(dev, case, dtype)
 
 
 def test_residual_add_fans_out_to_the_input(dev):  # noqa: F811
