@@ -24,6 +24,7 @@ import json
 import statistics
 import os
 import re
+import subprocess
 import sys
 import time
 
@@ -144,6 +145,21 @@ def cpu_baseline(wl, layers, out_shape, images):
                       f"backward + local update, {dt:.1f} s"}
 
 
+def single_thread_baseline(args):
+    """The oracle's sample on one thread and one image, timed in a child
+    process (OpenMP fixes its thread count when the library loads)."""
+    cmd = [sys.executable, os.path.abspath(__file__), "--cpu-baseline-only",
+           "--workload", args.workload, "--cpu-images", "1"]
+    if args.dtype is not None:
+        cmd += ["--dtype", args.dtype]
+    r = subprocess.run(cmd, env=dict(os.environ, OMP_NUM_THREADS="1"), capture_output=True,
+                       text=True, timeout=1800)
+    if r.returncode != 0:
+        raise RuntimeError("single-thread oracle sample failed:\n" + r.stderr[-2000:])
+    d = json.loads(r.stdout.strip().splitlines()[-1])
+    return {"value": d["value"], "unit": d["unit"], "cores": d["cores"], "sample": d["sample"]}
+
+
 def cpu_model():
     try:
         with open("/proc/cpuinfo") as f:
@@ -241,6 +257,12 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-images", type=int, default=4,
                     help="images of the oracle's bounded CPU sample")
+    ap.add_argument("--cpu-single-thread", action="store_true",
+                    help="also time the oracle on one thread, on one image (a child process "
+                         "with OMP_NUM_THREADS=1, started before this one touches the GPU)")
+    ap.add_argument("--cpu-baseline-only", action="store_true",
+                    help="time only the oracle's bounded CPU sample, without the GPU, and "
+                         "print it as one JSON line")
     ap.add_argument("--dtype", choices=["fp32", "bf16"], default=None,
                     help="contraction mode (default: the workload's); bf16 rounds the "
                          "contraction operands and keeps fp32 master weights")
@@ -257,6 +279,20 @@ def main():
               "single MI355X (virtual workers take turns on it); --gpus must be 1.",
               file=sys.stderr)
         sys.exit(2)
+
+    if args.cpu_baseline_only:
+        from oracle import nets as onets
+        from paper_2005_14038_amd import workloads
+        wl = workloads.WORKLOADS[args.workload]
+        if args.dtype is not None:
+            wl = dataclasses.replace(wl, dtype=args.dtype)
+        out_shape = onets.by_name(wl.net, **wl.net_kw).out_shape
+        print(json.dumps(cpu_baseline(wl, wl.builder().layers, out_shape, args.cpu_images)),
+              flush=True)
+        return
+    single = None
+    if args.cpu_single_thread and not args.no_cpu_baseline and not args.pipeline:
+        single = single_thread_baseline(args)
 
     import torch
     from paper_2005_14038_amd import workloads
@@ -375,6 +411,8 @@ def main():
     torch.cuda.synchronize()
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(wl, layers, out_shape, args.cpu_images)
+        if single is not None:
+            out["cpu_baseline"]["single_thread"] = single
     print(json.dumps(out), flush=True)
 
 
