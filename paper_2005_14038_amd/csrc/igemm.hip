@@ -563,6 +563,16 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_kernel(KA
         for (int i = 0; i < BV; ++i) { brow_n[i] = 0; brow_ok[i] = true; }
     }
 
+    // data gradient: when K is a multiple of the k tile no tile crosses a
+    // tap, and row kr of a tile in tap (r, s) at channel c0 reads weight
+    // (c0 + kr)*R*S*C + (r*S + s)*C + c: the thread's part is fixed
+    const long rsc = (long)g.R * g.S * g.C;
+    const bool dg_one_tap = (OP == OP_DGRAD) && (g.K % BK == 0);
+    long b_thr[BV];
+#pragma unroll
+    for (int i = 0; i < BV; ++i)
+        b_thr[i] = (long)((t + i * NT) / BVPR) * rsc + bcol_c;
+
     // two register sets of staged operands (tile kt+2 loads while kt+1 waits
     // to be written to LDS) and their masks; loads are unconditional (masked
     // lanes read the operand's first element) and the mask is applied when
@@ -637,11 +647,18 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_kernel(KA
                     bok[s][i] = ok;
                 } else {   // B[kk = (r,s,k)][c] = w[k][r][s][c]
                     const int kr = (t + i * NT) / BVPR;
-                    int k = c0 + kr, r = r0, sx = s0;
-                    while (k >= CC) { k -= CC; if (++sx == g.S) { sx = 0; ++r; } }
                     bool ok = bcol_ok && k0 + kr < kend_i;
-                    const float* ptr =
-                        args.b + (ok ? ((((long)k * g.R + r) * g.S + sx) * g.C + bcol_c) : 0);
+                    long off;
+                    if (dg_one_tap) {
+                        // the tile lies within tap (r0, s0): a uniform base plus
+                        // this thread's constant offset
+                        off = (long)c0 * rsc + ((long)r0 * g.S + s0) * g.C + b_thr[i];
+                    } else {
+                        int k = c0 + kr, r = r0, sx = s0;
+                        while (k >= CC) { k -= CC; if (++sx == g.S) { sx = 0; ++r; } }
+                        off = (((long)k * g.R + r) * g.S + sx) * g.C + bcol_c;
+                    }
+                    const float* ptr = args.b + (ok ? off : 0);
                     ld(ptr, breg[s][i]);
                     bok[s][i] = ok;
                 }
