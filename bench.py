@@ -67,6 +67,84 @@ def contraction_flops(layers, batch, H, W, C):
     return total
 
 
+LAYER_NAMES = {1: "conv", 2: "fc", 3: "relu", 4: "maxpool", 5: "batchnorm", 6: "add",
+               7: "gap", 8: "softmax_ce"}
+
+
+def layer_work(layers, batch, H, W, C):
+    """Per layer: output shape and the algorithmic FLOP and bytes of its forward
+    and backward passes (every tensor read or written once per pass, 4 bytes an
+    element; a layer reading the stage input computes no data gradient)."""
+    shape = {-1: (H, W, C)}
+    rows = []
+    for i, d in enumerate(layers):
+        src = d.get("in0", i - 1)
+        h, w, c = shape[src]
+        k = d["kind"]
+        n_in = batch * h * w * c
+        f_flop = b_flop = 0
+        if k in (1, 2):
+            if k == 1:
+                P = (h + 2 * d["pad"] - d["R"]) // d["stride"] + 1
+                Q = (w + 2 * d["pad"] - d["S"]) // d["stride"] + 1
+                out, wts = (P, Q, d["K"]), d["K"] * d["R"] * d["S"] * c
+            else:
+                out, wts = (1, 1, d["K"]), d["K"] * d["C"]
+            n_out = batch * out[0] * out[1] * out[2]
+            macs = n_out * (wts // d["K"])
+            dgrad = src >= 0
+            f_flop, b_flop = 2 * macs, 2 * macs * (2 if dgrad else 1)
+            f_el = n_in + wts + n_out
+            b_el = (n_out + n_in + wts) * (2 if dgrad else 1)
+        else:
+            if k == 4:
+                out = ((h + 2 * d["pad"] - d["R"]) // d["stride"] + 1,
+                       (w + 2 * d["pad"] - d["S"]) // d["stride"] + 1, c)
+            elif k == 7:
+                out = (1, 1, c)
+            else:
+                out = (h, w, c)
+            n_out = batch * out[0] * out[1] * out[2]
+            if k == 6:                   # add: two inputs, gradient to both
+                f_el, b_el = 2 * n_in + n_out, n_out + 2 * n_in
+            elif k in (3, 4, 5):         # backward also reads the forward input
+                f_el, b_el = n_in + n_out, n_out + 2 * n_in
+            else:
+                f_el, b_el = n_in + n_out, n_out + n_in
+        shape[i] = out
+        rows.append({"layer": i, "op": LAYER_NAMES.get(k, str(k)), "out": list(out),
+                     "fwd_flop": f_flop, "bwd_flop": b_flop,
+                     "fwd_bytes": 4 * f_el, "bwd_bytes": 4 * b_el})
+    return rows
+
+
+def per_layer_rooflines(rows, fwd_ms, bwd_ms, steps, peak_tflops):
+    """Achieved fraction of the bounding peak per layer and pass, beside the
+    roofline-attainable fraction min(1, AI * 8 TB/s / MFMA peak) of a
+    contraction (element-wise layers are bound by HBM: attainable 1)."""
+    out = []
+    for r, tf, tb in zip(rows, fwd_ms, bwd_ms):
+        for ph, t, fl, by in (("fwd", tf, r["fwd_flop"], r["fwd_bytes"]),
+                              ("bwd", tb, r["bwd_flop"], r["bwd_bytes"])):
+            ms = t / steps
+            if ms <= 0:
+                continue                 # done inside another layer's kernels
+            e = {"layer": r["layer"], "op": r["op"], "pass": ph, "out": r["out"],
+                 "ms": round(ms, 4), "GB/s": round(by / (ms * 1e-3) / 1e9, 1)}
+            if fl:
+                ai = fl / by
+                e.update({"bound": "mfma" if ai * HBM_PEAK_GBS * 1e9 >= peak_tflops * 1e12 else "hbm",
+                          "TFLOP/s": round(fl / (ms * 1e-3) / 1e12, 2),
+                          "frac": round(fl / (ms * 1e-3) / (peak_tflops * 1e12), 4),
+                          "hbm_frac": round(by / (ms * 1e-3) / (HBM_PEAK_GBS * 1e9), 4),
+                          "attainable": round(min(1.0, ai * HBM_PEAK_GBS * 1e9 / (peak_tflops * 1e12)), 4)})
+            else:
+                e.update({"bound": "hbm", "frac": round(by / (ms * 1e-3) / (HBM_PEAK_GBS * 1e9), 4),
+                          "attainable": 1.0})
+            out.append(e)
+    return out
+
+
 def kernel_code_hash(path=None):
     """Hash of the contraction kernels' code: igemm.hip with its comments and
     whitespace removed, so that a change to a comment keeps stored counter
@@ -263,6 +341,10 @@ def main():
     ap.add_argument("--cpu-baseline-only", action="store_true",
                     help="time only the oracle's bounded CPU sample, without the GPU, and "
                          "print it as one JSON line")
+    ap.add_argument("--per-layer", action="store_true",
+                    help="add each layer's forward and backward time, achieved fraction of its "
+                         "bounding peak and roofline-attainable fraction (from the kernel-timing "
+                         "pass)")
     ap.add_argument("--dtype", choices=["fp32", "bf16"], default=None,
                     help="contraction mode (default: the workload's); bf16 rounds the "
                          "contraction operands and keeps fp32 master weights")
@@ -364,6 +446,11 @@ def main():
         drv.minibatch(next_vw())
     torch.cuda.synchronize()
     ms, launches = st.read_timing()
+    if args.per_layer:
+        # the same records give either view: K more steps for the per-layer one
+        for _ in range(args.steps):
+            drv.minibatch(next_vw())
+        layer_fwd_ms, layer_bwd_ms = st.read_layer_timing()
     st.set_timing(False)
     ums, ulaunch = drv.ps.read_timing()
     drv.ps.set_timing(False)
@@ -406,6 +493,9 @@ def main():
                     if wave_rates else None),
         "wsp_update_roofline": update_roofline(st.P, ums, ulaunch),
     }
+    if args.per_layer:
+        out["per_layer"] = per_layer_rooflines(layer_work(layers, wl.batch, wl.H, wl.W, wl.C),
+                                               layer_fwd_ms, layer_bwd_ms, args.steps, peak)
     drv.close()
     st.close()
     torch.cuda.synchronize()

@@ -128,6 +128,12 @@ struct StageTimer {
         cur = cat;
         if (cur_a) (void)hipEventRecord(cur_a, s);
     }
+    // drop the open record: the layer launched nothing of its own
+    void cancel() {
+        if (!on || !cur_a) return;
+        pool.push_back(cur_a);
+        cur_a = nullptr;
+    }
     void end(hipStream_t s) {
         if (!on || !cur_a) return;
         hipEvent_t b = take();
@@ -717,7 +723,9 @@ extern "C" int hp_stage_forward(hp_stage* st, const float* w, const float* x, fl
                 vis.y16_ready = true;
             }
         }
-        tm.begin(L.kind == HP_CONV || L.kind == HP_FC ? 0 : 1, s);
+        // a ReLU applied in its producer's epilogue launches nothing: no record
+        const bool launches = !(L.kind == HP_RELU && nd.relu_fused);
+        if (launches) tm.begin(L.kind == HP_CONV || L.kind == HP_FC ? 0 : 1, s);
         switch (L.kind) {
             case HP_CONV:
             case HP_FC: {
@@ -782,7 +790,7 @@ extern "C" int hp_stage_forward(hp_stage* st, const float* w, const float* x, fl
                 break;
             }
         }
-        tm.end(s);
+        if (launches) tm.end(s);
         int rc = launch_ok(e, "forward", (int)i);
         if (rc) return rc;
     }
@@ -920,11 +928,13 @@ extern "C" int hp_stage_backward(hp_stage* st, const float* w, const float* dy, 
                 const bool into_bn = nd.relu_fused && st->nodes[L.in0].L.kind == HP_BN;
                 if (nd.bwd_by_consumer) {
                     // already applied by the consumer's data-gradient write
+                    st->timer.cancel();
                 } else if (into_bn) {
                     // the BN backward applies the ReLU mask itself: hand it this gradient
                     Node& pr = st->nodes[L.in0];
                     pr.g_alias = gin;
                     pr.g_written = true;
+                    st->timer.cancel();
                 } else if (dest(L.in0, &d, &acc)) {
                     e = launch_relu_bwd(nd.y, gin, d, nd.out_elems, acc, s);
                 }
@@ -962,6 +972,7 @@ extern "C" int hp_stage_backward(hp_stage* st, const float* w, const float* dy, 
                 // nothing else reads takes it as its own without a copy (its
                 // backward only reads it; the layers that wrote it are done),
                 // unless it is the caller's dy.
+                bool copied = false;
                 auto route = [&](int j, int side) -> hipError_t {
                     if (j >= 0 && gin != dy && st->nodes[j].consumers == 1 &&
                         !st->nodes[j].g_written) {
@@ -975,11 +986,15 @@ extern "C" int hp_stage_backward(hp_stage* st, const float* w, const float* dy, 
                         st->nodes[j].g_shared = true;
                         return hipSuccess;
                     }
-                    if (dest(j, &d, &acc)) return launch_copy_or_acc(gin, d, nd.out_elems, acc, s);
+                    if (dest(j, &d, &acc)) {
+                        copied = true;
+                        return launch_copy_or_acc(gin, d, nd.out_elems, acc, s);
+                    }
                     return hipSuccess;
                 };
                 e = route(L.in0, 0);
                 if (e == hipSuccess) e = route(L.in1, 1);
+                if (!copied) st->timer.cancel();    // both inputs took the buffer
                 break;
             }
             case HP_GAP:

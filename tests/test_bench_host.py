@@ -63,3 +63,32 @@ def test_cpu_baseline_only_runs_the_oracle_without_a_gpu():
     d = json.loads(r.stdout.strip().splitlines()[-1])
     assert d["kind"] == "oracle" and d["cores"] == 1 and d["value"] > 0
     assert d["unit"] == "images/s" and "2 image(s)" in d["sample"]
+
+
+def test_per_layer_work_sums_to_the_step_flop():
+    # the per-layer forward and backward FLOP add up to the step's
+    # contraction FLOP, for every workload's layer list
+    b = _bench()
+    sys.path.insert(0, ROOT)
+    from paper_2005_14038_amd import workloads
+    for name, wl in workloads.WORKLOADS.items():
+        layers = wl.builder().layers
+        rows = b.layer_work(layers, wl.batch, wl.H, wl.W, wl.C)
+        assert len(rows) == len(layers)
+        total = sum(r["fwd_flop"] + r["bwd_flop"] for r in rows)
+        assert total == b.contraction_flops(layers, wl.batch, wl.H, wl.W, wl.C), name
+        assert all(r["fwd_bytes"] > 0 and r["bwd_bytes"] > 0 for r in rows), name
+
+
+def test_per_layer_rooflines_fractions():
+    b = _bench()
+    rows = [{"layer": 0, "op": "conv", "out": [1, 1, 8], "fwd_flop": 2e9, "bwd_flop": 4e9,
+             "fwd_bytes": 1e6, "bwd_bytes": 2e6},
+            {"layer": 1, "op": "relu", "out": [1, 1, 8], "fwd_flop": 0, "bwd_flop": 0,
+             "fwd_bytes": 8e6, "bwd_bytes": 8e6}]
+    out = b.per_layer_rooflines(rows, [0.2, 0.0], [0.4, 0.0], 10, 157.3)
+    assert [e["pass"] for e in out] == ["fwd", "bwd"]      # the ReLU launched nothing
+    e = out[0]
+    assert abs(e["TFLOP/s"] - 2e9 / 0.02e-3 / 1e12) < 1e-6
+    assert abs(e["attainable"] - 1.0) < 1e-9              # 2000 FLOP/B is above the ridge
+    assert e["bound"] == "mfma"
