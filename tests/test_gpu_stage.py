@@ -127,3 +127,111 @@ def test_stage_protocol_errors(dev):  # noqa: F811
     with pytest.raises(hp.HPError) as e:
         hp.Stage(bad, 2, 16, 16, 3)
     assert e.value.code == hp.HP_ERR_ARG
+
+
+def random_graph(seed):
+    """A seeded small residual network: convs (1x1 and 3x3, with and without
+    batch norm and ReLU), bottleneck blocks with identity or projection
+    shortcuts (the stage input among them), a value read by two convs whose
+    outputs are added, max-pools; with or without a loss head.  It exercises
+    the gradient hand-over between layers (aliases, shared shortcut buffers,
+    ReLU masks applied by consumers) on graphs no fixed network has."""
+    rng = np.random.default_rng(6000 + seed)
+    H = int(rng.choice([8, 10, 12]))
+    C = int(rng.choice([8, 16]))
+    n = onets.Net(f"rnd{seed}", H, H, C)
+    cur = -1
+    for _ in range(int(rng.integers(2, 5))):
+        kind = str(rng.choice(["plain", "res", "proj", "pool", "fan"]))
+        if kind == "pool" and n._shape(cur)[0] < 4:
+            kind = "plain"
+        if kind == "plain":
+            K, R = int(rng.choice([8, 16, 24])), int(rng.choice([1, 3]))
+            a = n.conv(cur, C, K, R, 1, R // 2, bias=bool(rng.integers(0, 2)))
+            if rng.random() < 0.7:
+                a = n.bn(a, K)
+            if rng.random() < 0.7:
+                a = n.relu(a)
+            cur, C = a, K
+        elif kind in ("res", "proj"):
+            K = C if kind == "res" else int(rng.choice([8, 16, 32]))
+            mid = int(rng.choice([8, 16]))
+            b = n.relu(n.bn(n.conv(cur, C, mid, 1), mid))
+            b = n.relu(n.bn(n.conv(b, mid, mid, 3, 1, 1), mid))
+            b = n.bn(n.conv(b, mid, K, 1), K)
+            sc = cur if K == C and kind == "res" else n.bn(n.conv(cur, C, K, 1), K)
+            cur = n.relu(n.addn(b, sc) if rng.random() < 0.5 else n.addn(sc, b))
+            C = K
+        elif kind == "pool":
+            cur = n.maxpool(cur, 2, 2)
+        else:                                   # fan-out into two convs, then add
+            K = int(rng.choice([8, 16]))
+            a = n.bn(n.conv(cur, C, K, 3, 1, 1), K)
+            b = n.bn(n.conv(cur, C, K, 1), K)
+            cur = n.relu(n.addn(a, b))
+            C = K
+    if rng.random() < 0.5:
+        n.ce(n.fc(n.gap(cur), C, 10), 10)
+    return n
+
+
+def _segments(net, v):
+    """(label, values, exactly zero in exact arithmetic) per parameter segment:
+    the bias of a conv read only by batch norms has a zero gradient, since a
+    batch norm's input gradient sums to zero over each channel."""
+    readers = {}
+    for j, nd in enumerate(net.nodes):
+        for src in (nd.get("in"), nd.get("in2")):
+            if src is not None:
+                readers.setdefault(src, []).append(nd["op"])
+    out, off = [], 0
+    for i, name, shape, _ in net.param_segments():
+        k = int(np.prod(shape))
+        zero = (name == "b" and net.nodes[i]["op"] == "conv" and
+                all(op == "bn" for op in readers.get(i, ["-"])))
+        out.append((f"layer {i} {name}", v[off:off + k], zero))
+        off += k
+    return out
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+@pytest.mark.parametrize("seed", range(12))
+def test_random_residual_graph(dev, seed, dtype):  # noqa: F811
+    # judged normwise per output, input gradient and parameter segment against
+    # max(floor, 2x the oracle's own movement under a small relative weight
+    # perturbation): batch norm over as few as 8 values makes some of these
+    # graphs ill-conditioned (floor and perturbation: 1e-3 and 1e-5 in fp32,
+    # 2e-2 and 1e-7 in bf16, as for the fixed networks)
+    net = random_graph(seed)
+    B = 2 + seed % 2
+    bf16 = dtype == "bf16"
+    floor, rel = (BF16_TOL, 1e-7) if bf16 else (FP32_TOL, 1e-5)
+    w = oracle_weights(net, 90 + seed, scale_bn=True)
+    x, lab, dy = make_inputs(net, B, 91 + seed, dy_std=1e-3)
+    g = run_gpu(net, B, w, x, lab, dy, True, dtype)
+    r = run_oracle(net, w, x, lab, dy, True, bf16=bf16)
+    rng = np.random.default_rng(1)
+    w1 = np.asarray(w, np.float64) * (1 + rel * rng.standard_normal(len(w)))
+    r1 = run_oracle(net, w1, x, lab, dy, True, bf16=bf16)
+    pairs = [("output", g["y"], r["y"], r1["y"], False),
+             ("input gradient", g["dx"], r["dx"], r1["dx"], False)]
+    for (what, a, zero), (_, b, _), (_, c, _) in zip(_segments(net, g["grad"]),
+                                                    _segments(net, r["grad"]),
+                                                    _segments(net, r1["grad"])):
+        pairs.append((what, a, b, c, zero))
+    gnorm = float(np.linalg.norm(np.asarray(r["grad"], np.float64)))
+    for what, a, b, c, zero in pairs:
+        if zero:
+            # round-off around an exact zero on both sides: judged against the
+            # stage gradient's size (the sums are fp32 in both modes)
+            d = float(np.linalg.norm(np.asarray(a, np.float64)))
+            assert d <= 1e-6 * gnorm, (f"graph {seed} {dtype} {what}: {d:.3e} away from its exact "
+                                       f"zero, {d / gnorm:.3e} of the gradient's norm")
+            continue
+        if not np.any(np.asarray(b) != 0):
+            np.testing.assert_array_equal(np.asarray(a), 0, err_msg=f"{what} should be zero")
+            continue
+        e, sens = norm_err(a, b), norm_err(c, b)
+        bound = max(floor, 2 * sens)
+        assert e <= bound, (f"graph {seed} {dtype} {what}: normwise error {e:.3e} > {bound:.3e} "
+                            f"(oracle self-sensitivity {sens:.3e})")
