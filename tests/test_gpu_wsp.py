@@ -80,6 +80,28 @@ def test_wsp_bit_exact(dev, case):  # noqa: F811
     drv.close()
 
 
+def random_wsp_case(seed):
+    """A seeded WSP configuration: 1-5 virtual workers of random periods,
+    s_local 0-4, D 0-3, 2-5 waves, parameter counts with and without a
+    vector tail, input or toy gradients."""
+    rng = np.random.default_rng(7000 + seed)
+    N = int(rng.integers(1, 6))
+    return (int(rng.choice([1, 3, 5, 63, 64, 1000, 4097, 65539])), N, int(rng.integers(0, 5)),
+            int(rng.integers(0, 4)), int(rng.integers(2, 6)),
+            [int(v) for v in rng.integers(1, 4, size=N)], float(rng.choice([0.01, 0.1, 0.5])),
+            bool(rng.integers(0, 2)))
+
+
+RANDOM_CASES = [random_wsp_case(s) for s in range(20)]
+
+
+@pytest.mark.parametrize("case", RANDOM_CASES,
+                         ids=[f"rnd{i}-P{c[0]}_N{c[1]}_W{c[2]+1}_D{c[3]}"
+                              for i, c in enumerate(RANDOM_CASES)])
+def test_wsp_bit_exact_random(dev, case):  # noqa: F811
+    test_wsp_bit_exact(dev, case)
+
+
 def test_wsp_protocol_errors(dev):  # noqa: F811
     P = 64
     w0 = to_dev(np.zeros(P, np.float32), dev)
