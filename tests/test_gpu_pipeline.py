@@ -137,3 +137,72 @@ def test_window_full_is_an_error(dev):  # noqa: F811
     torch.cuda.synchronize()
     vw.close()
     ps.close()
+
+
+def random_builder(seed):
+    """A seeded small residual network with a loss head (convs with and
+    without batch norm and ReLU, identity and projection shortcuts, fan-out of
+    one value into two convs, max-pools)."""
+    rng = np.random.default_rng(8000 + seed)
+    H = int(rng.choice([8, 12]))
+    b = nets.Builder(H, H, int(rng.choice([8, 16])))
+    cur = -1
+    for _ in range(int(rng.integers(2, 5))):
+        C = b.shape[cur][2]
+        kind = str(rng.choice(["plain", "res", "proj", "pool", "fan"]))
+        if kind == "pool" and b.shape[cur][0] < 4:
+            kind = "plain"
+        if kind == "plain":
+            R = int(rng.choice([1, 3]))
+            a = b.conv(cur, int(rng.choice([8, 16, 24])), R, 1, R // 2,
+                       bias=bool(rng.integers(0, 2)))
+            if rng.random() < 0.7:
+                a = b.bn(a)
+            if rng.random() < 0.7:
+                a = b.relu(a)
+            cur = a
+        elif kind in ("res", "proj"):
+            K = C if kind == "res" else int(rng.choice([8, 16, 32]))
+            mid = int(rng.choice([8, 16]))
+            x = b.relu(b.bn(b.conv(cur, mid, 1)))
+            x = b.relu(b.bn(b.conv(x, mid, 3, 1, 1)))
+            x = b.bn(b.conv(x, K, 1))
+            sc = cur if K == C and kind == "res" else b.bn(b.conv(cur, K, 1))
+            cur = b.relu(b.add(x, sc) if rng.random() < 0.5 else b.add(sc, x))
+        elif kind == "pool":
+            cur = b.maxpool(cur, 2, 2)
+        else:
+            K = int(rng.choice([8, 16]))
+            cur = b.relu(b.add(b.bn(b.conv(cur, K, 3, 1, 1)), b.bn(b.conv(cur, K, 1))))
+    b.ce(b.fc(b.gap(cur), 10))
+    return b
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+@pytest.mark.parametrize("seed", range(8))
+def test_random_graph_pipeline_equals_sequential(dev, seed, dtype):  # noqa: F811
+    # random valid cuts of a random residual network: the pipelined VW must
+    # reproduce the sequential one bit for bit
+    b = random_builder(seed)
+    H, W, C = b.input_shape
+    rng = np.random.default_rng(9000 + seed)
+    valid = pl.valid_cuts(b.layers)
+    k = min(len(valid) + 1, int(rng.integers(2, 5)))
+    cuts = sorted(int(c) for c in rng.choice(valid, size=k - 1, replace=False)) if k > 1 else []
+    B = 4
+    w0 = si.initial_weights(workloads.param_segments(b.layers), 100 + seed)
+    data = _data(b, B, 101 + seed, 10, dev)
+    wt = torch.from_numpy(w0).to(dev)
+    pv = pl.PipelinedVW(b.layers, B, H, W, C, wt, 2, 0.05, data, cuts, dtype=dtype)
+    pv.run(2)
+    torch.cuda.synchronize()
+    st = hp.Stage(b.layers, B, H, W, C, dtype=dtype)
+    drv = WSPDriver(st, wt, 1, 2, 0, 0.05, data)
+    drv.run(2)
+    torch.cuda.synchronize()
+    assert pv.k == k, (pv.k, k, cuts)
+    _assert_same_state(pv, drv, st.P, 3)
+    assert _split_events(pv.events) == _split_events(drv.events)
+    pv.close()
+    drv.close()
+    st.close()
