@@ -110,6 +110,22 @@ def test_fc(dev, case):  # noqa: F811
     assert_close(g["dx"], r["dx"], FP32_TOL, "data gradient")
 
 
+def random_fc(seed):
+    """A seeded FC geometry: batch 1-32, an input flattened from a small map,
+    output widths on and off the tile edges."""
+    rng = np.random.default_rng(3000 + seed)
+    return (int(rng.integers(1, 33)), int(rng.integers(1, 4)), int(rng.integers(1, 4)),
+            int(rng.choice([1, 3, 16, 37, 64, 130])), int(rng.choice([1, 10, 64, 100, 257, 1000])))
+
+
+RANDOM_FC = [random_fc(s) for s in range(12)]
+
+
+@pytest.mark.parametrize("case", RANDOM_FC, ids=[f"rnd{i}-{c}" for i, c in enumerate(RANDOM_FC)])
+def test_fc_random_geometry(dev, case):  # noqa: F811
+    test_fc(dev, case)
+
+
 POOL = [(2, 8, 8, 4, 2, 2, 0), (2, 9, 7, 6, 3, 2, 1), (1, 11, 11, 64, 3, 2, 1)]
 
 
