@@ -7,9 +7,10 @@ update + wave accumulation, and at every wave end the push and the gated pull
 against the parameter server in device memory.  Inputs (a pool of seeded
 minibatches) are resident in HBM before the timed region starts.
 
-Default workload: VGG-19 stage 1 (conv1_1 .. conv3_4 with two max-pools),
-batch 32 of 224x224x3 fp32 images, upstream gradient N(0, 1e-3^2), one
-virtual worker with s_local = 3.
+Default workload: the full VGG-19 as a single-stage virtual worker (16 3x3
+convolutions, FC 25088 -> 4096 -> 4096 -> 1000, softmax cross-entropy), batch
+32 of 224x224x3 fp32 images, four virtual workers with s_local = 3 and clock
+bound D = 0 -- the largest of the five workloads.
 
 Prints one JSON line: metric, value = images/s over K timed steps run exactly
 as a user runs them, the roofline of the dominant kernel class (the
@@ -36,10 +37,11 @@ HBM_PEAK_GBS = 8000.0
 METRIC = "stage-step images/sec (fwd+bwd+WSP update); % of MFMA peak, HBM GB/s"
 
 
-def contraction_flops(layers, batch, H, W, C):
+def contraction_flops(layers, batch, H, W, C, need_dx=False):
     """Algorithmic FLOPs (2 per multiply-add) of one stage step's conv / FC
     contractions: forward, weight gradient, and data gradient except for a
-    layer that reads the stage input (the image needs no gradient)."""
+    layer that reads the stage input when the stage needs no input gradient
+    (a first stage: the image needs none)."""
     from paper_2005_14038_amd.hetpipe import HP_CONV, HP_FC
     shape = {-1: (H, W, C)}
     total = 0
@@ -50,11 +52,11 @@ def contraction_flops(layers, batch, H, W, C):
             P = (h + 2 * d["pad"] - d["R"]) // d["stride"] + 1
             Q = (w + 2 * d["pad"] - d["S"]) // d["stride"] + 1
             macs = batch * P * Q * d["K"] * d["R"] * d["S"] * c
-            total += 2 * macs * (2 if d.get("in0", i - 1) < 0 else 3)
+            total += 2 * macs * (2 if d.get("in0", i - 1) < 0 and not need_dx else 3)
             shape[i] = (P, Q, d["K"])
         elif k == HP_FC:
             macs = batch * d["K"] * d["C"]
-            total += 2 * macs * (2 if d.get("in0", i - 1) < 0 else 3)
+            total += 2 * macs * (2 if d.get("in0", i - 1) < 0 and not need_dx else 3)
             shape[i] = (1, 1, d["K"])
         elif k == 4:   # max-pool
             P = (h + 2 * d["pad"] - d["R"]) // d["stride"] + 1
@@ -71,10 +73,11 @@ LAYER_NAMES = {1: "conv", 2: "fc", 3: "relu", 4: "maxpool", 5: "batchnorm", 6: "
                7: "gap", 8: "softmax_ce"}
 
 
-def layer_work(layers, batch, H, W, C):
+def layer_work(layers, batch, H, W, C, need_dx=False):
     """Per layer: output shape and the algorithmic FLOP and bytes of its forward
     and backward passes (every tensor read or written once per pass, 4 bytes an
-    element; a layer reading the stage input computes no data gradient)."""
+    element; a layer reading the stage input computes no data gradient unless
+    the stage hands one back)."""
     shape = {-1: (H, W, C)}
     rows = []
     for i, d in enumerate(layers):
@@ -92,7 +95,7 @@ def layer_work(layers, batch, H, W, C):
                 out, wts = (1, 1, d["K"]), d["K"] * d["C"]
             n_out = batch * out[0] * out[1] * out[2]
             macs = n_out * (wts // d["K"])
-            dgrad = src >= 0
+            dgrad = src >= 0 or need_dx
             f_flop, b_flop = 2 * macs, 2 * macs * (2 if dgrad else 1)
             f_el = n_in + wts + n_out
             b_el = (n_out + n_in + wts) * (2 if dgrad else 1)
@@ -174,7 +177,12 @@ def measured_traffic(workload):
 #   other local updates:          read g, w_newest, u~; write w_new, u~  20 B
 #   wave push:                    read w_g, u~; write w_g                12 B
 #   pull:                         read w_g; write the ring slot           8 B
-UPDATE_BYTES_PER_PARAM = {"update_first": 16, "update": 20, "push": 12, "pull": 8}
+#   fused wave end that pulls:    read g, u~, w_g; write u~, w_g, slot   24 B
+#   fused wave end, no pull:      read g, w_newest, u~, w_g;
+#                                 write w_new, u~, w_g                   28 B
+# (a wave of one minibatch reads no u~: 4 B less for the fused wave ends)
+UPDATE_BYTES_PER_PARAM = {"update_first": 16, "update": 20, "push": 12, "pull": 8,
+                          "wave_end_pull": 24, "wave_end": 28}
 
 
 def update_roofline(P, ms, launches):
@@ -330,7 +338,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=4)
-    ap.add_argument("--workload", default="vgg19_s1")
+    ap.add_argument("--workload", default="vgg19")
     ap.add_argument("--pool", type=int, default=2, help="distinct minibatches resident in HBM")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-images", type=int, default=4,
@@ -404,7 +412,8 @@ def main():
     def data(n, q):
         return pool[(n, (q - 1) % args.pool)]
 
-    drv = WSPDriver(st, w0, wl.N, wl.s_local, wl.D, wl.lr, data, periods=wl.periods)
+    drv = WSPDriver(st, w0, wl.N, wl.s_local, wl.D, wl.lr, data, periods=wl.periods,
+                    need_dx=wl.need_dx)
     order = []
 
     def next_vw():
@@ -457,7 +466,7 @@ def main():
 
     ms_step = max(wall, ev_ms / 1e3) * 1e3 / args.steps
     value = wl.batch * args.steps / (max(wall, ev_ms / 1e3))
-    flops_step = contraction_flops(layers, wl.batch, wl.H, wl.W, wl.C)
+    flops_step = contraction_flops(layers, wl.batch, wl.H, wl.W, wl.C, need_dx=wl.need_dx)
     gemm_ms_step = ms["contraction"] / args.steps
     achieved = flops_step / (gemm_ms_step * 1e-3) / 1e12
     peak = PEAK_TFLOPS[wl.dtype]
@@ -476,10 +485,12 @@ def main():
         "dtype": "f32" if wl.dtype == "fp32" else "bf16",
         "data": "synthetic",
         "config": {"workload": f"{wl.name}: batch {wl.batch} x {wl.H}x{wl.W}x{wl.C}, "
-                               f"{wl.N} virtual worker(s), s_local {wl.s_local}, D {wl.D}",
+                               f"{wl.N} virtual worker(s), s_local {wl.s_local}, D {wl.D}"
+                               + (", input gradient" if wl.need_dx else ""),
                    "global_batch": wl.batch, "parallelism": "single GPU, simulated VWs"},
         "roofline": {"bound": "mfma", "achieved": round(achieved, 3), "peak": peak,
                      "unit": "TFLOP/s", "frac": round(achieved / peak, 4), "traffic": traffic,
+                     "frac_of_bf16_peak": round(achieved / PEAK_TFLOPS["bf16"], 4),
                      "kernel": "implicit-GEMM conv/FC contractions (all launches of a step)",
                      "timing": f"HIP events around every launch, {args.steps} further steps",
                      "flop_per_step": flops_step, "ms_per_step": round(gemm_ms_step, 4),
@@ -494,7 +505,8 @@ def main():
         "wsp_update_roofline": update_roofline(st.P, ums, ulaunch),
     }
     if args.per_layer:
-        out["per_layer"] = per_layer_rooflines(layer_work(layers, wl.batch, wl.H, wl.W, wl.C),
+        out["per_layer"] = per_layer_rooflines(layer_work(layers, wl.batch, wl.H, wl.W, wl.C,
+                                                          need_dx=wl.need_dx),
                                                layer_fwd_ms, layer_bwd_ms, args.steps, peak)
     drv.close()
     st.close()

@@ -156,14 +156,15 @@ int hp_ps_destroy(hp_ps *ps);
 int hp_ps_weights(const hp_ps *ps, const float **wg);
 int hp_ps_clock(const hp_ps *ps, int *c_global);
 /* Device timing of the WSP update kernels, for profiling.  While enabled,
- * every kernel enqueued by hp_wsp_local_update, hp_wsp_push_wave and
- * hp_wsp_pull of this server's virtual workers is bracketed by HIP events on
- * the server's stream.  hp_ps_read_timing synchronises the stream, returns the
- * summed device time in milliseconds and the launch counts of [0] local
- * updates whose minibatch starts a wave, [1] the other local updates, [2]
- * wave pushes, [3] pulls that copied w_g, and resets the sums. */
+ * every kernel enqueued by hp_wsp_local_update, hp_wsp_push_wave, hp_wsp_pull
+ * and hp_wsp_wave_end of this server's virtual workers is bracketed by HIP
+ * events on the server's stream.  hp_ps_read_timing synchronises the stream,
+ * returns the summed device time in milliseconds and the launch counts of [0]
+ * local updates whose minibatch starts a wave, [1] the other local updates,
+ * [2] wave pushes, [3] pulls that copied w_g, [4] fused wave ends that pulled,
+ * [5] fused wave ends that did not pull, and resets the sums. */
 int hp_ps_set_timing(hp_ps *ps, int enable);
-int hp_ps_read_timing(hp_ps *ps, double ms[4], int64_t launches[4]);
+int hp_ps_read_timing(hp_ps *ps, double ms[6], int64_t launches[6]);
 
 /* ======================================================= virtual worker */
 
@@ -200,7 +201,14 @@ int hp_vw_set_momentum(hp_vw *vw, float mu);
  *   u = (-lr) * grad;  ring[(q-1) mod W] = ring[(q-2) mod W] + u;
  *   u~ = u (first minibatch of a wave) or u~ + u,
  * and advances p.  `grad` is caller-owned (P floats).
- * Errors: HP_ERR_STATE if no minibatch is in flight. */
+ * A wave end is settled before the next minibatch completes: after the update
+ * that completes wave c, hp_wsp_push_wave and a successful hp_wsp_pull come
+ * before the next hp_wsp_local_update.  The in-flight minibatches of wave c+1
+ * may run their forward and backward passes meanwhile (Sec. 5: s_local
+ * minibatches of the next wave proceed while the VW waits); only their
+ * completion waits, so each includes exactly the updates 1 .. q-W.
+ * Errors: HP_ERR_STATE if no minibatch is in flight, a completed wave has not
+ * been pushed, or the pull after the push has not succeeded. */
 int hp_wsp_local_update(hp_vw *vw, const float *grad, float lr);
 
 /* Push at the end of wave c (Sec. 5): w_g = w_g + u~, the VW's local clock
@@ -217,6 +225,24 @@ int hp_wsp_push_wave(hp_vw *vw, hp_ps *ps);
  * minibatch until a later hp_wsp_pull returns HP_OK, after other VWs pushed.
  * Never blocks the host thread.  A call with no pending gate returns HP_OK. */
 int hp_wsp_pull(hp_vw *vw, hp_ps *ps);
+
+/* Wave end in one call (Sec. 5, "Workings of WSP"): the local update of the
+ * oldest in-flight minibatch q, which must complete a wave (q mod W = 0), the
+ * push of that wave's aggregate u~ and the clock-bound gate, with the device
+ * work of all three in one streaming pass over the parameters.  The results
+ * -- ring, u~, w_g, clocks, version vectors, status -- are bit for bit those
+ * of hp_wsp_local_update, hp_wsp_push_wave and hp_wsp_pull called in turn
+ * (same fp32 operations, same order, no fused multiply-add); momentum, when
+ * set, is applied as in hp_wsp_local_update.  When the gate opens at once
+ * the new ring version is w_g itself and the newest version is not read
+ * (24 bytes per parameter: read grad, u~, w_g; write u~, w_g, the ring slot).
+ * Otherwise the slot gets the local version (28 bytes per parameter), and if
+ * the gate is closed the call returns HP_WOULD_BLOCK exactly as hp_wsp_pull
+ * does: retry hp_wsp_pull after other VWs pushed.  `grad` is caller-owned
+ * (P floats); `ps` must be the VW's server.
+ * Errors: HP_ERR_STATE if no minibatch is in flight, the oldest one does not
+ * complete a wave, or an earlier wave end is unsettled. */
+int hp_wsp_wave_end(hp_vw *vw, hp_ps *ps, const float *grad, float lr);
 
 /* Host-side bookkeeping of a VW (exact integers). */
 typedef struct hp_wsp_state {

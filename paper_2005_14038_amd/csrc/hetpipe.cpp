@@ -1068,9 +1068,9 @@ extern "C" int hp_ps_set_timing(hp_ps* ps, int enable) {
     return HP_OK;
 }
 
-extern "C" int hp_ps_read_timing(hp_ps* ps, double ms[4], int64_t launches[4]) {
+extern "C" int hp_ps_read_timing(hp_ps* ps, double ms[6], int64_t launches[6]) {
     if (!ps || !ms || !launches) return fail(HP_ERR_ARG, "hp_ps_read_timing: NULL argument");
-    return read_timer(ps->timer, ps->stream, 4, ms, launches);
+    return read_timer(ps->timer, ps->stream, 6, ms, launches);
 }
 
 // ========================================================== virtual worker
@@ -1167,6 +1167,14 @@ extern "C" int hp_wsp_local_update(hp_vw* v, const float* grad, float lr) {
     if (!v->ps) return fail(HP_ERR_STATE, "hp_wsp_local_update: parameter server destroyed");
     if (v->inflight == 0)
         return fail(HP_ERR_STATE, "hp_wsp_local_update: no minibatch was started (hp_wsp_weights)");
+    // a completed wave is pushed, and its gate passed, before the next
+    // minibatch completes: the first update of a wave overwrites u~, and the
+    // pull writes the ring slot the next completion would write
+    if (v->push_due)
+        return fail(HP_ERR_STATE, "hp_wsp_local_update: wave %d of VW %d not pushed yet",
+                    (int)(v->p / v->W) - 1, v->id);
+    if (v->need_pull)
+        return fail(HP_ERR_STATE, "hp_wsp_local_update: VW %d is gated by the clock bound", v->id);
     const int64_t q = v->p + 1;
     const int W = v->W;
     const int slot = (int)((q - 1) % W);
@@ -1228,6 +1236,57 @@ extern "C" int hp_wsp_pull(hp_vw* v, hp_ps* ps) {
     for (int n = 0; n < ps->N; ++n) v->V[slot][n] = (int64_t)v->W * ps->pushed[n];
     v->g = ps->cg;
     v->need_pull = false;
+    return HP_OK;
+}
+
+extern "C" int hp_wsp_wave_end(hp_vw* v, hp_ps* ps, const float* grad, float lr) {
+    if (!v || !ps || !grad) return fail(HP_ERR_ARG, "hp_wsp_wave_end: NULL argument");
+    if (v->ps != ps) return fail(HP_ERR_ARG, "hp_wsp_wave_end: VW belongs to another server");
+    if (v->inflight == 0)
+        return fail(HP_ERR_STATE, "hp_wsp_wave_end: no minibatch was started (hp_wsp_weights)");
+    if (v->push_due || v->need_pull)
+        return fail(HP_ERR_STATE, "hp_wsp_wave_end: VW %d has an unsettled wave end", v->id);
+    const int64_t q = v->p + 1;
+    const int W = v->W;
+    if (q % W != 0)
+        return fail(HP_ERR_STATE, "hp_wsp_wave_end: minibatch %lld does not complete a wave",
+                    (long long)q);
+    const int slot = (int)((q - 1) % W);
+    const int newest = (int)((q - 2 + W) % W);
+    const int first = ((q - 1) % W) == 0;
+    // the gate after the push, decided on the host before anything is enqueued
+    const int c_new = (int)(q / W);
+    int cg_new = c_new;
+    for (int n = 0; n < ps->N; ++n)
+        if (n != v->id) cg_new = std::min(cg_new, ps->clock[n]);
+    const int need = c_new - ps->D;
+    const bool satisfied = v->g >= need;
+    const bool pull = !satisfied && cg_new >= need;
+    StageTimer& tm = ps->timer;
+    tm.begin(pull ? 4 : 5, ps->stream);
+    hipError_t e = launch_wsp_wave_end(grad, v->ring + (size_t)newest * v->stride,
+                                       v->ring + (size_t)slot * v->stride, v->ut,
+                                       v->mu != 0.f ? v->vel : nullptr, ps->wg, v->P, lr, v->mu,
+                                       first, pull ? 1 : 0, ps->stream);
+    tm.end(ps->stream);
+    if (e != hipSuccess) return fail(HP_ERR_HIP, "wave-end launch: %s", hipGetErrorString(e));
+    // bookkeeping of the local update, the push and the gate, in that order
+    std::vector<int64_t> nv = v->V[newest];
+    nv[v->id] += 1;
+    v->V[slot] = nv;
+    v->p = q;
+    v->inflight -= 1;
+    ps->pushed[v->id] += 1;
+    v->c = c_new;
+    ps->clock[v->id] = c_new;
+    ps->cg = *std::min_element(ps->clock.begin(), ps->clock.end());
+    if (satisfied) return HP_OK;
+    if (!pull) {
+        v->need_pull = true;
+        return HP_WOULD_BLOCK;
+    }
+    for (int n = 0; n < ps->N; ++n) v->V[slot][n] = (int64_t)W * ps->pushed[n];
+    v->g = ps->cg;
     return HP_OK;
 }
 

@@ -177,5 +177,10 @@ hipError_t launch_wsp_local_update_momentum(const float* g, const float* newest,
 hipError_t launch_wsp_push(float* wg, const float* ut, size_t n, hipStream_t s);
 // dst = src
 hipError_t launch_wsp_copy(const float* src, float* dst, size_t n, hipStream_t s);
+// wave end fused: the local update (momentum when vel != nullptr), then
+// w_g = w_g + u~, then dst = w_g (pull != 0) or dst = newest + u
+hipError_t launch_wsp_wave_end(const float* g, const float* newest, float* dst, float* ut,
+                               float* vel, float* wg, size_t n, float lr, float mu, int first,
+                               int pull, hipStream_t s);
 
 }  // namespace hp

@@ -1,4 +1,5 @@
-// WSP update kernels (gfx950): local update + wave accumulation, push, pull.
+// WSP update kernels (gfx950): local update + wave accumulation, push, pull,
+// and the three fused at a wave end.
 //
 // All three stream flat fp32 parameter vectors once, so they are HBM-bound:
 // float4 accesses (four per thread per iteration on long vectors, all loads
@@ -208,6 +209,103 @@ copy_kernel(const float* __restrict__ src, float* __restrict__ dst, size_t n, in
         dst[i] = src[i];
 }
 
+// Wave end in one pass: the local update of the minibatch that completes a
+// wave, the push of the wave's aggregate and, when the clock-bound gate opens
+// at once, the pull.  Per element, in this order (the order of the three
+// separate kernels above, so the results are bit-identical to them):
+//   (momentum) v = mu * v + g;   u = (-lr) * (g or v);
+//   u~ = u or u~ + u;   w_g = w_g + u~;
+//   slot = w_g (PULL)  or  newest + u.
+// With PULL the newest ring version is not read: the pull replaces the
+// slot's new version by w_g.  Bytes per parameter: read g, u~ (unless FIRST),
+// w_g, newest (unless PULL), v (MOM); write u~, w_g, the slot, v (MOM).
+template <bool FIRST, bool PULL, bool MOM, int U>
+__global__ void __launch_bounds__(WSP_THREADS)
+wave_end_kernel(const float* __restrict__ g, const float* newest, float* dst,
+                float* __restrict__ ut, float* __restrict__ vel, float* __restrict__ wg,
+                size_t n, float neg_lr, float mu, int vec) {
+    const size_t n4 = vec ? n / 4 : 0;
+    const float4* g4 = reinterpret_cast<const float4*>(g);
+    const float4* w4 = reinterpret_cast<const float4*>(newest);
+    float4* d4 = reinterpret_cast<float4*>(dst);
+    float4* u4 = reinterpret_cast<float4*>(ut);
+    float4* v4 = reinterpret_cast<float4*>(vel);
+    float4* s4 = reinterpret_cast<float4*>(wg);
+    WSP_VECTOR_LOOP(n4) {
+        float4 gv[U], wv[U], av[U], vv[U], sv[U];
+#pragma unroll
+        for (int k = 0; k < U; ++k) {
+            const size_t i = base + (size_t)k * blockDim.x;
+            if (i < n4) {
+                gv[k] = ld4(g4 + i);
+                if (!PULL) wv[k] = ld4(w4 + i);
+                if (!FIRST) av[k] = ld4(u4 + i);
+                if (MOM) vv[k] = ld4(v4 + i);
+                sv[k] = ld4(s4 + i);
+            }
+        }
+#pragma unroll
+        for (int k = 0; k < U; ++k) {
+            const size_t i = base + (size_t)k * blockDim.x;
+            if (i >= n4) break;
+            float4 d = gv[k];
+            if (MOM) {
+                d.x = add_rn(mul_rn(mu, vv[k].x), gv[k].x);
+                d.y = add_rn(mul_rn(mu, vv[k].y), gv[k].y);
+                d.z = add_rn(mul_rn(mu, vv[k].z), gv[k].z);
+                d.w = add_rn(mul_rn(mu, vv[k].w), gv[k].w);
+                v4[i] = d;
+            }
+            float4 u;
+            u.x = mul_rn(neg_lr, d.x); u.y = mul_rn(neg_lr, d.y);
+            u.z = mul_rn(neg_lr, d.z); u.w = mul_rn(neg_lr, d.w);
+            if (!PULL) {
+                float4 nw;
+                nw.x = add_rn(wv[k].x, u.x); nw.y = add_rn(wv[k].y, u.y);
+                nw.z = add_rn(wv[k].z, u.z); nw.w = add_rn(wv[k].w, u.w);
+                d4[i] = nw;
+            }
+            float4 a = u;
+            if (!FIRST) {
+                a.x = add_rn(av[k].x, u.x); a.y = add_rn(av[k].y, u.y);
+                a.z = add_rn(av[k].z, u.z); a.w = add_rn(av[k].w, u.w);
+            }
+            u4[i] = a;
+            float4 w = sv[k];
+            w.x = add_rn(w.x, a.x); w.y = add_rn(w.y, a.y);
+            w.z = add_rn(w.z, a.z); w.w = add_rn(w.w, a.w);
+            s4[i] = w;
+            if (PULL) d4[i] = w;
+        }
+    }
+    for (size_t i = n4 * 4 + (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
+        float d = g[i];
+        if (MOM) {
+            d = add_rn(mul_rn(mu, vel[i]), g[i]);
+            vel[i] = d;
+        }
+        const float u = mul_rn(neg_lr, d);
+        if (!PULL) dst[i] = add_rn(newest[i], u);
+        const float a = FIRST ? u : add_rn(ut[i], u);
+        ut[i] = a;
+        const float w = add_rn(wg[i], a);
+        wg[i] = w;
+        if (PULL) dst[i] = w;
+    }
+}
+
+template <bool FIRST, bool PULL, bool MOM>
+void launch_wave_end_t(dim3 grid, dim3 block, int u, hipStream_t s, const float* g,
+                       const float* newest, float* dst, float* ut, float* vel, float* wg,
+                       size_t n, float neg_lr, float mu, int vec) {
+    if (u == 4)
+        hipLaunchKernelGGL((wave_end_kernel<FIRST, PULL, MOM, 4>), grid, block, 0, s, g, newest,
+                           dst, ut, vel, wg, n, neg_lr, mu, vec);
+    else
+        hipLaunchKernelGGL((wave_end_kernel<FIRST, PULL, MOM, 1>), grid, block, 0, s, g, newest,
+                           dst, ut, vel, wg, n, neg_lr, mu, vec);
+}
+
 inline int aligned16(const void* a, const void* b, const void* c = nullptr,
                      const void* d = nullptr) {
     uintptr_t u = (uintptr_t)a | (uintptr_t)b | (uintptr_t)c | (uintptr_t)d;
@@ -282,6 +380,32 @@ hipError_t launch_wsp_copy(const float* src, float* dst, size_t n, hipStream_t s
         hipLaunchKernelGGL(copy_kernel<4>, grid, block, 0, s, src, dst, n, vec);
     else
         hipLaunchKernelGGL(copy_kernel<1>, grid, block, 0, s, src, dst, n, vec);
+    return hipGetLastError();
+}
+
+hipError_t launch_wsp_wave_end(const float* g, const float* newest, float* dst, float* ut,
+                               float* vel, float* wg, size_t n, float lr, float mu, int first,
+                               int pull, hipStream_t s) {
+    const float neg_lr = -lr;
+    const bool mom = vel != nullptr;
+    const int vec = aligned16(g, newest, dst, ut) && aligned16(wg, mom ? vel : wg);
+    const size_t n4 = vec ? n / 4 : n;
+    const int u = wsp_unroll(n4);
+    const dim3 grid(wsp_blocks(n4, u)), block(WSP_THREADS);
+    const int sel = (first ? 4 : 0) | (pull ? 2 : 0) | (mom ? 1 : 0);
+#define HP_WAVE_END(F, P, M) \
+    launch_wave_end_t<F, P, M>(grid, block, u, s, g, newest, dst, ut, vel, wg, n, neg_lr, mu, vec)
+    switch (sel) {
+        case 0: HP_WAVE_END(false, false, false); break;
+        case 1: HP_WAVE_END(false, false, true); break;
+        case 2: HP_WAVE_END(false, true, false); break;
+        case 3: HP_WAVE_END(false, true, true); break;
+        case 4: HP_WAVE_END(true, false, false); break;
+        case 5: HP_WAVE_END(true, false, true); break;
+        case 6: HP_WAVE_END(true, true, false); break;
+        default: HP_WAVE_END(true, true, true); break;
+    }
+#undef HP_WAVE_END
     return hipGetLastError();
 }
 

@@ -5,7 +5,8 @@ the local updates 1..q-W, HetPipe Sec. 4), hp_stage_forward and
 hp_stage_backward at those weights, hp_wsp_local_update (u = -lr g, or with
 momentum u = -lr v, v = mu v + g; ring write, wave accumulation; lr may
 change per minibatch, e.g. the sigma/sqrt(t) schedule of Theorem 1), and at a wave end hp_wsp_push_wave followed by
-hp_wsp_pull, the clock-distance gate of Sec. 5.  A VW whose pull reports
+hp_wsp_pull, the clock-distance gate of Sec. 5 -- by default the three at a
+wave end as one call, hp_wsp_wave_end (bit-identical results).  A VW whose pull reports
 HP_WOULD_BLOCK stops until another VW's push lets its pull succeed.
 
 Scheduling (the paper leaves it open; virtual workers are independent
@@ -32,7 +33,7 @@ class Deadlock(RuntimeError):
 class WSPDriver:
     def __init__(self, stage: Stage, w0: torch.Tensor, N: int, s_local: int, D: int, lr,
                  data_fn, periods=None, stream=None, need_dx=False, on_minibatch=None,
-                 grad_fn=None, P=None, momentum=0.0):
+                 grad_fn=None, P=None, momentum=0.0, fused=True):
         # grad_fn(n, q, w_ptr, grad): fill `grad` without a stage (WSP-only runs)
         self.stage = stage
         self.grad_fn = grad_fn
@@ -62,6 +63,9 @@ class WSPDriver:
         self.done = [0] * N
         self.events = []
         self.on_minibatch = on_minibatch
+        # a wave's last minibatch: local update + push + gate in one call
+        # (hp_wsp_wave_end), or the three calls in turn
+        self.fused = fused
 
     def close(self):
         for v in self.vws:
@@ -86,9 +90,12 @@ class WSPDriver:
             self.stage.backward(w, dy, self.dx, self.grad)
         if self.on_minibatch is not None:
             self.on_minibatch(n, q, self)
-        vw.local_update(self.grad, self.lr(n, q))
-        if q % self.W == 0:
-            self._push_and_gate(n)
+        if q % self.W == 0 and self.fused:
+            self._push_and_gate(n, self.lr(n, q))
+        else:
+            vw.local_update(self.grad, self.lr(n, q))
+            if q % self.W == 0:
+                self._push_and_gate(n)
         self.t[n] += self.T[n]
         self.done[n] = q
 
@@ -96,13 +103,20 @@ class WSPDriver:
         s = self.vws[m].state()
         self.events.append(("pull", m, s["g"]))
 
-    def _push_and_gate(self, n):
+    def _push_and_gate(self, n, lr=None):
+        """Push of VW n's completed wave and its gate; with lr given, the wave's
+        last local update, the push and the gate in one call (hp_wsp_wave_end)."""
         vw = self.vws[n]
-        vw.push_wave()
+        g0 = vw.state()["g"]
+        if lr is not None:
+            ok = vw.wave_end(self.grad, lr)
+        else:
+            vw.push_wave()
         s = vw.state()
         self.events.append(("push", n, s["c"], self.ps.clock()))
-        g0 = s["g"]
-        if vw.pull():
+        if lr is None:
+            ok = vw.pull()
+        if ok:
             if vw.state()["g"] != g0:
                 self._pulled(n)
         else:

@@ -31,8 +31,8 @@ EXPORTS = [
     "hp_ps_read_timing",
     "hp_vw_create", "hp_vw_destroy", "hp_vw_set_momentum", "hp_wsp_weights",
     "hp_wsp_local_update",
-    "hp_wsp_push_wave", "hp_wsp_pull", "hp_wsp_state", "hp_wsp_version", "hp_wsp_buffers",
-    "hp_last_error",
+    "hp_wsp_push_wave", "hp_wsp_pull", "hp_wsp_wave_end", "hp_wsp_state", "hp_wsp_version",
+    "hp_wsp_buffers", "hp_last_error",
 ]
 
 
@@ -89,8 +89,8 @@ def lib():
     L.hp_ps_weights.argtypes = [_vp, _pp]
     L.hp_ps_clock.argtypes = [_vp, ctypes.POINTER(i32)]
     L.hp_ps_set_timing.argtypes = [_vp, i32]
-    L.hp_ps_read_timing.argtypes = [_vp, ctypes.POINTER(ctypes.c_double * 4),
-                                    ctypes.POINTER(ctypes.c_int64 * 4)]
+    L.hp_ps_read_timing.argtypes = [_vp, ctypes.POINTER(ctypes.c_double * 6),
+                                    ctypes.POINTER(ctypes.c_int64 * 6)]
     L.hp_vw_create.argtypes = [_vp, i32, i32, _pp]
     L.hp_vw_destroy.argtypes = [_vp]
     L.hp_vw_set_momentum.argtypes = [_vp, ctypes.c_float]
@@ -98,6 +98,7 @@ def lib():
     L.hp_wsp_local_update.argtypes = [_vp, _vp, ctypes.c_float]
     L.hp_wsp_push_wave.argtypes = [_vp, _vp]
     L.hp_wsp_pull.argtypes = [_vp, _vp]
+    L.hp_wsp_wave_end.argtypes = [_vp, _vp, _vp, ctypes.c_float]
     L.hp_wsp_state.argtypes = [_vp, ctypes.POINTER(hp_wsp_state_t)]
     L.hp_wsp_version.argtypes = [_vp, ctypes.POINTER(ctypes.c_int64)]
     L.hp_wsp_buffers.argtypes = [_vp, _pp, ctypes.POINTER(sz), _pp]
@@ -253,7 +254,7 @@ class ParameterServer:
         _check(self._L.hp_ps_clock(self.h, ctypes.byref(c)))
         return c.value
 
-    TIMING_CLASSES = ("update_first", "update", "push", "pull")
+    TIMING_CLASSES = ("update_first", "update", "push", "pull", "wave_end_pull", "wave_end")
 
     def set_timing(self, on=True):
         _check(self._L.hp_ps_set_timing(self.h, 1 if on else 0))
@@ -261,8 +262,8 @@ class ParameterServer:
     def read_timing(self):
         """({class: ms}, {class: launches}) of the WSP update kernels for the
         classes in TIMING_CLASSES; resets the sums."""
-        ms = (ctypes.c_double * 4)()
-        n = (ctypes.c_int64 * 4)()
+        ms = (ctypes.c_double * 6)()
+        n = (ctypes.c_int64 * 6)()
         _check(self._L.hp_ps_read_timing(self.h, ctypes.byref(ms), ctypes.byref(n)))
         return ({k: ms[i] for i, k in enumerate(self.TIMING_CLASSES)},
                 {k: int(n[i]) for i, k in enumerate(self.TIMING_CLASSES)})
@@ -300,6 +301,14 @@ class VirtualWorker:
 
     def push_wave(self):
         _check(self._L.hp_wsp_push_wave(self.h, self.ps.h))
+
+    def wave_end(self, grad, lr):
+        """Local update + push + gate of a wave's last minibatch in one call
+        (hp_wsp_wave_end).  Returns True if the VW may proceed, False if the
+        clock bound blocks it (then pull() until it returns True)."""
+        rc = _check(self._L.hp_wsp_wave_end(self.h, self.ps.h, _ptr(grad), ctypes.c_float(lr)),
+                    allow=(HP_OK, HP_WOULD_BLOCK))
+        return rc == HP_OK
 
     def pull(self):
         """Returns True if the VW may proceed, False if the clock bound blocks it."""

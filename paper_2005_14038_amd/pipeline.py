@@ -403,16 +403,18 @@ class PipelinedVW:
         """Minibatch m completed: local update, push / pull at a wave end, then
         the next minibatch enters."""
         self._wait(self.ps_stream, ("B", m, 0))
-        self.vw.local_update(self.grads[slot], self.lr(0, m))
         if m % self.W == 0:
-            self.vw.push_wave()
+            # local update + push + gate in one call (hp_wsp_wave_end)
+            g0 = self.vw.state()["g"]
+            ok = self.vw.wave_end(self.grads[slot], self.lr(0, m))
             s = self.vw.state()
             self.events.append(("push", 0, s["c"], self.ps.clock()))
-            g0 = s["g"]
-            if not self.vw.pull():
+            if not ok:
                 raise RuntimeError("a single VW cannot be blocked by the clock bound")
-            if self.vw.state()["g"] != g0:
-                self.events.append(("pull", 0, self.vw.state()["g"]))
+            if s["g"] != g0:
+                self.events.append(("pull", 0, s["g"]))
+        else:
+            self.vw.local_update(self.grads[slot], self.lr(0, m))
         self._record(("U", m), self.ps_stream)
         self.completed = m
         for key in [k for k in self.done_ev if k[1] == m and k[0] != "U"]:

@@ -39,6 +39,9 @@ class Workload:
     classes: int = 0
     net_kw: dict = field(default_factory=dict)
     seed: int = SEED
+    # a middle stage hands the gradient of its input back to the previous
+    # stage (Sec. 3), so its step computes dx; a first stage reads the image
+    need_dx: bool = False
 
     def builder(self):
         return nets.by_name(self.net, **self.net_kw)
@@ -56,7 +59,7 @@ WORKLOADS = {
     "vgg19": Workload("vgg19", "vgg19", 32, 224, 224, 3, N=4, s_local=3, D=0, waves=2, lr=0.01,
                       classes=1000, periods=[1, 1, 1, 1]),
     "resnet152_mid": Workload("resnet152_mid", "resnet152_mid", 32, 56, 56, 256, N=1, s_local=4,
-                              D=0, waves=3, lr=0.1, dy_std=1e-3, periods=[1]),
+                              D=0, waves=3, lr=0.1, dy_std=1e-3, periods=[1], need_dx=True),
     "resnet152": Workload("resnet152", "resnet152", 32, 224, 224, 3, N=4, s_local=3, D=1,
                           waves=5, lr=0.01, dtype="bf16", classes=1000, periods=[1, 1, 1, 2]),
 }

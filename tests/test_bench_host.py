@@ -73,10 +73,11 @@ def test_per_layer_work_sums_to_the_step_flop():
     from paper_2005_14038_amd import workloads
     for name, wl in workloads.WORKLOADS.items():
         layers = wl.builder().layers
-        rows = b.layer_work(layers, wl.batch, wl.H, wl.W, wl.C)
+        rows = b.layer_work(layers, wl.batch, wl.H, wl.W, wl.C, need_dx=wl.need_dx)
         assert len(rows) == len(layers)
         total = sum(r["fwd_flop"] + r["bwd_flop"] for r in rows)
-        assert total == b.contraction_flops(layers, wl.batch, wl.H, wl.W, wl.C), name
+        assert total == b.contraction_flops(layers, wl.batch, wl.H, wl.W, wl.C,
+                                            need_dx=wl.need_dx), name
         assert all(r["fwd_bytes"] > 0 and r["bwd_bytes"] > 0 for r in rows), name
 
 
@@ -92,3 +93,22 @@ def test_per_layer_rooflines_fractions():
     assert abs(e["TFLOP/s"] - 2e9 / 0.02e-3 / 1e12) < 1e-6
     assert abs(e["attainable"] - 1.0) < 1e-9              # 2000 FLOP/B is above the ridge
     assert e["bound"] == "mfma"
+
+
+def test_step_flop_of_the_five_workloads():
+    """Contraction FLOP per minibatch step (2 per multiply-add; forward, data
+    gradient and weight gradient; no data gradient for the layer reading the
+    image; the ResNet-152 middle stage hands its input gradient back), from
+    the per-image forward multiply-adds of the networks: 0.36 M, 11.18 G,
+    19.63 G, 9.92 G, 11.51 G."""
+    b = _bench()
+    sys.path.insert(0, ROOT)
+    from paper_2005_14038_amd import workloads
+    want = {"tiny": 8.2e6, "vgg19_s1": 2.142e12, "vgg19": 3.764e12,
+            "resnet152_mid": 1.904e12, "resnet152": 2.203e12}
+    for name, wl in workloads.WORKLOADS.items():
+        f = b.contraction_flops(wl.builder().layers, wl.batch, wl.H, wl.W, wl.C,
+                                need_dx=wl.need_dx)
+        assert abs(f / want[name] - 1) < 2e-3, (name, f)
+    assert workloads.WORKLOADS["resnet152_mid"].need_dx
+    assert not any(w.need_dx for n, w in workloads.WORKLOADS.items() if n != "resnet152_mid")

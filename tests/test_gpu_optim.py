@@ -33,8 +33,9 @@ CASES = [
 ]
 
 
+@pytest.mark.parametrize("fused", [False, True], ids=["separate", "fused"])
 @pytest.mark.parametrize("case", CASES, ids=[f"P{c[0]}_N{c[1]}_mu{c[7]}_{c[6]}" for c in CASES])
-def test_optimizer_variants_bit_exact(dev, case):  # noqa: F811
+def test_optimizer_variants_bit_exact(dev, case, fused):  # noqa: F811
     P, N, s_local, D, waves, periods, step, mu, toy = case
     W = s_local + 1
     Q = waves * W
@@ -56,7 +57,7 @@ def test_optimizer_variants_bit_exact(dev, case):  # noqa: F811
             grad[:P].copy_(dtab[(n, q)])
 
     drv = WSPDriver(None, to_dev(w0, dev), N, s_local, D, lr, None, periods=periods,
-                    grad_fn=gfn, P=P, momentum=mu)
+                    grad_fn=gfn, P=P, momentum=mu, fused=fused)
     drv.run(waves)
     torch.cuda.synchronize()
     assert drv.events == ref.events

@@ -76,7 +76,7 @@ def test_tiny_complete_wsp_run(dev):  # noqa: F811
         for s in range(wl.s_local + 1):
             assert_close(hp.read_vector(ring + 4 * s * stride, st.P), ref.ring[n][s], FP32_TOL,
                          f"VW {n} ring slot {s}")
-        assert_close(hp.read_vector(ut, st.P), ref.ut[n], 1e-2, f"VW {n} u~")
+        assert_close(hp.read_vector(ut, st.P), ref.ut[n], FP32_TOL, f"VW {n} u~")
     drv.close()
     st.close()
 
@@ -94,11 +94,14 @@ def test_workload_event_log_and_finiteness(dev, name):  # noqa: F811
     def check(n, q, drv):
         g = drv.grad[:st.P]
         assert torch.isfinite(g).all().item(), (n, q)
+        if wl.need_dx:
+            assert torch.isfinite(drv.dx).all().item() and drv.dx.abs().max().item() > 0, (n, q)
         if wl.has_loss:
             losses.append(float(drv.loss.item()))
 
     drv = WSPDriver(st, torch.from_numpy(w0).to(dev), wl.N, wl.s_local, wl.D, wl.lr,
-                    _device_data(wl, out_shape, dev), periods=wl.periods, on_minibatch=check)
+                    _device_data(wl, out_shape, dev), periods=wl.periods, on_minibatch=check,
+                    need_dx=wl.need_dx)
     drv.run(wl.waves)
     torch.cuda.synchronize()
     # the bookkeeping does not depend on the gradient values: compare with the

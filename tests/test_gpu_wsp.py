@@ -35,8 +35,11 @@ def grads_table(P, N, Q, seed=99):
             for n in range(N) for q in range(1, Q + 1)}
 
 
+@pytest.mark.parametrize("fused", [False, True], ids=["separate", "fused"])
 @pytest.mark.parametrize("case", CASES, ids=[f"P{c[0]}_N{c[1]}_W{c[2]+1}_D{c[3]}" for c in CASES])
-def test_wsp_bit_exact(dev, case):  # noqa: F811
+def test_wsp_bit_exact(dev, case, fused):  # noqa: F811
+    """fused: each wave's last minibatch goes through hp_wsp_wave_end (local
+    update + push + gate in one pass) instead of the three calls in turn."""
     P, N, s_local, D, waves, periods, lr, toy = case
     W = s_local + 1
     Q = waves * W
@@ -61,8 +64,15 @@ def test_wsp_bit_exact(dev, case):  # noqa: F811
             grad[:P].copy_(dtab[(n, q)])
 
     drv = WSPDriver(None, to_dev(w0, dev), N, s_local, D, lr, None, periods=periods,
-                    grad_fn=gfn, P=P)
+                    grad_fn=gfn, P=P, fused=fused)
+    drv.ps.set_timing(True)
     drv.run(waves)
+    _, launches = drv.ps.read_timing()
+    drv.ps.set_timing(False)
+    # every wave end took the path asked for
+    wave_ends = sum(1 for e in ref.events if e[0] == "push")
+    assert launches["push"] == (0 if fused else wave_ends)
+    assert launches["wave_end_pull"] + launches["wave_end"] == (wave_ends if fused else 0)
     torch.cuda.synchronize()
     assert drv.events == ref.events
     wg = hetpipe.read_vector(drv.ps.weights_ptr(), P)
@@ -98,8 +108,9 @@ RANDOM_CASES = [random_wsp_case(s) for s in range(20)]
 @pytest.mark.parametrize("case", RANDOM_CASES,
                          ids=[f"rnd{i}-P{c[0]}_N{c[1]}_W{c[2]+1}_D{c[3]}"
                               for i, c in enumerate(RANDOM_CASES)])
-def test_wsp_bit_exact_random(dev, case):  # noqa: F811
-    test_wsp_bit_exact(dev, case)
+@pytest.mark.parametrize("fused", [False, True], ids=["separate", "fused"])
+def test_wsp_bit_exact_random(dev, case, fused):  # noqa: F811
+    test_wsp_bit_exact(dev, case, fused)
 
 
 def test_wsp_protocol_errors(dev):  # noqa: F811
@@ -139,6 +150,52 @@ def test_wsp_protocol_errors(dev):  # noqa: F811
     assert ps.clock() == 1
     assert v1.pull() is True and v0.pull() is True
     v0.weights()
+    v1.close(); v0.close(); ps.close()
+
+
+def test_completion_waits_for_the_wave_end(dev):  # noqa: F811
+    """W minibatches in flight at a wave end (the pipelined case of Sec. 5): the
+    next completion is refused until the finished wave is pushed and its gate
+    passes, so u~ still holds the whole wave when it is pushed and the pull
+    writes the ring slot no completion has written yet."""
+    P, W = 96, 3
+    w0 = to_dev(np.zeros(P, np.float32), dev)
+    ones = torch.ones(P, dtype=torch.float32, device=dev)
+    ps = hetpipe.ParameterServer(P, w0, 2, 0)
+    v0 = hetpipe.VirtualWorker(ps, 0, W - 1)
+    v1 = hetpipe.VirtualWorker(ps, 1, W - 1)
+    for _ in range(W):                          # minibatches 1..W in flight
+        v0.weights()
+    for q in range(1, W + 1):                   # complete wave 0 ...
+        v0.local_update(ones * q, 1.0)
+        if q < W:
+            v0.weights()                        # ... while W-1 later ones start
+    assert v0.state()["in_flight"] == W - 1 and v0.state()["push_due"]
+    with pytest.raises(hetpipe.HPError) as e:   # completion before the push
+        v0.local_update(ones, 1.0)
+    assert e.value.code == hetpipe.HP_ERR_STATE
+    v0.push_wave()
+    assert v0.pull() is False                   # D = 0: VW 1 has not pushed wave 0
+    with pytest.raises(hetpipe.HPError) as e:   # completion while gated
+        v0.local_update(ones, 1.0)
+    assert e.value.code == hetpipe.HP_ERR_STATE
+    assert v0.state()["p"] == W
+    for _ in range(W):
+        v1.weights()
+        v1.local_update(ones * 10, 1.0)
+    v1.push_wave()
+    assert v1.pull() is True and v0.pull() is True
+    # w_g = -(1 + 2 + ... + W) - 10 W, and the pulled slot (read by minibatch
+    # 2W) holds it; the minibatches W+1 .. 2W-1 in flight now complete
+    want = -(W * (W + 1) / 2) - 10.0 * W
+    np.testing.assert_array_equal(hetpipe.read_vector(ps.weights_ptr(), P),
+                                  np.full(P, want, np.float32))
+    ring, stride, ut = v0.buffers()
+    np.testing.assert_array_equal(hetpipe.read_vector(ring + 4 * (W - 1) * stride, P),
+                                  np.full(P, want, np.float32))
+    for _ in range(W - 1):
+        v0.local_update(ones, 1.0)
+    assert v0.state()["p"] == 2 * W - 1
     v1.close(); v0.close(); ps.close()
 
 

@@ -146,3 +146,71 @@ def test_bf16_mode_within_rounding_bound():
     # the bf16 result is exactly the fp64 contraction of the rounded operands
     y_r = ops.conv_fwd(round_bf16(x), round_bf16(w), None, 1, 1)
     np.testing.assert_array_equal(y16, y_r)
+
+
+def _forward_macs_per_image(net):
+    """Multiply-adds of one image's forward pass, summed over the conv and FC
+    nodes from each node's own output shape (P x Q x K outputs, R x S x C
+    multiply-adds each; an FC has IN x OUT)."""
+    total = 0
+    for i, nd in enumerate(net.nodes):
+        if nd["op"] == "conv":
+            P, Q, K = net.shapes[i]
+            total += P * Q * K * nd["R"] * nd["S"] * nd["C"]
+        elif nd["op"] == "fc":
+            total += nd["IN"] * nd["OUT"]
+    return total
+
+
+def test_forward_multiply_adds_per_image_pin_the_graphs():
+    """The forward multiply-adds per 224x224 image are fixed by the
+    architectures: VGG-19 19.63 G (the commonly quoted 19.6 G), ResNet-152 with
+    its stride on the 3x3 convolution 11.51 G (the original placement on the
+    first 1x1, quoted as 11.3 G, gives 11.28 G), the VGG-19 stage 1 and the
+    ResNet-152 middle stage their shares of those.  The parameter counts cannot
+    tell the two ResNet placements apart; the multiply-adds can."""
+    want = {"tiny": 360_448, "vgg19_s1": 11_184_832_512, "vgg19": 19_632_062_464,
+            "resnet152_mid": 9_916_383_232, "resnet152": 11_513_626_624}
+    for name, macs in want.items():
+        assert _forward_macs_per_image(nets.by_name(name)) == macs, name
+    # the stage shares add up: stage 1 is conv1_1 .. conv3_4 of VGG-19
+    v = nets.vgg19()
+    s1 = nets.vgg19_s1()
+    assert [n for n in v.nodes[:len(s1.nodes)]] == s1.nodes
+    # a ResNet-152 with the stride on the first 1x1 of each downsampling block
+    # has the same parameters but fewer multiply-adds
+    n = nets.Net("r152_v1", 224, 224, 3)
+    a = n.relu(n.bn(n.conv(-1, 3, 64, 7, 2, 3), 64))
+    a = n.maxpool(a, 3, 2, 1)
+    c = 64
+    for mid, blocks, stride in nets._RESNET152_GROUPS:
+        for bi in range(blocks):
+            s = stride if bi == 0 else 1
+            out = 4 * mid
+            b = n.relu(n.bn(n.conv(a, c, mid, 1, s), mid))
+            b = n.relu(n.bn(n.conv(b, mid, mid, 3, 1, 1), mid))
+            b = n.bn(n.conv(b, mid, out, 1), out)
+            sc = n.bn(n.conv(a, c, out, 1, s), out) if bi == 0 else a
+            a, c = n.relu(n.addn(b, sc)), out
+    n.fc(n.gap(a), c, 1000)
+    assert n.param_count() == nets.resnet152().param_count()
+    assert _forward_macs_per_image(n) == 11_282_415_616
+    assert _forward_macs_per_image(n) != _forward_macs_per_image(nets.resnet152())
+
+
+def test_stage_boundaries_of_the_middle_and_first_stages():
+    """VGG-19 stage 1 ends at conv3_4's ReLU (pool3 belongs to the next stage);
+    the ResNet-152 middle stage is conv3_x + conv4_x: 8 + 36 bottlenecks, two
+    of them with projection shortcuts, 56x56x256 in, 14x14x1024 out."""
+    s1 = nets.vgg19_s1()
+    assert sum(nd["op"] == "conv" for nd in s1.nodes) == 8
+    assert sum(nd["op"] == "maxpool" for nd in s1.nodes) == 2
+    assert s1.nodes[-1]["op"] == "relu" and s1.out_shape == (56, 56, 256)
+    m = nets.resnet152_mid()
+    adds = [nd for nd in m.nodes if nd["op"] == "add"]
+    assert len(adds) == 44
+    convs = [nd for nd in m.nodes if nd["op"] == "conv"]
+    assert len(convs) == 3 * 44 + 2
+    strided = [nd for nd in convs if nd["stride"] == 2]
+    # one 3x3 and one projection per downsampling block
+    assert sorted((nd["R"], nd["C"]) for nd in strided) == [(1, 256), (1, 512), (3, 128), (3, 256)]
