@@ -145,6 +145,27 @@ int hp_stage_forward(hp_stage *st, const float *w, const float *x, float *y,
  * Errors: HP_ERR_STATE if no forward preceded or `w` differs from it. */
 int hp_stage_backward(hp_stage *st, const float *w, const float *dy, float *dx, float *grad);
 
+/* Read-only device pointers to the buffers in which the stage holds layer
+ * `layer`'s forward value and the gradient of the loss with respect to it, for
+ * inspection (the layer-by-layer check of a real graph against a reference).
+ * Both are [batch][H][W][C] fp32 (hp_stage_output_shape), owned by the stage
+ * (or the caller, where noted), and valid until the next forward / backward
+ * pass on the stage's stream.
+ *   value: the layer's output from the last hp_stage_forward; NULL for the
+ *          loss head and for a conv / FC / batch norm / add whose consumer
+ *          ReLU it applies itself (its buffer holds the ReLU's output, which
+ *          the ReLU layer reports).  Layer -1: the caller's stage input x.
+ *   grad:  dL/d(value) from the last hp_stage_backward (the caller's dy for
+ *          the last layer of a stage without loss head, the loss head's
+ *          gradient for the logits); NULL where no buffer holds it after the
+ *          pass: a ReLU whose mask its consumer applied, a batch norm that
+ *          applies its consumer ReLU, an add whose buffer became its identity
+ *          shortcut's gradient, a value no gradient reaches, or before any
+ *          backward pass.  Layer -1: the caller's dx (NULL if none was asked).
+ * Errors: HP_ERR_ARG for a NULL argument or a layer outside -1 .. n-1. */
+int hp_stage_layer_buffers(const hp_stage *st, int layer, const float **value,
+                           const float **grad);
+
 /* ==================================================== parameter server */
 
 /* Create the parameter server for N virtual workers with clock-distance

@@ -59,6 +59,9 @@ struct Node {
     float* y = nullptr;                 // forward output (a fused ReLU aliases its producer)
     float* g = nullptr;                 // gradient of the output
     bool g_written = false;
+    // after a backward pass: the buffer holding the gradient of this value
+    // (NULL where none does: see hp_stage_layer_buffers)
+    const float* g_final = nullptr;
     const float* g_alias = nullptr;     // gradient handed over without a copy (ReLU -> BN, add -> sole-consumer input)
     bool g_shared = false;              // g_alias is a buffer this value's other consumers accumulate into
     bool add_share[2] = {false, false}; // (add) input 0 / 1 may take this gradient buffer as its own
@@ -188,6 +191,8 @@ struct hp_stage {
     const float* fwd_w = nullptr;
     const float* fwd_x = nullptr;
     bool fwd_done = false;
+    // the last backward pass's input gradient (caller's dx, may be NULL)
+    const float* bwd_dx = nullptr;
 };
 
 struct hp_vw;
@@ -820,7 +825,9 @@ extern "C" int hp_stage_backward(hp_stage* st, const float* w, const float* dy, 
         nd.g_written = false;
         nd.g_alias = nullptr;
         nd.g_shared = false;
+        nd.g_final = nullptr;
     }
+    st->bwd_dx = nullptr;
     bool dx_written = false;
     for (Node& nd : st->nodes) nd.g16_ready = false;
     // `a` happens before everything enqueued on `b` afterwards
@@ -862,6 +869,9 @@ extern "C" int hp_stage_backward(hp_stage* st, const float* w, const float* dy, 
         else if (nd.g_alias) gin = nd.g_alias;
         else if (nd.g_written) gin = nd.g;
         else continue;   // no gradient reaches this value
+        // complete now (every consumer is done); a batch norm that applies its
+        // consumer ReLU receives the ReLU's unmasked gradient instead
+        nd.g_final = (L.kind == HP_BN && nd.fuses_relu) ? nullptr : gin;
         const float* in = L.in0 < 0 ? x : st->nodes[L.in0].y;
         hipError_t e = hipSuccess;
         float* d;
@@ -984,6 +994,7 @@ extern "C" int hp_stage_backward(hp_stage* st, const float* w, const float* dy, 
                         st->nodes[j].g_alias = gin;       // the identity shortcut's gradient
                         st->nodes[j].g_written = true;
                         st->nodes[j].g_shared = true;
+                        nd.g_final = nullptr;             // the buffer now accumulates j's
                         return hipSuccess;
                     }
                     if (dest(j, &d, &acc)) {
@@ -1006,9 +1017,34 @@ extern "C" int hp_stage_backward(hp_stage* st, const float* w, const float* dy, 
         int rc = launch_ok(e, "backward", i);
         if (rc) return rc;
     }
+    // a buffer handed to an identity shortcut as its shared gradient went on
+    // accumulating the shortcut's other consumers after the layers that only
+    // read it (the add, the add's other input) were done with it
+    for (const Node& a : st->nodes)
+        if (a.g_shared && a.g_alias)
+            for (Node& b : st->nodes)
+                if (&b != &a && b.g_final == a.g_alias) b.g_final = nullptr;
     // the caller's stream sees the complete gradient
     HP_HIP(order(st->side, s));
     st->fwd_done = false;
+    st->bwd_dx = dx_written ? dx : nullptr;
+    return HP_OK;
+}
+
+extern "C" int hp_stage_layer_buffers(const hp_stage* st, int layer, const float** value,
+                                      const float** grad) {
+    if (!st || !value || !grad) return fail(HP_ERR_ARG, "hp_stage_layer_buffers: NULL argument");
+    const int n = (int)st->nodes.size();
+    if (layer < -1 || layer >= n)
+        return fail(HP_ERR_ARG, "hp_stage_layer_buffers: no layer %d", layer);
+    if (layer == -1) {
+        *value = st->fwd_x;
+        *grad = st->bwd_dx;
+        return HP_OK;
+    }
+    const Node& nd = st->nodes[layer];
+    *value = (nd.L.kind == HP_SOFTMAX_CE || nd.fuses_relu) ? nullptr : nd.y;
+    *grad = nd.g_final;
     return HP_OK;
 }
 

@@ -26,7 +26,7 @@ EXPORTS = [
     "hp_stage_output_shape", "hp_stage_device_bytes", "hp_stage_layer_bytes",
     "hp_stage_set_timing",
     "hp_stage_read_timing", "hp_stage_read_layer_timing", "hp_stage_forward",
-    "hp_stage_backward",
+    "hp_stage_backward", "hp_stage_layer_buffers",
     "hp_ps_create", "hp_ps_destroy", "hp_ps_weights", "hp_ps_clock", "hp_ps_set_timing",
     "hp_ps_read_timing",
     "hp_vw_create", "hp_vw_destroy", "hp_vw_set_momentum", "hp_wsp_weights",
@@ -84,6 +84,7 @@ def lib():
     L.hp_stage_layer_bytes.argtypes = [_vp, _vp, i32]
     L.hp_stage_forward.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp]
     L.hp_stage_backward.argtypes = [_vp, _vp, _vp, _vp, _vp]
+    L.hp_stage_layer_buffers.argtypes = [_vp, i32, _pp, _pp]
     L.hp_ps_create.argtypes = [sz, _vp, i32, i32, _vp, _pp]
     L.hp_ps_destroy.argtypes = [_vp]
     L.hp_ps_weights.argtypes = [_vp, _pp]
@@ -222,6 +223,14 @@ class Stage:
     def forward(self, w, x, y=None, labels=None, loss=None):
         _check(self._L.hp_stage_forward(self.h, _ptr(w), _ptr(x), _ptr(y), _ptr(labels),
                                         _ptr(loss)))
+
+    def layer_buffers(self, layer):
+        """(value_ptr, grad_ptr) of layer `layer` after the last forward and
+        backward passes (hp_stage_layer_buffers); None where the stage holds
+        no such buffer."""
+        v, g = ctypes.c_void_p(), ctypes.c_void_p()
+        _check(self._L.hp_stage_layer_buffers(self.h, layer, ctypes.byref(v), ctypes.byref(g)))
+        return v.value, g.value
 
     def backward(self, w, dy, dx, grad):
         _check(self._L.hp_stage_backward(self.h, _ptr(w), _ptr(dy), _ptr(dx), _ptr(grad)))
