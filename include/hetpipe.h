@@ -145,6 +145,27 @@ int hp_stage_forward(hp_stage *st, const float *w, const float *x, float *y,
  * Errors: HP_ERR_STATE if no forward preceded or `w` differs from it. */
 int hp_stage_backward(hp_stage *st, const float *w, const float *dy, float *dx, float *grad);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the
+ * backward pass of hp_stage_backward -- same arguments, same kernels, same
+ * results bit for bit -- with its workspaces (split-reduction partial tiles,
+ * column-sum and batch-norm partials of the stage stream and of the
+ * weight-gradient stream) taken from a static device array of the library,
+ * HP_NOALLOC_SCRATCH_BYTES per device, instead of the stage's own.  Calls no
+ * allocating routine.  Every call on one GPU shares that GPU's array, so
+ * calls whose device work overlaps on one GPU (two stages on different
+ * streams, or a call enqueued before the previous one has run) race: order
+ * them on one stream.  Nothing in the array needs to start at zero: every
+ * partial is written before it is read.  Must be called with the device
+ * current on which the stage was created.
+ * Errors: as hp_stage_backward; HP_ERR_ARG if the stage's workspaces exceed
+ * HP_NOALLOC_SCRATCH_BYTES (the message gives both sizes); HP_ERR_STATE if
+ * another device is current; HP_ERR_HIP if the array's device address cannot
+ * be obtained. */
+#define HP_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+int hp_stage_backward_noalloc(hp_stage *st, const float *w, const float *dy, float *dx,
+                              float *grad);
+
 /* Read-only device pointers to the buffers in which the stage holds layer
  * `layer`'s forward value and the gradient of the loss with respect to it, for
  * inspection (the layer-by-layer check of a real graph against a reference).

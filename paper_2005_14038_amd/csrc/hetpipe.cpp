@@ -17,6 +17,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -193,6 +194,7 @@ struct hp_stage {
     bool fwd_done = false;
     // the last backward pass's input gradient (caller's dx, may be NULL)
     const float* bwd_dx = nullptr;
+    int device = 0;                 // the HIP device current at creation
 };
 
 struct hp_vw;
@@ -553,6 +555,7 @@ extern "C" int hp_stage_create(const hp_layer* layers, int n_layers, int batch, 
     if (dtype_mode != HP_FP32 && dtype_mode != HP_BF16)
         return fail(HP_ERR_ARG, "hp_stage_create: unknown dtype mode %d", dtype_mode);
     hp_stage* st = new hp_stage();
+    (void)hipGetDevice(&st->device);
     st->batch = batch; st->H = H; st->W = W; st->C = C;
     st->dtype = dtype_mode;
     st->stream = (hipStream_t)stream;
@@ -809,8 +812,13 @@ extern "C" int hp_stage_forward(hp_stage* st, const float* w, const float* x, fl
     return HP_OK;
 }
 
-extern "C" int hp_stage_backward(hp_stage* st, const float* w, const float* dy, float* dx,
-                                 float* grad) {
+namespace {
+
+// The backward pass with the workspaces of the stage stream (ws) and of the
+// weight-gradient stream (ws2) given by the caller: the stage's own, or the
+// library's static scratch (hp_stage_backward_noalloc).
+int stage_backward(hp_stage* st, const float* w, const float* dy, float* dx, float* grad,
+                   float* ws, float* ws2) {
     if (!st || !grad || (!w && st->P)) return fail(HP_ERR_ARG, "hp_stage_backward: NULL argument");
     if (!st->fwd_done) return fail(HP_ERR_STATE, "hp_stage_backward: no forward pass to differentiate");
     if (w != st->fwd_w)
@@ -896,7 +904,7 @@ extern "C" int hp_stage_backward(hp_stage* st, const float* w, const float* dy, 
                 // weight gradient (and a separate bias column sum), on the side
                 // stream once gin and its bf16 copy are complete
                 hipStream_t sd = nd.wgrad_side ? st->side : s;
-                float* wsw = nd.wgrad_side ? st->ws2 : st->ws;
+                float* wsw = nd.wgrad_side ? ws2 : ws;
                 if (e == hipSuccess && nd.wgrad_side) e = order(s, sd);
                 tm.begin(0, sd);
                 Epilogue wep;                     // bias gradient = appended column
@@ -927,7 +935,7 @@ extern "C" int hp_stage_backward(hp_stage* st, const float* w, const float* dy, 
                         dep.mask = st->nodes[L.in0].y;
                     }
                     tm.begin(0, s);
-                    e = launch_gemm(nd.dgrad, nd.geo, gin, w + nd.w_off, d, dep, st->ws, s, g16,
+                    e = launch_gemm(nd.dgrad, nd.geo, gin, w + nd.w_off, d, dep, ws, s, g16,
                                     g16 ? st->w16 + nd.w_off : nullptr,
                                     g16 && st->w16t ? st->w16t + nd.w_off : nullptr);
                     tm.end(s);
@@ -974,7 +982,7 @@ extern "C" int hp_stage_backward(hp_stage* st, const float* w, const float* dy, 
                 }
                 e = launch_bn_bwd(in, gin, nd.fuses_relu ? nd.y : nullptr, (long)B * nd.H * nd.W,
                                   nd.C, w + nd.w_off, nd.mean, nd.invstd, want ? d : nullptr,
-                                  grad + nd.w_off, grad + nd.b_off, want ? acc : 0, st->ws, s, d16);
+                                  grad + nd.w_off, grad + nd.b_off, want ? acc : 0, ws, s, d16);
                 break;
             }
             case HP_ADD: {
@@ -1029,6 +1037,75 @@ extern "C" int hp_stage_backward(hp_stage* st, const float* w, const float* dy, 
     st->fwd_done = false;
     st->bwd_dx = dx_written ? dx : nullptr;
     return HP_OK;
+}
+
+}  // namespace
+
+extern "C" int hp_stage_backward(hp_stage* st, const float* w, const float* dy, float* dx,
+                                 float* grad) {
+    if (!st) return fail(HP_ERR_ARG, "hp_stage_backward: NULL stage");
+    return stage_backward(st, w, dy, dx, grad, st->ws, st->ws2);
+}
+
+// ------------------------------------------- backward pass without allocation
+//
+// The workspaces of hp_stage_backward_noalloc: one static array per device
+// (each GPU the library runs on holds its own copy until the process ends).
+// In host code `scratch` names a host-side stand-in, not device memory: its
+// device address is taken once per device with hipGetSymbolAddress, with that
+// device current, and only that address is ever handed to kernels.
+constexpr size_t HP_SCRATCH_BYTES = HP_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) unsigned char scratch[HP_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int HP_MAX_DEVICES = 64;
+std::mutex g_scratch_mutex;
+void* g_scratch_ptr[HP_MAX_DEVICES] = {};
+
+// Device address of `scratch` on the current device (set up on first use).
+int scratch_address(int dev, void** out) {
+    if (dev < 0 || dev >= HP_MAX_DEVICES)
+        return fail(HP_ERR_ARG, "hp_stage_backward_noalloc: device %d out of range", dev);
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess || !p)
+            return fail(HP_ERR_HIP, "hipGetSymbolAddress(scratch) on device %d: %s", dev,
+                        hipGetErrorString(e));
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return HP_OK;
+}
+
+}  // namespace
+
+extern "C" int hp_stage_backward_noalloc(hp_stage* st, const float* w, const float* dy,
+                                         float* dx, float* grad) {
+    if (!st) return fail(HP_ERR_ARG, "hp_stage_backward_noalloc: NULL stage");
+    // the stage's stream workspace, then the weight-gradient stream's, each
+    // starting on a 256-byte boundary
+    const size_t ws_bytes = round_up(std::max<size_t>(st->ws_floats, 64) * sizeof(float), 256);
+    const size_t ws2_bytes = round_up(std::max<size_t>(st->ws2_floats, 64) * sizeof(float), 256);
+    if (ws_bytes + ws2_bytes > HP_SCRATCH_BYTES)
+        return fail(HP_ERR_ARG,
+                    "hp_stage_backward_noalloc: the stage needs %zu bytes of workspace, the "
+                    "static scratch holds %zu",
+                    ws_bytes + ws2_bytes, HP_SCRATCH_BYTES);
+    int cur = -1;
+    HP_HIP(hipGetDevice(&cur));
+    if (cur != st->device)
+        return fail(HP_ERR_STATE,
+                    "hp_stage_backward_noalloc: device %d is current, the stage lives on %d",
+                    cur, st->device);
+    void* base = nullptr;
+    int rc = scratch_address(cur, &base);
+    if (rc) return rc;
+    float* ws = static_cast<float*>(base);
+    float* ws2 = reinterpret_cast<float*>(static_cast<unsigned char*>(base) + ws_bytes);
+    return stage_backward(st, w, dy, dx, grad, ws, ws2);
 }
 
 extern "C" int hp_stage_layer_buffers(const hp_stage* st, int layer, const float** value,

@@ -26,7 +26,7 @@ EXPORTS = [
     "hp_stage_output_shape", "hp_stage_device_bytes", "hp_stage_layer_bytes",
     "hp_stage_set_timing",
     "hp_stage_read_timing", "hp_stage_read_layer_timing", "hp_stage_forward",
-    "hp_stage_backward", "hp_stage_layer_buffers",
+    "hp_stage_backward", "hp_stage_backward_noalloc", "hp_stage_layer_buffers",
     "hp_ps_create", "hp_ps_destroy", "hp_ps_weights", "hp_ps_clock", "hp_ps_set_timing",
     "hp_ps_read_timing",
     "hp_vw_create", "hp_vw_destroy", "hp_vw_set_momentum", "hp_wsp_weights",
@@ -85,6 +85,7 @@ def lib():
     L.hp_stage_forward.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp]
     L.hp_stage_backward.argtypes = [_vp, _vp, _vp, _vp, _vp]
     L.hp_stage_layer_buffers.argtypes = [_vp, i32, _pp, _pp]
+    L.hp_stage_backward_noalloc.argtypes = [_vp, _vp, _vp, _vp, _vp]
     L.hp_ps_create.argtypes = [sz, _vp, i32, i32, _vp, _pp]
     L.hp_ps_destroy.argtypes = [_vp]
     L.hp_ps_weights.argtypes = [_vp, _pp]
@@ -234,6 +235,11 @@ class Stage:
 
     def backward(self, w, dy, dx, grad):
         _check(self._L.hp_stage_backward(self.h, _ptr(w), _ptr(dy), _ptr(dx), _ptr(grad)))
+
+    def backward_noalloc(self, w, dy, dx, grad):
+        """hp_stage_backward_noalloc: the backward pass with the library's
+        static workspace (no device allocation)."""
+        _check(self._L.hp_stage_backward_noalloc(self.h, _ptr(w), _ptr(dy), _ptr(dx), _ptr(grad)))
 
 
 class ParameterServer:
