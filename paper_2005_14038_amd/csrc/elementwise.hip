@@ -178,7 +178,7 @@ template <int VEC>
 __global__ void maxpool_bwd_kernel(const float* __restrict__ x, const float* __restrict__ dy,
                                    float* __restrict__ dx, int N, int H, int W, int C, int R,
                                    int S, int st, int pad, int P, int Q, int acc,
-                                   const float* __restrict__ mask) {
+                                   const float* __restrict__ mask, uint16_t* __restrict__ dx16) {
     const size_t total = (size_t)N * H * W * C;
     for (size_t i = ((size_t)blockIdx.x * blockDim.x + threadIdx.x) * VEC; i < total;
          i += (size_t)gridDim.x * blockDim.x * VEC) {
@@ -239,6 +239,7 @@ __global__ void maxpool_bwd_kernel(const float* __restrict__ x, const float* __r
             for (int j = 0; j < VEC; ++j) sum[j] = d[j] + sum[j];
         }
         stv<VEC>(dx + i, sum);
+        if (dx16) st16v<VEC>(dx16 + i, sum);
     }
 }
 
@@ -249,7 +250,8 @@ template <int VEC>
 __global__ void maxpool_bwd_arg_kernel(const uint8_t* __restrict__ arg,
                                        const float* __restrict__ dy, float* __restrict__ dx,
                                        int N, int H, int W, int C, int R, int S, int st, int pad,
-                                       int P, int Q, int acc, const float* __restrict__ mask) {
+                                       int P, int Q, int acc, const float* __restrict__ mask,
+                                       uint16_t* __restrict__ dx16) {
     const size_t total = (size_t)N * H * W * C;
     for (size_t i = ((size_t)blockIdx.x * blockDim.x + threadIdx.x) * VEC; i < total;
          i += (size_t)gridDim.x * blockDim.x * VEC) {
@@ -293,6 +295,7 @@ __global__ void maxpool_bwd_arg_kernel(const uint8_t* __restrict__ arg,
             for (int j = 0; j < VEC; ++j) sum[j] = d[j] + sum[j];
         }
         stv<VEC>(dx + i, sum);
+        if (dx16) st16v<VEC>(dx16 + i, sum);
     }
 }
 
@@ -304,7 +307,8 @@ __global__ void maxpool_bwd_arg_kernel(const uint8_t* __restrict__ arg,
 template <int RT, int VEC>
 __global__ void maxpool_bwd_tiled_kernel(const float* __restrict__ x, const float* __restrict__ dy,
                                          float* __restrict__ dx, int N, int H, int W, int C, int Rr,
-                                         int P, int Q, int acc, const float* __restrict__ mask) {
+                                         int P, int Q, int acc, const float* __restrict__ mask,
+                                       uint16_t* __restrict__ dx16) {
     const int R = RT > 0 ? RT : Rr;
     const size_t total = (size_t)N * P * Q * C;
     for (size_t i = ((size_t)blockIdx.x * blockDim.x + threadIdx.x) * VEC; i < total;
@@ -341,6 +345,7 @@ __global__ void maxpool_bwd_tiled_kernel(const float* __restrict__ x, const floa
                     if (acc) o[j] = d[j] + o[j];
                 }
                 stv<VEC>(dx + e, o);
+                if (dx16) st16v<VEC>(dx16 + e, o);
             }
         } else {
             float m[VEC];
@@ -364,6 +369,7 @@ __global__ void maxpool_bwd_tiled_kernel(const float* __restrict__ x, const floa
                     if (acc) o[j] = d[j] + o[j];
                 }
                 stv<VEC>(dx + e, o);
+                if (dx16) st16v<VEC>(dx16 + e, o);
             }
         }
     }
@@ -854,38 +860,38 @@ bool maxpool_tiled(int H, int W, int R, int S, int st, int pad, int P, int Q) {
 
 hipError_t launch_maxpool_bwd(const float* x, const float* dy, float* dx, int N, int H, int W,
                               int C, int R, int S, int st, int pad, int P, int Q, int accumulate,
-                              const float* mask, hipStream_t s, const uint8_t* arg) {
-    const bool v4 = C % 4 == 0 && aligned16({x, dy, dx, mask});
+                              const float* mask, hipStream_t s, const uint8_t* arg, uint16_t* dx16) {
+    const bool v4 = C % 4 == 0 && aligned16({x, dy, dx, mask}) && ((uintptr_t)dx16 & 7) == 0;
     if (maxpool_tiled(H, W, R, S, st, pad, P, Q)) {
         size_t n = (size_t)N * P * Q * C;
         const dim3 g(ew_blocks(v4 ? n / 4 : n)), b(EW_THREADS);
         if (R == 2 && v4)
             hipLaunchKernelGGL((maxpool_bwd_tiled_kernel<2, 4>), g, b, 0, s, x, dy, dx, N, H, W, C,
-                               R, P, Q, accumulate, mask);
+                               R, P, Q, accumulate, mask, dx16);
         else if (R == 2)
             hipLaunchKernelGGL((maxpool_bwd_tiled_kernel<2, 1>), g, b, 0, s, x, dy, dx, N, H, W, C,
-                               R, P, Q, accumulate, mask);
+                               R, P, Q, accumulate, mask, dx16);
         else if (v4)
             hipLaunchKernelGGL((maxpool_bwd_tiled_kernel<0, 4>), g, b, 0, s, x, dy, dx, N, H, W, C,
-                               R, P, Q, accumulate, mask);
+                               R, P, Q, accumulate, mask, dx16);
         else
             hipLaunchKernelGGL((maxpool_bwd_tiled_kernel<0, 1>), g, b, 0, s, x, dy, dx, N, H, W, C,
-                               R, P, Q, accumulate, mask);
+                               R, P, Q, accumulate, mask, dx16);
         return hipGetLastError();
     }
     size_t n = (size_t)N * H * W * C;
     if (arg && v4)
         hipLaunchKernelGGL(maxpool_bwd_arg_kernel<4>, dim3(ew_blocks(n / 4)), dim3(EW_THREADS), 0, s,
-                           arg, dy, dx, N, H, W, C, R, S, st, pad, P, Q, accumulate, mask);
+                           arg, dy, dx, N, H, W, C, R, S, st, pad, P, Q, accumulate, mask, dx16);
     else if (arg)
         hipLaunchKernelGGL(maxpool_bwd_arg_kernel<1>, dim3(ew_blocks(n)), dim3(EW_THREADS), 0, s,
-                           arg, dy, dx, N, H, W, C, R, S, st, pad, P, Q, accumulate, mask);
+                           arg, dy, dx, N, H, W, C, R, S, st, pad, P, Q, accumulate, mask, dx16);
     else if (v4)
         hipLaunchKernelGGL(maxpool_bwd_kernel<4>, dim3(ew_blocks(n / 4)), dim3(EW_THREADS), 0, s, x,
-                           dy, dx, N, H, W, C, R, S, st, pad, P, Q, accumulate, mask);
+                           dy, dx, N, H, W, C, R, S, st, pad, P, Q, accumulate, mask, dx16);
     else
         hipLaunchKernelGGL(maxpool_bwd_kernel<1>, dim3(ew_blocks(n)), dim3(EW_THREADS), 0, s, x, dy,
-                           dx, N, H, W, C, R, S, st, pad, P, Q, accumulate, mask);
+                           dx, N, H, W, C, R, S, st, pad, P, Q, accumulate, mask, dx16);
     return hipGetLastError();
 }
 

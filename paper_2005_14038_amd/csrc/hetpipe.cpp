@@ -741,6 +741,13 @@ extern "C" int hp_stage_forward(hp_stage* st, const float* w, const float* x, fl
                 ep.flags = (L.bias ? EPI_BIAS : 0) | (nd.fuses_relu ? EPI_RELU : 0);
                 ep.bias = L.bias ? w + nd.b_off : nullptr;
                 ep.stats = nd.stats;
+                // the bf16 copy a consuming contraction reads (of the ReLU's
+                // value when this layer applies it) comes from the epilogue
+                Node& vis = nd.fuses_relu ? st->nodes[nd.relu_node] : nd;
+                if (vis.y16 && !nd.stats) {
+                    ep.out16 = vis.y16;
+                    vis.y16_ready = true;
+                }
                 if (nd.padC) {
                     // zero-padded copies of the input and the weights, then the
                     // contraction on the padded geometry
@@ -866,6 +873,17 @@ int stage_backward(hp_stage* st, const float* w, const float* dy, float* dx, flo
         return true;
     };
 
+    // the bf16 copy of value j's gradient, which j's own contractions read,
+    // written by the layer that sends j its gradient when that is the only
+    // contribution (j has one consumer and nothing was written before)
+    auto sole_grad16 = [&](int j, int acc) -> uint16_t* {
+        if (j < 0 || acc) return nullptr;
+        Node& t = st->nodes[j];
+        if (!t.g16 || t.consumers != 1 || t.g_shared) return nullptr;
+        t.g16_ready = true;
+        return t.g16;
+    };
+
     st->timer.phase = 1;
     for (int i = n - 1; i >= 0; --i) {
         Node& nd = st->nodes[i];
@@ -934,6 +952,7 @@ int stage_backward(hp_stage* st, const float* w, const float* dy, float* dx, flo
                         dep.flags |= EPI_MASK;
                         dep.mask = st->nodes[L.in0].y;
                     }
+                    dep.out16 = sole_grad16(tgt, acc);
                     tm.begin(0, s);
                     e = launch_gemm(nd.dgrad, nd.geo, gin, w + nd.w_off, d, dep, ws, s, g16,
                                     g16 ? st->w16 + nd.w_off : nullptr,
@@ -963,7 +982,8 @@ int stage_backward(hp_stage* st, const float* w, const float* dy, float* dx, flo
                 const float* mask = nd.mask_into >= 0 ? st->nodes[L.in0].y : nullptr;
                 if (dest(tgt, &d, &acc))
                     e = launch_maxpool_bwd(in, gin, d, B, nd.inH, nd.inW, nd.inC, L.R, L.S,
-                                           L.stride, L.pad, nd.H, nd.W, acc, mask, s, nd.arg);
+                                           L.stride, L.pad, nd.H, nd.W, acc, mask, s, nd.arg,
+                                           sole_grad16(tgt, acc));
                 break;
             }
             case HP_BN: {

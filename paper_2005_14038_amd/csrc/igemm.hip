@@ -81,6 +81,9 @@ struct KArgs {
     int epi;
     const unsigned short* a16;   // bf16 copies of a and b (16-bit operand kernel only)
     const unsigned short* b16;
+    // optional: every final output element is also written here rounded to
+    // bf16 (nearest even), row-major like out (no bias-gradient column)
+    unsigned short* out16;
     // weight gradient on bf16 operands: floor(i / Q) = (i * mq) >> sq and
     // floor(i / P) = (i * mp) >> sp for 0 <= i < 2^31
     unsigned mq, mp;
@@ -117,6 +120,10 @@ __device__ __forceinline__ float round_bf16(float x) {
 // Two floats rounded to bf16, packed low element first (LDS byte order).
 __device__ __forceinline__ unsigned pack_bf16(float lo, float hi) {
     return (__float_as_uint(round_bf16(lo)) >> 16) | (__float_as_uint(round_bf16(hi)) & 0xFFFF0000u);
+}
+
+__device__ __forceinline__ unsigned short bf16_bits(float x) {
+    return (unsigned short)(__float_as_uint(round_bf16(x)) >> 16);
 }
 
 // Work assignment.  The first `tfull` workgroups each compute one whole
@@ -243,6 +250,7 @@ __device__ __forceinline__ void store_tile(const KArgs& args, const Work& w,
                     if ((epi & EPI_MASK) && !(msk[u] > 0.f)) val = 0.f;
                     if (epi & EPI_ACCUM) val += prev[u];
                     obase[r * ldi] = val;
+                    if (args.out16) args.out16[(row0 + r) * args.Ncols + col] = bf16_bits(val);
                 }
             }
         }
@@ -346,8 +354,17 @@ __device__ __forceinline__ void store_tile_wide(const KArgs& args, const Work& w
                     if (full) {
                         *reinterpret_cast<float4*>(args.out + off) =
                             make_float4(o[0], o[1], o[2], o[3]);
+                        if (args.out16) {
+                            uint2 h;
+                            h.x = pack_bf16(o[0], o[1]);
+                            h.y = pack_bf16(o[2], o[3]);
+                            *reinterpret_cast<uint2*>(args.out16 + off) = h;
+                        }
                     } else {
-                        for (int e = 0; e < 4 && col + e < N; ++e) args.out[off + e] = o[e];
+                        for (int e = 0; e < 4 && col + e < N; ++e) {
+                            args.out[off + e] = o[e];
+                            if (args.out16) args.out16[off + e] = bf16_bits(o[e]);
+                        }
                     }
                 }
             }
@@ -1921,7 +1938,9 @@ igemm_splitk_reduce_kernel(KArgs args, int BM, int BN) {
         float acc = 0.f;
         for (int l = 0; l < SK_LANES; ++l) acc += red[l][el];
         float* dst = out_ptr(args.out, args.bias_out, row, col, args.Ncols, args.epi);
-        *dst = epilogue(acc, row, col, args.Ncols, args.epi, args.bias, args.mask, dst);
+        const float v = epilogue(acc, row, col, args.Ncols, args.epi, args.bias, args.mask, dst);
+        *dst = v;
+        if (args.out16) args.out16[row * args.Ncols + col] = bf16_bits(v);
     }
 }
 
@@ -1973,6 +1992,7 @@ __global__ void __launch_bounds__(256) igemm_cut_reduce_kernel(KArgs args, int B
             if ((epi & EPI_MASK) && !(args.mask[row * args.Ncols + col] > 0.f)) v = 0.f;
             if (epi & EPI_ACCUM) v += prev[j];
             *out_ptr(args.out, args.bias_out, row, col, args.Ncols, epi) = v;
+            if (args.out16) args.out16[row * args.Ncols + col] = bf16_bits(v);
         }
     }
 }
@@ -2306,6 +2326,13 @@ hipError_t launch_gemm(const GemmPlan& plan, const ConvGeo& g, const float* a, c
     k.ws = ws;
     k.a16 = a16;
     k.b16 = b16;
+    // the bf16 copy: not with a bias-gradient column or column statistics (a
+    // batch norm, not a contraction, reads such an output), 16-byte aligned
+    if (ep.out16) {
+        if (plan.bias_col || k.stats || (((uintptr_t)ep.out16) & 15) != 0)
+            return hipErrorInvalidValue;
+        k.out16 = reinterpret_cast<unsigned short*>(ep.out16);
+    }
     const TileCfg& c = kCfgs[plan.cfg];
     k.tiles_m = (int)((plan.M + c.bm - 1) / c.bm);
     k.tiles_n = (int)((plan.Ncols + c.bn - 1) / c.bn);

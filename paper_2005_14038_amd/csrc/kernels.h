@@ -61,6 +61,9 @@ struct Epilogue {
     // plan.bm rows, the tile's mean and sum of squared deviations from it:
     // stats[t * Ncols + col] and stats[(tiles_m + t) * Ncols + col]
     float* stats = nullptr;
+    // optional (not with stats or a bias-gradient column; 16-byte aligned):
+    // each final output element also written rounded to bf16 (nearest even)
+    uint16_t* out16 = nullptr;
 };
 
 // a16 / b16 (bf16 plans with plan.h16, optional): the same operands already
@@ -124,10 +127,11 @@ bool maxpool_tiled(int H, int W, int R, int S, int st, int pad, int P, int Q);
 // zeroed where mask <= 0 (ReLU backward fused).  arg (optional): the taps the
 // forward pass recorded, used for overlapping windows instead of recomputing
 // each window's maximum from x.
+// dx16 (optional): also write the final dx rounded to bf16 (nearest even)
 hipError_t launch_maxpool_bwd(const float* x, const float* dy, float* dx, int N, int H, int W,
                               int C, int R, int S, int st, int pad, int P, int Q,
                               int accumulate, const float* mask, hipStream_t s,
-                              const uint8_t* arg = nullptr);
+                              const uint8_t* arg = nullptr, uint16_t* dx16 = nullptr);
 hipError_t launch_gap_fwd(const float* x, float* y, int N, int HW, int C, hipStream_t s);
 hipError_t launch_gap_bwd(const float* dy, float* dx, int N, int HW, int C, int accumulate,
                           hipStream_t s);

@@ -9,9 +9,11 @@ benchmark uses.
     vectors) must equal the oracle's for the same schedule bit for bit, and
     every loss / gradient must be finite.
   * Every distinct conv / FC geometry of every workload, at batch 32 and full
-    spatial size, as a one-layer stage: sampled outputs of forward, data
-    gradient and weight gradient against the oracle evaluated element by
-    element.
+    spatial size, as a one-layer stage (in the workload's precision, and the
+    VGG-19 ones in bf16 too): outputs of forward, data gradient and weight
+    gradient sampled once in every 64 x 64 block of each output matrix (so in
+    every tile a kernel computes, whole or cut) against the oracle evaluated
+    element by element.
   * VGG-19 stage 1 and full VGG-19 (no batch-norm, so images are
     independent): the complete forward output of image 0 of the batch
     against the oracle run on that image alone.
@@ -144,21 +146,39 @@ def _geometries(name):
 GEOMS = [g for n in ["vgg19_s1", "vgg19", "resnet152_mid", "resnet152"] for g in _geometries(n)]
 _seen_ids = set()
 GEOMS_UNIQ = []
-for _g in GEOMS:
-    _k = (workloads.WORKLOADS[_g[0]].dtype,) + _g[1]
-    if _k not in _seen_ids:
-        _seen_ids.add(_k)
-        GEOMS_UNIQ.append(_g)
+# every geometry in its workload's precision, and the VGG-19 ones in bf16 too
+# (the precision the bf16 contraction kernels run them in when asked)
+for _dt_of in (lambda n: workloads.WORKLOADS[n].dtype,
+               lambda n: "bf16" if n.startswith("vgg") else None):
+    for _g in GEOMS:
+        _dt = _dt_of(_g[0])
+        _k = (_dt,) + _g[1]
+        if _dt is not None and _k not in _seen_ids:
+            _seen_ids.add(_k)
+            GEOMS_UNIQ.append((_dt,) + _g)
 
 
 def _gid(g):
-    name, (op, src, K, R, st, pad, bias, first) = g
-    return f"{name}-{op}{R}x{R}s{st}-{src[0]}x{src[1]}x{src[2]}-{K}"
+    dt, name, (op, src, K, R, st, pad, bias, first) = g
+    return f"{name}-{dt}-{op}{R}x{R}s{st}-{src[0]}x{src[1]}x{src[2]}-{K}"
+
+
+def tile_samples(rows, cols, rng, block=64):
+    """Flat indices of one element in every block x block block of a rows x
+    cols matrix: every output tile a contraction kernel computes (whole or
+    cut, ragged edge tiles included; every tile is a union of such blocks)
+    has at least one of its outputs checked."""
+    br, bc = -(-rows // block), -(-cols // block)
+    r0 = np.repeat(np.arange(br) * block, bc)
+    c0 = np.tile(np.arange(bc) * block, br)
+    r = r0 + (rng.random(r0.size) * np.minimum(block, rows - r0)).astype(np.int64)
+    c = c0 + (rng.random(c0.size) * np.minimum(block, cols - c0)).astype(np.int64)
+    return np.unique(np.concatenate([r * cols + c, [0, rows * cols - 1]]))
 
 
 @pytest.mark.parametrize("geom", GEOMS_UNIQ, ids=[_gid(g) for g in GEOMS_UNIQ])
 def test_full_size_layer_sampled(dev, geom):  # noqa: F811
-    name, (op, src, K, R, stride, pad, bias, first) = geom
+    dtype, name, (op, src, K, R, stride, pad, bias, first) = geom
     wl = workloads.WORKLOADS[name]
     B = wl.batch
     H, W, C = src
@@ -179,7 +199,7 @@ def test_full_size_layer_sampled(dev, geom):  # noqa: F811
     layers = [dict(kind=hp.HP_CONV, in0=-1, C=C, K=K, R=R, S=R, stride=stride, pad=pad,
                    bias=bias)] if op == "conv" else \
         [dict(kind=hp.HP_FC, in0=-1, C=H * W * C, K=K, bias=bias)]
-    stg = hp.Stage(layers, B, H, W, C, dtype=wl.dtype)
+    stg = hp.Stage(layers, B, H, W, C, dtype=dtype)
     wt = torch.from_numpy(w).to(dev)
     xt = torch.from_numpy(x).to(dev)
     y = torch.empty((B,) + tuple(out), dtype=torch.float32, device=dev)
@@ -191,7 +211,7 @@ def test_full_size_layer_sampled(dev, geom):  # noqa: F811
     yg, gg, dxg = y.cpu().numpy(), grad.cpu().numpy(), dx.cpu().numpy()
     stg.close()
 
-    bf = wl.dtype == "bf16"
+    bf = dtype == "bf16"
     from oracle.bf16 import round_bf16
     rnd = round_bf16 if bf else (lambda a: np.asarray(a, np.float64))
     tol = BF16_TOL if bf else FP32_TOL
@@ -208,20 +228,20 @@ def test_full_size_layer_sampled(dev, geom):  # noqa: F811
     xr, wr, dyr = rnd(xo), rnd(wk), rnd(dyo)
     bvec = w[-K:].astype(np.float64) if bias else None
 
-    def sample(size, k=256):
-        return np.unique(np.concatenate([rng.choice(size, min(k, size), replace=False),
-                                         [0, size - 1]]))
-
-    idx = sample(yg.size)
+    # forward [B*P*Q][K], weight gradient [K][R*S*C], data gradient [B*H*W][C]
+    idx = tile_samples(yg.size // K, K, rng)
     ref = oops.conv_fwd_at(xr, wr, bvec, geo[0], geo[1], idx)
     _cmp(yg.reshape(-1)[idx], ref, tol, "forward")
-    idx = sample(K * wr[0].size)
+    idx = tile_samples(K, wr[0].size, rng)
     ref = oops.conv_wgrad_at(xr, dyr, wr.shape[1], wr.shape[2], geo[0], geo[1], idx)
     _cmp(gg[:K * wr[0].size][idx], ref, tol, "weight gradient")
     if bias:
+        # the whole bias gradient (in fp32 mode the weight-gradient kernel's
+        # appended column)
         ref = dy.reshape(-1, K).astype(np.float64).sum(0)
         _cmp(gg[-K:], ref, tol, "bias gradient")
-    idx = sample(dxg.size)
+    cin = xo.shape[-1]
+    idx = tile_samples(dxg.size // cin, cin, rng)
     ref = oops.conv_dgrad_at(dyr, wr, geo[0], geo[1], xo.shape[1], xo.shape[2], idx)
     _cmp(dxg.reshape(-1)[idx], ref, tol, "data gradient")
 
