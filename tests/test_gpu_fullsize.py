@@ -1,0 +1,107 @@
+"""Whole stage steps at full size against the oracle: one minibatch of the
+VGG-19 stage 1, the full VGG-19 and the ResNet-152 middle stage (with its
+input gradient), fp32, batch 32, run through the C ABI in the configuration
+the benchmark uses.  The oracle's values were computed by
+tests/golden/make_fullsize.py (oracle only, same seeded inputs) at one
+sampled element of every 64 x 64 block of each output matrix -- the stage
+output or the logits and loss, every parameter segment of the weight
+gradient, the input gradient.
+
+  * Forward results (stage output or logits, loss): element by element,
+    max |a - r| / max(|r|, 1e-2 max|r|) <= 1e-3, the maximum over the whole
+    tensor taken from the oracle's full result.
+  * Backward results (weight-gradient segments, input gradient): normwise
+    over the samples against max(1e-3, 2 x the oracle's own movement when its
+    weights are perturbed by a relative 1e-6).  A ReLU whose pre-activation
+    lies within fp32 round-off of zero is decided either way by correct
+    implementations, and each such decision moves whole-stage gradients by a
+    full upstream-gradient term (a few 1e-3 per flipped position at full
+    size), so whole-stage gradients are not unique to 1e-3 element by
+    element; every layer is held to 1e-3 element by element on its own GPU
+    inputs (same masks) by test_gpu_chained_full.py.
+"""
+import glob
+import json
+import os
+
+import numpy as np
+import pytest
+import torch
+
+from paper_2005_14038_amd import hetpipe as hp
+from paper_2005_14038_amd import workloads
+
+from gpu_common import FP32_TOL, dev  # noqa: F401
+
+pytestmark = pytest.mark.gpu
+
+GOLDEN = sorted(glob.glob(os.path.join(os.path.dirname(__file__), "golden", "fullsize_*.json")))
+
+
+def _err(a, t):
+    r = np.asarray(t["val"], np.float64)
+    a = np.asarray(a, np.float64)
+    assert np.all(np.isfinite(a))
+    den = np.maximum(np.abs(r), 1e-2 * t["absmax"])
+    return float(np.max(np.abs(a - r) / den))
+
+
+@pytest.mark.parametrize("path", GOLDEN, ids=[os.path.basename(p)[9:-5] for p in GOLDEN])
+def test_full_size_stage_step(dev, path):  # noqa: F811
+    gold = json.load(open(path))
+    wl = workloads.WORKLOADS[gold["workload"]]
+    assert wl.batch == gold["batch"] and wl.seed == gold["seed"] and wl.need_dx == gold["need_dx"]
+    layers = wl.builder().layers
+    st = hp.Stage(layers, wl.batch, wl.H, wl.W, wl.C, dtype="fp32")
+    out_shape = st.output_shape(-1)
+    w0 = workloads.initial_weights(wl, layers)
+    x, lab, dy = workloads.inputs(wl, out_shape, gold["vw"], gold["minibatch"])
+    wt = torch.from_numpy(w0).to(dev)
+    xt = torch.from_numpy(x).to(dev)
+    grad = torch.full((st.P,), float("nan"), dtype=torch.float32, device=dev)
+    dx = torch.full(x.shape, float("nan"), dtype=torch.float32, device=dev) if wl.need_dx else None
+    if wl.has_loss:
+        y = torch.empty((wl.batch, wl.classes), dtype=torch.float32, device=dev)
+        loss = torch.empty(1, dtype=torch.float32, device=dev)
+        st.forward(wt, xt, y, torch.from_numpy(lab).to(dev), loss)
+        st.backward(wt, None, dx, grad)
+    else:
+        y = torch.empty((wl.batch,) + tuple(out_shape), dtype=torch.float32, device=dev)
+        st.forward(wt, xt, y)
+        st.backward(wt, torch.from_numpy(dy).to(dev), dx, grad)
+    torch.cuda.synchronize()
+    got = {"y": y.cpu().numpy().reshape(-1), "grad": grad.cpu().numpy()}
+    if wl.has_loss:
+        got["logits"] = got["y"]
+        lg = float(loss.item())
+        assert abs(lg - gold["loss"]) <= FP32_TOL * abs(gold["loss"]), (lg, gold["loss"])
+    if dx is not None:
+        got["dx"] = dx.cpu().numpy().reshape(-1)
+    st.close()
+    bad = []
+    n = 0
+    backward = [k for k in gold["tensors"] if k.startswith("grad:") or k == "dx"]
+    if backward and not all("sens" in gold["tensors"][k] for k in backward):
+        pytest.skip("the golden file holds no oracle sensitivities (make_fullsize.py --sens)")
+    for key, t in gold["tensors"].items():
+        idx = np.asarray(t["idx"], np.int64)
+        if key.startswith("grad:"):
+            a = got["grad"][t["offset"] + idx]
+        else:
+            a = got[key][idx]
+        e = _err(a, t)
+        r = np.asarray(t["val"], np.float64)
+        nw = float(np.linalg.norm(np.asarray(a, np.float64) - r) / max(np.linalg.norm(r), 1e-300))
+        n += idx.size
+        if key in backward:
+            bound = max(FP32_TOL, 2 * t["sens"])
+            print(f"{gold['workload']} {key}: normwise {nw:.3e} (bound {bound:.3e}), "
+                  f"element-wise {e:.3e}")
+            if nw > bound:
+                bad.append(f"{key}: normwise {nw:.3e} > {bound:.3e}")
+        else:
+            print(f"{gold['workload']} {key}: element-wise {e:.3e}")
+            if e > FP32_TOL:
+                bad.append(f"{key}: element-wise {e:.3e}")
+    assert not bad, f"{gold['workload']}: " + ", ".join(bad[:20])
+    assert n > 1000
