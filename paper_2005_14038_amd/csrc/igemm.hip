@@ -498,6 +498,22 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_kernel(KA
     const long m0 = wk.m0, n0 = wk.n0, kbeg = wk.kbeg, kend = wk.kend;
     const int ktiles = (int)((kend - kbeg + BK - 1) / BK);
 
+    // Reduction order of the k tiles.  When the channel count of a tap is a
+    // multiple of BK (every tile lies within one tap) the tiles are taken
+    // channel chunk by channel chunk, all taps of a chunk in a row: the R*S
+    // tap-shifted reads of the same BK channels follow each other and hit in
+    // the caches instead of coming back from DRAM once per tap.  Tile T is
+    // then (chunk T / RS, tap T % RS); a cut chunk covers a range of T.
+    // Otherwise tiles follow the linear reduction index.
+    const int CCH = (OP == OP_FWD) ? g.C : g.K;
+    const int RSN = g.R * g.S;
+    const bool tap_inner = (OP != OP_WGRAD) && (CCH % BK == 0) && RSN > 1;
+    const int tbeg = (int)(kbeg / BK), tend = (int)((kend + BK - 1) / BK);
+    auto tile_k0 = [&](int T) -> int {
+        if (tap_inner) return (T % RSN) * CCH + (T / RSN) * BK;
+        return T * BK;
+    };
+
     // ---- per-thread staging coordinates ----
     // A: OP_FWD / OP_DGRAD gather rows m with the reduction index contiguous
     // ("k-major"); OP_WGRAD reads dy rows (reduction index = row) with m = k
@@ -612,8 +628,11 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_kernel(KA
     // own small offset instead of dividing per element.
     auto gload = [&](int kt, auto S) {
         constexpr int s = decltype(S)::value;
-        const int k0 = (int)(kbeg + (long)kt * BK);
-        const int kend_i = (int)kend;
+        const int T = tbeg + kt;
+        const bool tin = T < tend;
+        const int k0 = tap_inner ? (tin ? tile_k0(T) : 0) : (int)(kbeg + (long)kt * BK);
+        // reduction bound of a tile's rows: whole tiles in tap order
+        const int kend_i = tap_inner ? (tin ? k0 + BK : 0) : (int)kend;
         if constexpr (OP == OP_FWD || OP == OP_DGRAD) {
             const int CC = (OP == OP_FWD) ? g.C : g.K;       // contiguous axis of a tap
             const int rs0 = k0 / CC;
@@ -1607,12 +1626,16 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_h16k_kern
     }
 
     uintx4 ra[2][GA], rb[2][GB];
-    // tap (tr, ts), channel base tc and reduction index of the next tile to load
-    int kload = (int)wk.kbeg;
-    int tc = kload % CC;
-    int tr, ts;
+    // tap (tr, ts) and channel base tc of the next tile to load.  The tiles
+    // go channel chunk by channel chunk, all R*S taps of a chunk in a row
+    // (tile T = chunk T / RS, tap T % RS): the tap-shifted reads of the same
+    // BKX channels follow each other and hit in the caches.
+    const int RSN = g.R * g.S;
+    int tc, tr, ts;
     {
-        const int rs = kload / CC;
+        const int T0 = (int)(wk.kbeg / BKX);
+        tc = (T0 / RSN) * BKX;
+        const int rs = T0 % RSN;
         tr = rs / g.S;
         ts = rs - tr * g.S;
     }
@@ -1638,13 +1661,12 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_h16k_kern
                 ra[s][i] = buf_load16(rsA, ok ? (unsigned)(a_off[i] + sk) * 2u : BUF_OOB, 0u);
             }
         }
+        const unsigned kload = (unsigned)((tr * g.S + ts) * CC + tc);   // linear reduction index
 #pragma unroll
-        for (int i = 0; i < GB; ++i) rb[s][i] = buf_load16(rsB, b_off[i], (unsigned)kload * 2u);
-        kload += BKX;
-        tc += BKX;
-        if (tc == CC) {
-            tc = 0;
-            if (++ts == g.S) { ts = 0; ++tr; }
+        for (int i = 0; i < GB; ++i) rb[s][i] = buf_load16(rsB, b_off[i], kload * 2u);
+        if (++ts == g.S) {
+            ts = 0;
+            if (++tr == g.R) { tr = 0; tc += BKX; }
         }
     };
 
