@@ -458,6 +458,13 @@ int build_stage(hp_stage* st, const hp_layer* layers, int n_layers) {
             int cons = -1;
             for (int c = i + 1; c < n_layers && cons < 0; ++c)
                 if (st->nodes[c].L.in0 == i) cons = c;
+            // a conv read only by a batch norm hands it its column statistics:
+            // keep its forward on a kernel whose epilogue forms them
+            if (cons >= 0 && st->nodes[cons].L.kind == HP_BN && nd.fwd.h16d) {
+                nd.fwd = plan_gemm(OP_FWD, nd.padC ? nd.geo_p : nd.geo, st->dtype, num_cus(),
+                                   0, 0);
+                st->ws_floats = std::max(st->ws_floats, nd.fwd.ws_floats);
+            }
             if (cons >= 0 && st->nodes[cons].L.kind == HP_BN &&
                 plan_stats(nd.fwd, nd.L.bias ? EPI_BIAS : 0)) {
                 nd.stats_rb = nd.fwd.bm;

@@ -61,6 +61,7 @@ constexpr TileCfg kCfgs[] = {
     {64, 256, 16, 64, 64, 32},     // 2: narrow M, N a multiple of 256 or large
     {64, 128, 16, 32, 64, 64},     // 3: narrow M otherwise (4 waves)
     {64, 64, 16, 32, 32, 64},      // 4: small M and N (4 waves of 32x32)
+    {256, 128, 16, 128, 64, 32},   // 5: igemm_h16d_kernel (4 waves)
 };
 
 struct KArgs {
@@ -183,7 +184,7 @@ __device__ __forceinline__ Work decode_work(const KArgs& args) {
 // knows, so interleaving them would serialise one memory latency per element.
 constexpr int EPI_CHUNK = 8;     // outputs per lane whose epilogue reads are batched
 
-template <int BM, int BN, int TM, int TN>
+template <int BM, int BN, int TM, int TN, bool FENCE = false>
 __device__ __forceinline__ void store_tile(const KArgs& args, const Work& w,
                                            const floatx16 (&acc)[TM][TN], int wm, int wn,
                                            int lane) {
@@ -192,6 +193,7 @@ __device__ __forceinline__ void store_tile(const KArgs& args, const Work& w,
         float* pslot = args.ws + ((long)(w.tile - args.tfull) * args.splits + w.z) * (BM * BN);
 #pragma unroll
         for (int j = 0; j < TN; ++j) {
+                if constexpr (FENCE) __builtin_amdgcn_sched_barrier(0);   // one block at a time
             const int lcol = wn + 32 * j + lr;
             if (w.n0 + lcol >= args.Ncols) continue;
 #pragma unroll
@@ -221,6 +223,7 @@ __device__ __forceinline__ void store_tile(const KArgs& args, const Work& w,
         const float bias = (epi & EPI_BIAS) ? args.bias[col] : 0.f;
 #pragma unroll
         for (int i = 0; i < TM; ++i) {
+            if constexpr (FENCE) __builtin_amdgcn_sched_barrier(0);   // one block at a time
             const long row0 = w.m0 + wm + 32 * i + 4 * lk;
             // rows row0 + 8(v/4) + v%4 of this lane; those >= M are outside
             const int left = (int)min(args.M - row0, 32L);
@@ -266,7 +269,7 @@ __device__ __forceinline__ void store_tile(const KArgs& args, const Work& w,
 // columns that crosses the last column is written element by element.
 constexpr int SLOT_FLOATS = 32 * 32;
 
-template <int BM, int BN, int TM, int TN>
+template <int BM, int BN, int TM, int TN, bool FENCE = false>
 __device__ __forceinline__ void store_tile_wide(const KArgs& args, const Work& w,
                                                 const floatx16 (&acc)[TM][TN], int wm, int wn,
                                                 int lane, float* slot) {
@@ -281,6 +284,7 @@ __device__ __forceinline__ void store_tile_wide(const KArgs& args, const Work& w
     for (int j = 0; j < TN; ++j) {
 #pragma unroll
         for (int i = 0; i < TM; ++i) {
+            if constexpr (FENCE) __builtin_amdgcn_sched_barrier(0);   // one block at a time
 #pragma unroll
             for (int v = 0; v < 16; ++v)
                 slot[(8 * (v >> 2) + 4 * lk + (v & 3)) * 32 + lr] = acc[i][j][v];
@@ -435,6 +439,24 @@ __device__ __forceinline__ void tile_stats(const KArgs& args, const Work& w,
 // (WIDE) and its conditions hold (uniform).  The wide path costs registers,
 // which the fp32 kernels on long reductions, where the epilogue is a small
 // part of the time, keep for occupancy.
+// The epilogue without column statistics: the wide path where the output, the
+// bias, the mask and the workspace allow 16-byte access and there is no
+// bias-gradient column, else the narrow one.
+template <int BM, int BN, int TM, int TN, bool FENCE = false>
+__device__ __forceinline__ void write_tile_plain(const KArgs& args, const Work& w,
+                                                 const floatx16 (&acc)[TM][TN], int wm, int wn,
+                                                 int lane, float* slot) {
+    auto a16 = [](const void* p) { return (((uintptr_t)p) & 15) == 0; };
+    const int epi = args.epi;
+    const bool wide = !(epi & EPI_BIASCOL) && (args.Ncols & 3) == 0 && a16(args.out) &&
+                      (!(epi & EPI_BIAS) || a16(args.bias)) &&
+                      (!(epi & EPI_MASK) || a16(args.mask)) && a16(args.ws);
+    if (wide)
+        store_tile_wide<BM, BN, TM, TN, FENCE>(args, w, acc, wm, wn, lane, slot);
+    else
+        store_tile<BM, BN, TM, TN, FENCE>(args, w, acc, wm, wn, lane);
+}
+
 template <int BM, int BN, int TM, int TN, bool WIDE = true>
 __device__ __forceinline__ void write_tile(const KArgs& args, const Work& w,
                                            const floatx16 (&acc)[TM][TN], int wm, int wn,
@@ -445,15 +467,8 @@ __device__ __forceinline__ void write_tile(const KArgs& args, const Work& w,
         // the wide kernels, whose register budget already allows it.
         if (args.stats && !w.partial)
             tile_stats<BM, BN, TM, TN>(args, w, acc, wm, wn, lane, lds_all);
-        auto a16 = [](const void* p) { return (((uintptr_t)p) & 15) == 0; };
-        const int epi = args.epi;
-        const bool wide = !(epi & EPI_BIASCOL) && (args.Ncols & 3) == 0 && a16(args.out) &&
-                          (!(epi & EPI_BIAS) || a16(args.bias)) &&
-                          (!(epi & EPI_MASK) || a16(args.mask)) && a16(args.ws);
-        if (wide) {
-            store_tile_wide<BM, BN, TM, TN>(args, w, acc, wm, wn, lane, slot);
-            return;
-        }
+        write_tile_plain<BM, BN, TM, TN>(args, w, acc, wm, wn, lane, slot);
+        return;
     }
     store_tile<BM, BN, TM, TN>(args, w, acc, wm, wn, lane);
 }
@@ -1740,6 +1755,271 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_h16k_kern
 }
 
 
+// ---- bf16 k-major contraction with operands loaded straight into LDS ---------
+// The forward and stride-1 data-gradient contractions of igemm_h16k_kernel on
+// a 256 x 128 workgroup tile of four waves, one per SIMD, each owning a
+// 128 x 64 block as 4 x 2 MFMA 32x32x16 tiles: per 16-deep k step a wave reads
+// 6 operand fragments from LDS for 8 MFMAs, where the 32 x 64 waves of
+// igemm_h16k_kernel read 3 for 2.  Operands go from memory into LDS directly
+// (buffer_load_dwordx4 ... lds: lane l of a wave writes 16 bytes at the wave's
+// LDS base + 16 l), range-checked like the other buffer loads (padding taps
+// and rows past the matrix read zeros), so no registers stage them.
+//
+// A k tile is 32 reduction indices (64 bytes per row, four 16-byte chunks),
+// taken channel chunk by channel chunk with all taps of a chunk in a row, as in
+// igemm_h16k_kernel; the tap and chunk of the next tile to load are stepped,
+// not divided out.  One load instruction fills 16 rows; the lane that lands in
+// chunk position p of row r loads chunk p ^ ((r / 4) mod 4) of that row, so
+// the operand reads of consecutive rows at one chunk fall in distinct bank
+// groups.  Four LDS stages, each its own array (so the compiler's wait
+// counters tell them apart), A rows then B rows.
+//
+// With one wave per SIMD a wave issues at most one instruction per four
+// clocks, eight per MFMA 32x32x16, and nothing else hides its latencies, so
+// the k loop is lean and software-pipelined by hand.  Which taps of each A
+// row lie inside the image is a bit mask computed once, so a load costs three
+// vector operations; the steady-state steps carry no conditions.  Each tile is
+// two 16-deep halves; the operands of one half are read from LDS while the
+// products of the other run (the reads spread between the MFMAs).  In the
+// middle of tile kt, between its halves, the wave waits for its own loads of
+// tile kt+1, a barrier makes every wave's loads of kt+1 visible and tells that
+// all reads of tile kt-1 are done, the loads of tile kt+3 go into kt-1's
+// stage, and the first half of kt+1 is read during the second half's products
+// of kt.  A load thus has two tiles' time to land.
+constexpr int H16D_BM = 256, H16D_BN = 128, H16D_BK = 32, H16D_WAVES = 4, H16D_STAGES = 3;
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    // s_waitcnt vmcnt(N), expcnt and lgkmcnt not waited for (gfx9 encoding)
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+
+// 16 bytes per lane from a buffer straight into LDS: lane l writes at lds + 16 l
+// (the LDS byte address goes in M0, which must be uniform).  Written as
+// assembly so that the compiler does not track these loads: the kernel waits
+// for them itself (wait_vmcnt before the barrier that publishes a stage), and
+// the compiler's own tracking, which cannot tell the stages apart across the
+// loop's back edge, would wait for every load in flight before the next
+// stage's LDS reads.  The memory clobber keeps LDS accesses on their side.
+__device__ __forceinline__ void buf_load16_lds(__amdgpu_buffer_rsrc_t rs, void* lds, unsigned voff,
+                                               unsigned soff) {
+    const unsigned m0 = (unsigned)(size_t)(lds_ptr_t)lds;
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
+                 :
+                 : "s"(m0), "v"(voff), "s"(rs), "s"(soff)
+                 : "memory", "m0");
+}
+
+// s_barrier without a memory fence (no wait for outstanding loads); the asm
+// memory clobber keeps the compiler from moving LDS accesses across it
+__device__ __forceinline__ void lds_barrier() { asm volatile("s_barrier" ::: "memory"); }
+
+// scheduling hint for one block of straight-line code: R LDS reads spread
+// evenly among M MFMAs, each read after its share of MFMAs
+template <int M, int R, int Q = 0>
+__device__ __forceinline__ void interleave_mfma_reads() {
+    if constexpr (Q < R) {
+        constexpr int n = (Q + 1) * M / R - Q * M / R;
+        if constexpr (n > 0) __builtin_amdgcn_sched_group_barrier(0x008, n, 0);
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        interleave_mfma_reads<M, R, Q + 1>();
+    }
+}
+
+template <int OP>
+__global__ void __launch_bounds__(64 * H16D_WAVES, 2) igemm_h16d_kernel(KArgs args) {
+    static_assert(OP == OP_FWD || OP == OP_DGRAD, "k-major operands");
+    constexpr int BM = H16D_BM, BN = H16D_BN, BK = H16D_BK, ROW = 2 * BK, NW = H16D_WAVES;
+    constexpr int WM = BM / 2, WN = BN / 2, TM = WM / 32, TN = WN / 32;
+    constexpr int LA = BM / 16 / NW, LB = BN / 16 / NW;   // load instructions per wave per tile
+    constexpr int LPT = LA + LB;
+    constexpr int SB = (BM + BN) * ROW;                    // one stage: A rows, then B rows
+    constexpr int NS = H16D_STAGES;
+    __shared__ __attribute__((aligned(1024))) unsigned char smem[NS * SB];
+
+    const ConvGeo& g = args.g;
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int wm = (wave >> 1) * WM;
+    const int wn = (wave & 1) * WN;
+    const Work wk = decode_work<BM, BN>(args);
+    const int ktiles = (int)((wk.kend - wk.kbeg) / BK);   // whole tiles by construction
+    const int T0 = (int)(wk.kbeg / BK);
+    const int IH = (OP == OP_FWD) ? g.H : g.P;
+    const int IW = (OP == OP_FWD) ? g.W : g.Q;
+    const int CC = (OP == OP_FWD) ? g.C : g.K;
+    const int RSN = g.R * g.S;                             // at most 32 (the tap masks)
+    const unsigned a_bytes = (unsigned)((long)g.N * IH * IW * CC * 2);
+    const unsigned b_bytes = (unsigned)(args.Ncols * args.Kred * 2);
+    const __amdgpu_buffer_rsrc_t rsA = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<unsigned short*>(args.a16), (short)0, (int)a_bytes, BUF_CFG);
+    const __amdgpu_buffer_rsrc_t rsB = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<unsigned short*>(args.b16), (short)0, (int)b_bytes, BUF_CFG);
+
+    // the chunk this lane loads: position lane % 4 of row (.. + lane / 4),
+    // swizzled by (row / 4) mod 4 = (lane / 16) mod 4
+    const int kc = ((lane & 3) ^ ((lane >> 4) & 3)) * 8;
+    // A rows: byte offset of the row's pixel at tap (0, 0) and chunk kc,
+    // and the taps (bit r*S + s) whose pixel lies outside the image (all of
+    // them for rows past M)
+    int a_off[LA];
+    unsigned a_out[LA];
+#pragma unroll
+    for (int j = 0; j < LA; ++j) {
+        const long m = wk.m0 + (wave * LA + j) * 16 + (lane >> 2);
+        const bool row_ok = m < args.M;
+        const long mm = row_ok ? m : 0;
+        int n, h0, w0;
+        if constexpr (OP == OP_FWD) {
+            const int q = (int)(mm % g.Q); const long tt = mm / g.Q;
+            const int p = (int)(tt % g.P); n = (int)(tt / g.P);
+            h0 = p * g.st - g.pad;
+            w0 = q * g.st - g.pad;
+        } else {
+            const int w = (int)(mm % g.W); const long tt = mm / g.W;
+            const int h = (int)(tt % g.H); n = (int)(tt / g.H);
+            h0 = h + g.pad;
+            w0 = w + g.pad;
+        }
+        unsigned out = 0;
+        for (int r = 0; r < g.R; ++r)
+            for (int s = 0; s < g.S; ++s) {
+                const int h = (OP == OP_FWD) ? h0 + r : h0 - r;
+                const int w = (OP == OP_FWD) ? w0 + s : w0 - s;
+                if (!row_ok || (unsigned)h >= (unsigned)IH || (unsigned)w >= (unsigned)IW)
+                    out |= 1u << (r * g.S + s);
+            }
+        a_out[j] = out;
+        a_off[j] = (((n * IH + h0) * IW + w0) * CC + kc) * 2;
+    }
+    unsigned b_off[LB];
+#pragma unroll
+    for (int j = 0; j < LB; ++j) {
+        const long n = wk.n0 + (wave * LB + j) * 16 + (lane >> 2);
+        b_off[j] = n < args.Ncols ? (unsigned)((n * args.Kred + kc) * 2) : BUF_OOB;
+    }
+
+    // the next tile to load, in reduction order (chunk T / RS, tap T % RS):
+    // tap (ir, is), index itap = ir * S + is, of channel chunk ic
+    const int rs0 = T0 % RSN;
+    int ic = (T0 / RSN) * BK, ir = rs0 / g.S, is = rs0 - ir * g.S, itap = rs0;
+    auto issue = [&](unsigned char* S) __attribute__((always_inline)) {
+        const int dr = (OP == OP_FWD) ? ir : -ir;
+        const int ds = (OP == OP_FWD) ? is : -is;
+        const int sk2 = ((dr * IW + ds) * CC + ic) * 2;
+#pragma unroll
+        for (int j = 0; j < LA; ++j) {
+            // a tap outside the image sets bit 31: past the end of any operand
+            // (only bit 0 of the shifted mask survives the shift by 31)
+            buf_load16_lds(rsA, S + (wave * LA + j) * 1024,
+                           ((a_out[j] >> itap) << 31) | (unsigned)(a_off[j] + sk2), 0u);
+        }
+        const int kload = (itap * CC + ic) * 2;
+#pragma unroll
+        for (int j = 0; j < LB; ++j)
+            buf_load16_lds(rsB, S + BM * ROW + (wave * LB + j) * 1024, b_off[j], (unsigned)kload);
+        ++itap;
+        if (++is == g.S) {
+            is = 0;
+            if (++ir == g.R) { ir = 0; itap = 0; ic += BK; }
+        }
+    };
+
+    floatx16 acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+
+    const int lr = lane & 31, lk = lane >> 5;
+    const int rsw = (lr >> 2) & 3;       // swizzle of this lane's operand rows
+    // operand offsets of half 0 and half 1 of a tile within a stage
+    const int oa0 = (wm + lr) * ROW + ((0 + lk) ^ rsw) * 16;
+    const int oa1 = (wm + lr) * ROW + ((2 + lk) ^ rsw) * 16;
+    const int ob0 = BM * ROW + (wn + lr) * ROW + ((0 + lk) ^ rsw) * 16;
+    const int ob1 = BM * ROW + (wn + lr) * ROW + ((2 + lk) ^ rsw) * 16;
+    bf16x8 a0[TM], b0[TN], a1[TM], b1[TN];
+    auto lds16 = [](const unsigned char* p) __attribute__((always_inline)) {
+        return __builtin_bit_cast(bf16x8, *reinterpret_cast<const uintx4*>(p));
+    };
+    auto read_half = [&](const unsigned char* S, int oa, int ob, bf16x8 (&a)[TM], bf16x8 (&b)[TN])
+        __attribute__((always_inline)) {
+#pragma unroll
+        for (int i = 0; i < TM; ++i) a[i] = lds16(S + oa + 32 * i * ROW);
+#pragma unroll
+        for (int j = 0; j < TN; ++j) b[j] = lds16(S + ob + 32 * j * ROW);
+    };
+    auto mma_half = [&](const bf16x8 (&a)[TM], const bf16x8 (&b)[TN]) __attribute__((always_inline)) {
+#pragma unroll
+        for (int i = 0; i < TM; ++i)
+#pragma unroll
+            for (int j = 0; j < TN; ++j)
+                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+    };
+
+    // tile kt sits in stage `cur`, kt+1 in `nxt`; `fill` (kt-1's stage)
+    // receives tile kt+NS-1.  On entry a0/b0 hold the first half of tile kt.
+    // A steady step: tiles kt+1 .. kt+NS-1 all exist.
+    auto step_full = [&](const unsigned char* cur, const unsigned char* nxt, unsigned char* fill)
+        __attribute__((always_inline)) {
+        read_half(cur, oa1, ob1, a1, b1);
+        mma_half(a0, b0);
+        interleave_mfma_reads<TM * TN, TM + TN>();
+        wait_vmcnt<(NS - 3) * LPT>();
+        lds_barrier();
+        issue(fill);
+        read_half(nxt, oa0, ob0, a0, b0);
+        mma_half(a1, b1);
+        interleave_mfma_reads<TM * TN, TM + TN>();
+    };
+    // one of the last steps: tiles past the end are neither waited for nor
+    // loaded (outstanding after the wait: the existing tiles kt+2 .. kt+NS-2)
+    auto step_tail = [&](int kt, const unsigned char* cur, const unsigned char* nxt,
+                         unsigned char* fill) __attribute__((always_inline)) {
+        read_half(cur, oa1, ob1, a1, b1);
+        mma_half(a0, b0);
+        if (kt + 1 < ktiles) {
+            if (NS == 4 && kt + 2 < ktiles) wait_vmcnt<LPT>();
+            else wait_vmcnt<0>();
+            lds_barrier();
+            if (kt + NS - 1 < ktiles) issue(fill);
+            read_half(nxt, oa0, ob0, a0, b0);
+        }
+        mma_half(a1, b1);
+    };
+    static_assert(NS == 3 || NS == 4, "stages");
+#pragma unroll
+    for (int s = 0; s < NS - 1; ++s)
+        if (s < ktiles) issue(smem + s * SB);
+    if (ktiles > 0) {
+        if (NS == 4 && ktiles > 2) wait_vmcnt<2 * LPT>();
+        else if (ktiles > 1) wait_vmcnt<LPT>();
+        else wait_vmcnt<0>();
+        lds_barrier();
+        read_half(smem, oa0, ob0, a0, b0);
+    }
+    int kt = 0;
+    for (; kt + NS - 1 + (NS - 1) < ktiles; kt += NS) {
+#pragma unroll
+        for (int s = 0; s < NS; ++s)
+            step_full(smem + s * SB, smem + ((s + 1) % NS) * SB, smem + ((s + NS - 1) % NS) * SB);
+    }
+    for (; kt < ktiles; ++kt) {
+        const int s = kt % NS;
+        step_tail(kt, smem + s * SB, smem + ((s + 1) % NS) * SB, smem + ((s + NS - 1) % NS) * SB);
+    }
+    __syncthreads();
+    // the epilogue's per-wave 4 KB slots, in the first stage
+    static_assert(SB >= NW * SLOT_FLOATS * (int)sizeof(float), "epilogue slots");
+    float* slot = reinterpret_cast<float*>(smem) + wave * SLOT_FLOATS;
+    write_tile_plain<BM, BN, TM, TN, true>(args, wk, acc, wm, wn, lane, slot);
+}
+
+
 // ---- bf16 weight-gradient kernel on m-major LDS tiles --------------------------
 // out[k][(r,s,c)] = sum over output pixels (n,p,q) of dy[(n,p,q)][k] *
 // x[n, p*st-pad+r, q*st-pad+s, c].  Both operands have the reduction index
@@ -2133,7 +2413,7 @@ struct KernelRef {
 // (general gather), bf16 operands in memory, both k-major (FWD and stride-1
 // DGRAD with a reduction channel count that is a multiple of the k tile), and
 // fp32 (vector width 4 or 1) with the wide epilogue.
-enum { KF_F32_1, KF_F32_4, KF_BF_1, KF_BF_4, KF_H16, KF_H16K, KF_F32_4W, KF_F32_1W };
+enum { KF_F32_1, KF_F32_4, KF_BF_1, KF_BF_4, KF_H16, KF_H16K, KF_F32_4W, KF_F32_1W, KF_H16D };
 
 template <int OP, int CFG, int KF>
 KernelRef kref() {
@@ -2172,7 +2452,16 @@ KernelRef kref_cfg(int cfg) {
 }
 
 template <int OP>
+KernelRef kref_h16d() {
+    if constexpr (OP == OP_WGRAD)
+        return {nullptr, 0};
+    else
+        return {reinterpret_cast<const void*>(&igemm_h16d_kernel<OP>), 64 * H16D_WAVES};
+}
+
+template <int OP>
 KernelRef kref_op(int cfg, int kf) {
+    if (kf == KF_H16D) return kref_h16d<OP>();
     switch (kf) {
         case KF_F32_4: return kref_cfg<OP, KF_F32_4>(cfg);
         case KF_BF_1: return kref_cfg<OP, KF_BF_1>(cfg);
@@ -2206,7 +2495,7 @@ int choose_cfg(int op, long M, long N, long Kred) {
 
 }  // namespace
 
-GemmPlan plan_gemm(int op, const ConvGeo& g, int bf16, int num_cus, int bias_col) {
+GemmPlan plan_gemm(int op, const ConvGeo& g, int bf16, int num_cus, int bias_col, int allow_h16d) {
     GemmPlan p{};
     p.op = op;
     p.bf16 = bf16;
@@ -2235,10 +2524,10 @@ GemmPlan plan_gemm(int op, const ConvGeo& g, int bf16, int num_cus, int bias_col
             p.cfg = c0;
         }
     }
-    const TileCfg& c = kCfgs[p.cfg];
-    const long tiles = ((p.M + c.bm - 1) / c.bm) * ((p.Ncols + c.bn - 1) / c.bn);
-    const int bk = p.h16 ? c.bkh : (bf16 ? BKH : c.bk);
-    const long ktiles = (p.Kred + bk - 1) / bk;
+    const TileCfg* cp = &kCfgs[p.cfg];
+    long tiles = ((p.M + cp->bm - 1) / cp->bm) * ((p.Ncols + cp->bn - 1) / cp->bn);
+    int bk = p.h16 ? cp->bkh : (bf16 ? BKH : cp->bk);
+    long ktiles = (p.Kred + bk - 1) / bk;
     // fp32: the wide epilogue where the epilogue weighs: a short reduction
     // (writes much relative to what it computes), or a moderate reduction over
     // so few tiles that it is cut into eight or more chunks (the partial tiles
@@ -2264,9 +2553,28 @@ GemmPlan plan_gemm(int op, const ConvGeo& g, int bf16, int num_cus, int bias_col
     } else if (p.h16 && op == OP_WGRAD && !p.bias_col) {
         p.h16k = (x_el < lim && dy_el < lim) ? 1 : 0;
     }
+    // the direct-to-LDS kernel: forward and stride-1 data gradient on bf16
+    // operands, at most 32 taps, where it measured faster than the 128 x 128
+    // tiles (by about a fifth): at least 512 output columns (a multiple of
+    // 128), 64 tiles of 256 rows and a reduction of at least 2304.  With
+    // fewer columns or a shorter reduction the 256 x 128 tiles lose: their
+    // epilogue weighs more and hides less behind the products of the other
+    // workgroup (eight waves per CU, against sixteen for the 128 x 128 tiles).
+    p.h16d = 0;
+    if (allow_h16d && p.h16k && op != OP_WGRAD && (op == OP_FWD || g.st == 1) &&
+        p.Ncols % H16D_BN == 0 && p.Ncols >= 512 && p.M >= 64L * H16D_BM && p.Kred >= 2304 &&
+        p.Kred % H16D_BK == 0 && !p.bias_col && g.R * g.S <= 32) {
+        p.h16d = 1;
+        p.cfg = 5;
+        cp = &kCfgs[p.cfg];
+        tiles = ((p.M + cp->bm - 1) / cp->bm) * ((p.Ncols + cp->bn - 1) / cp->bn);
+        bk = H16D_BK;
+        ktiles = (p.Kred + bk - 1) / bk;
+    }
+    const TileCfg& c = *cp;
     // workgroups resident at once
     KernelRef kr = kernel_for(op, p.cfg,
-                              p.h16k ? KF_H16K
+                              p.h16d ? KF_H16D : p.h16k ? KF_H16K
                                      : p.h16 ? KF_H16
                                              : bf16 ? (v4 ? KF_BF_4 : KF_BF_1)
                                                     : (v4 ? (p.wide ? KF_F32_4W : KF_F32_4)
@@ -2280,9 +2588,15 @@ GemmPlan plan_gemm(int op, const ConvGeo& g, int bf16, int num_cus, int bias_col
         // whole rounds of whole tiles; cut the tiles of a partial last round
         // into s chunks when that shortens it: time ~ ceil(rem*s/slots)/s
         const long rounds = tiles / slots, rem = tiles - rounds * slots;
+        // the direct-to-LDS tiles are large: writing and re-reading the
+        // partial tile of each chunk (8 bytes per output at about 5 TB/s over
+        // the whole device) is weighed against the round it shortens (2 Kred
+        // flops per output at about 60% of one CU's MFMA rate), about
+        // 4.7 / Kred rounds per chunk
+        const double pc = p.h16d ? 4.7 / (double)p.Kred : 0.0;
         double best = 1.0;
         for (long s = 2; rem && s <= 16 && s * 4 <= ktiles; ++s) {
-            double t = (double)((rem * s + slots - 1) / slots) / s + 0.01 * s;
+            double t = (double)((rem * s + slots - 1) / slots) / s + 0.01 * s + pc * rem * s;
             if (t < best) { best = t; splits = s; }
         }
         if (splits > 1) tfull = rounds * slots;
@@ -2321,7 +2635,7 @@ void div_magic(int d, unsigned* m, int* sh) {
 }  // namespace
 
 bool plan_stats(const GemmPlan& plan, int flags) {
-    return (flags & ~EPI_BIAS) == 0 && (plan.bf16 || plan.wide);
+    return (flags & ~EPI_BIAS) == 0 && (plan.bf16 || plan.wide) && !plan.h16d;
 }
 
 hipError_t launch_gemm(const GemmPlan& plan, const ConvGeo& g, const float* a, const float* b,
@@ -2372,7 +2686,7 @@ hipError_t launch_gemm(const GemmPlan& plan, const ConvGeo& g, const float* a, c
     const bool h16 = !h16k && plan.h16 && plan.bf16 && !plan.bias_col && a16 && b16 &&
                      ((((uintptr_t)a16) | ((uintptr_t)b16)) & 15) == 0;
     if (h16k) k.b16 = bk16;
-    const int kf = h16k ? KF_H16K
+    const int kf = (h16k && plan.h16d) ? KF_H16D : h16k ? KF_H16K
                         : h16 ? KF_H16
                               : plan.bf16 ? (v4 ? KF_BF_4 : KF_BF_1)
                                           : (v4 ? (plan.wide ? KF_F32_4W : KF_F32_4)

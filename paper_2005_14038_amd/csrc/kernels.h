@@ -26,6 +26,7 @@ struct GemmPlan {
     int bf16;          // round operands to bf16 (RNE) when staging
     int h16;           // bf16: the geometry allows bf16 operands in memory (launch_gemm a16/b16)
     int h16k;          // h16 and both operands k-major (FWD; DGRAD with stride 1 or 2 and b16t)
+    int h16d;          // h16k on the 256 x 128 direct-to-LDS kernel (FWD, stride-1 DGRAD)
     int wide;          // fp32 with the wide (LDS-staged, 16-byte) epilogue: short reductions
     int bias_col;      // OP_WGRAD: Ncols includes the bias-gradient column
     int cfg;           // tile configuration
@@ -41,7 +42,10 @@ struct GemmPlan {
 // bias_col (OP_WGRAD only): append a column of ones to the gathered input so
 // that the last output column is sum_m dy[m][k], the bias gradient.  The plan
 // keeps it only when it costs no extra tile; plan.bias_col says whether it did.
-GemmPlan plan_gemm(int op, const ConvGeo& g, int bf16, int num_cus, int bias_col = 0);
+// allow_h16d = 0 keeps the plan off the 256 x 128 direct-to-LDS kernel (whose
+// epilogue writes no column statistics).
+GemmPlan plan_gemm(int op, const ConvGeo& g, int bf16, int num_cus, int bias_col = 0,
+                   int allow_h16d = 1);
 
 // epilogue flags
 enum {

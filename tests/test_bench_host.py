@@ -39,11 +39,11 @@ def test_code_hash_ignores_comments_and_whitespace(tmp_path):
 def test_stored_traffic_is_keyed_by_the_code_hash():
     b = _bench()
     import json
-    d = json.load(open(os.path.join(ROOT, "profiles", "igemm_vgg19_s1_traffic.json")))
+    d = json.load(open(os.path.join(ROOT, "profiles", "igemm_vgg19_traffic.json")))
     assert "igemm_code_sha256_16" in d and d["bytes_per_step"] > 0
     # reported only while the stored hash matches the current kernel code
     expect = d["bytes_per_step"] if d["igemm_code_sha256_16"] == b.kernel_code_hash() else None
-    assert b.measured_traffic("vgg19_s1") == expect
+    assert b.measured_traffic("vgg19") == expect
 
 
 def test_more_than_one_gpu_is_refused():

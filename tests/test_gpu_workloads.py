@@ -178,16 +178,41 @@ def tile_samples(rows, cols, rng, block=64):
 
 @pytest.mark.parametrize("geom", GEOMS_UNIQ, ids=[_gid(g) for g in GEOMS_UNIQ])
 def test_full_size_layer_sampled(dev, geom):  # noqa: F811
-    dtype, name, (op, src, K, R, stride, pad, bias, first) = geom
-    wl = workloads.WORKLOADS[name]
-    B = wl.batch
+    dtype, name, key = geom
+    seed = 1000 + zlib.crc32(_gid(geom).encode()) % 1000
+    _layer_sampled(dev, dtype, workloads.WORKLOADS[name].batch, key, seed)
+
+
+# bf16 geometries on the 256 x 128 direct-to-LDS tiles (at least 512 output
+# columns, 16384 rows and a reduction of 2304): ragged last row of tiles and
+# image borders; cut tiles (520 tiles: a partial last round); the data
+# gradient on them; 25 taps (the per-row tap masks)
+H16D_GEOMS = [
+    (64, ("conv", (17, 17, 256), 512, 3, 1, 1, True, False)),
+    (130, ("conv", (16, 16, 256), 512, 3, 1, 1, False, False)),
+    (64, ("conv", (17, 17, 512), 256, 3, 1, 1, False, False)),
+    (64, ("conv", (17, 17, 128), 512, 5, 1, 2, False, False)),
+]
+
+
+@pytest.mark.parametrize("bg", H16D_GEOMS, ids=[f"B{b}-" + _gid(("bf16", "t", g)).split("-", 2)[2]
+                                                for b, g in H16D_GEOMS])
+def test_direct_lds_tile_layer_sampled(dev, bg):  # noqa: F811
+    B, key = bg
+    _layer_sampled(dev, "bf16", B, key, 4000 + B + key[2] + key[3])
+
+
+def _layer_sampled(dev, dtype, B, key, seed):
+    """One conv or FC layer on the GPU (forward and backward), checked on one
+    sampled output per 64 x 64 block of each output matrix against the
+    oracle on the same (for bf16: bf16-rounded) operands."""
+    op, src, K, R, stride, pad, bias, first = key
     H, W, C = src
     n = onets.Net("layer", H, W, C)
     if op == "conv":
         n.conv(-1, C, K, R, stride, pad, bias=bias)
     else:
         n.fc(-1, H * W * C, K, bias=bias)
-    seed = 1000 + zlib.crc32(_gid(geom).encode()) % 1000
     segs = [("w" if nm == "w" else nm, int(np.prod(s)), f) for _, nm, s, f in n.param_segments()]
     w = si.initial_weights(segs, seed)
     if bias:
