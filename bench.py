@@ -341,7 +341,7 @@ def main():
     ap.add_argument("--workload", default="vgg19")
     ap.add_argument("--pool", type=int, default=2, help="distinct minibatches resident in HBM")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-images", type=int, default=4,
+    ap.add_argument("--cpu-images", type=int, default=2,
                     help="images of the oracle's bounded CPU sample")
     ap.add_argument("--cpu-single-thread", action="store_true",
                     help="also time the oracle on one thread, on one image (a child process "
