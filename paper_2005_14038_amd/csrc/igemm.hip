@@ -524,10 +524,6 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_kernel(KA
     const int RSN = g.R * g.S;
     const bool tap_inner = (OP != OP_WGRAD) && (CCH % BK == 0) && RSN > 1;
     const int tbeg = (int)(kbeg / BK), tend = (int)((kend + BK - 1) / BK);
-    auto tile_k0 = [&](int T) -> int {
-        if (tap_inner) return (T % RSN) * CCH + (T / RSN) * BK;
-        return T * BK;
-    };
 
     // ---- per-thread staging coordinates ----
     // A: OP_FWD / OP_DGRAD gather rows m with the reduction index contiguous
@@ -637,23 +633,54 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_kernel(KA
         }
     };
 
-    // Staging of one reduction tile [k0, k0 + BK).  The decomposition of k0 into
-    // (filter tap, channel) or (image, output row, output column) is uniform
-    // across the workgroup (scalar unit); each thread then steps from it by its
-    // own small offset instead of dividing per element.
+    // The decomposition of the next tile's first reduction index into (filter
+    // tap, channel) or (image, output row, output column) is uniform across
+    // the workgroup (scalar unit) and stepped from tile to tile (the tiles are
+    // staged in order, kt = 0, 1, 2, ...) instead of divided out per tile:
+    // FWD / DGRAD tap (nr, ns), its index ntap and the channel offset nc
+    // within it; WGRAD the pixel (nn, np, nq).
+    int nr = 0, ns = 0, nc = 0, ntap = 0, nq = 0, np = 0, nn = 0;
+    if constexpr (OP == OP_FWD || OP == OP_DGRAD) {
+        if (tap_inner) {
+            ntap = tbeg % RSN;
+            nc = (tbeg / RSN) * BK;
+        } else {
+            ntap = (int)kbeg / CCH;
+            nc = (int)kbeg - ntap * CCH;
+        }
+        nr = ntap / g.S;
+        ns = ntap - nr * g.S;
+    } else {
+        nq = (int)kbeg % g.Q;
+        const int t0 = (int)kbeg / g.Q;
+        np = t0 % g.P;
+        nn = t0 / g.P;
+    }
+
+    // Staging of one reduction tile [k0, k0 + BK); each thread steps from the
+    // tile's decomposition by its own small offset instead of dividing per
+    // element.
     auto gload = [&](int kt, auto S) {
         constexpr int s = decltype(S)::value;
         const int T = tbeg + kt;
         const bool tin = T < tend;
-        const int k0 = tap_inner ? (tin ? tile_k0(T) : 0) : (int)(kbeg + (long)kt * BK);
+        const int k0 = tap_inner ? (tin ? ntap * CCH + nc : 0) : (int)(kbeg + (long)kt * BK);
         // reduction bound of a tile's rows: whole tiles in tap order
         const int kend_i = tap_inner ? (tin ? k0 + BK : 0) : (int)kend;
         if constexpr (OP == OP_FWD || OP == OP_DGRAD) {
-            const int CC = (OP == OP_FWD) ? g.C : g.K;       // contiguous axis of a tap
-            const int rs0 = k0 / CC;
-            const int c0 = k0 - rs0 * CC;
-            const int r0 = rs0 / g.S;
-            const int s0 = rs0 - r0 * g.S;
+            const int CC = CCH;                               // contiguous axis of a tap
+            const int c0 = nc, r0 = nr, s0 = ns;
+            // the next tile
+            if (tap_inner) {
+                ++ntap;
+                if (++ns == g.S) {
+                    ns = 0;
+                    if (++nr == g.R) { nr = 0; ntap = 0; nc += BK; }
+                }
+            } else {
+                nc += BK;
+                while (nc >= CC) { nc -= CC; if (++ns == g.S) { ns = 0; ++nr; } }
+            }
             // ---- A: k-major gathered rows ----
             {
                 int c = c0 + akv, r = r0, sx = s0;
@@ -725,10 +752,9 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_kernel(KA
                 aok[s][i] = ok;
             }
             // ---- B: B[kk = (n,p,q)][j = (r,s,c)] = x[n, p*st-pad+r, q*st-pad+s, c] ----
-            const int q0 = k0 % g.Q;
-            const int t0 = k0 / g.Q;
-            const int p0 = t0 % g.P;
-            const int n0i = t0 / g.P;
+            const int q0 = nq, p0 = np, n0i = nn;
+            nq += BK;      // the next tile
+            while (nq >= g.Q) { nq -= g.Q; if (++np == g.P) { np = 0; ++nn; } }
 #pragma unroll
             for (int i = 0; i < BV; ++i) {
                 const int kr = (t + i * NT) / BVPR;
