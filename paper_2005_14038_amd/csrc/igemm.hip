@@ -473,6 +473,19 @@ __device__ __forceinline__ void write_tile(const KArgs& args, const Work& w,
     store_tile<BM, BN, TM, TN>(args, w, acc, wm, wn, lane);
 }
 
+// Raw buffer loads: the hardware's range check returns zeros for an offset at
+// or past the end of the buffer, so an operand element that lies in the
+// padding or outside the matrix is read with an offset of BUF_OOB instead of
+// being masked.
+typedef unsigned uintx4 __attribute__((ext_vector_type(4)));
+constexpr unsigned BUF_OOB = 0x80000000u;      // buffer offset past any operand here
+constexpr int BUF_CFG = 0x00020000;            // buffer descriptor word 3 (gfx9 family)
+
+__device__ __forceinline__ uintx4 buf_load16(__amdgpu_buffer_rsrc_t rs, unsigned voff,
+                                             unsigned soff) {
+    return __builtin_amdgcn_raw_buffer_load_b128(rs, (int)voff, (int)soff, 0);
+}
+
 // ---- operand gathers -------------------------------------------------------
 // Each returns VW consecutive elements along the operand's contiguous axis
 // (zero where the element lies outside the problem or in the padding).
@@ -632,6 +645,21 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_kernel(KA
             v[0] = *p;
         }
     };
+    // VW = 4: range-checked buffer loads at 32-bit element offsets (every
+    // operand below 2 GB, checked by the host), an element off the problem
+    // read as zeros through an offset of BUF_OOB, so staging applies no masks
+    const long x_el = (long)g.N * g.H * g.W * g.C, dy_el = (long)g.N * g.P * g.Q * g.K;
+    const long a_el = (OP == OP_DGRAD) ? dy_el : x_el;
+    const long b_el = (OP == OP_WGRAD) ? dy_el : (long)g.K * g.R * g.S * g.C;
+    const __amdgpu_buffer_rsrc_t rsa = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<float*>(args.a), (short)0, (int)(a_el * 4), BUF_CFG);
+    const __amdgpu_buffer_rsrc_t rsb = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<float*>(args.b), (short)0, (int)(b_el * 4), BUF_CFG);
+    auto ldb = [](__amdgpu_buffer_rsrc_t rs, bool ok, int off, float* v) {
+        const uintx4 t = buf_load16(rs, ok ? (unsigned)off * 4u : BUF_OOB, 0u);
+        v[0] = __uint_as_float(t[0]); v[1] = __uint_as_float(t[1]);
+        v[2] = __uint_as_float(t[2]); v[3] = __uint_as_float(t[3]);
+    };
 
     // The decomposition of the next tile's first reduction index into (filter
     // tap, channel) or (image, output row, output column) is uniform across
@@ -692,9 +720,13 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_kernel(KA
                         int h = arow_h[i] + r, w = arow_w[i] + sx;
                         bool ok = arow_ok[i] && kin && (unsigned)h < (unsigned)g.H &&
                                   (unsigned)w < (unsigned)g.W;
-                        const float* ptr =
-                            args.a + (ok ? (arow_base[i] + ((long)h * g.W + w) * g.C + c) : 0);
-                        ld(ptr, areg[s][i]);
+                        if constexpr (VW == 4) {
+                            ldb(rsa, ok, arow_base[i] + (h * g.W + w) * g.C + c, areg[s][i]);
+                        } else {
+                            const float* ptr =
+                                args.a + (ok ? (arow_base[i] + ((long)h * g.W + w) * g.C + c) : 0);
+                            ld(ptr, areg[s][i]);
+                        }
                         aok[s][i] = ok;
                     } else {
                         int tp = arow_h[i] - r, tq = arow_w[i] - sx;
@@ -707,9 +739,13 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_kernel(KA
                         }
                         bool ok = arow_ok[i] && kin && tp >= 0 && tq >= 0 && on_grid &&
                                   p < g.P && q < g.Q;
-                        const float* ptr =
-                            args.a + (ok ? (arow_base[i] + ((long)p * g.Q + q) * g.K + c) : 0);
-                        ld(ptr, areg[s][i]);
+                        if constexpr (VW == 4) {
+                            ldb(rsa, ok, arow_base[i] + (p * g.Q + q) * g.K + c, areg[s][i]);
+                        } else {
+                            const float* ptr =
+                                args.a + (ok ? (arow_base[i] + ((long)p * g.Q + q) * g.K + c) : 0);
+                            ld(ptr, areg[s][i]);
+                        }
                         aok[s][i] = ok;
                     }
                 }
@@ -720,8 +756,12 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_kernel(KA
                 if constexpr (OP == OP_FWD) {
                     const int kk = k0 + bkv;
                     bool ok = brow_ok[i] && kk < kend_i;
-                    const float* ptr = args.b + (ok ? (brow_n[i] * args.Kred + kk) : 0);
-                    ld(ptr, breg[s][i]);
+                    if constexpr (VW == 4) {
+                        ldb(rsb, ok, (int)brow_n[i] * (int)args.Kred + kk, breg[s][i]);
+                    } else {
+                        const float* ptr = args.b + (ok ? (brow_n[i] * args.Kred + kk) : 0);
+                        ld(ptr, breg[s][i]);
+                    }
                     bok[s][i] = ok;
                 } else {   // B[kk = (r,s,k)][c] = w[k][r][s][c]
                     const int kr = (t + i * NT) / BVPR;
@@ -736,8 +776,12 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_kernel(KA
                         while (k >= CC) { k -= CC; if (++sx == g.S) { sx = 0; ++r; } }
                         off = (((long)k * g.R + r) * g.S + sx) * g.C + bcol_c;
                     }
-                    const float* ptr = args.b + (ok ? off : 0);
-                    ld(ptr, breg[s][i]);
+                    if constexpr (VW == 4) {
+                        ldb(rsb, ok, (int)off, breg[s][i]);
+                    } else {
+                        const float* ptr = args.b + (ok ? off : 0);
+                        ld(ptr, breg[s][i]);
+                    }
                     bok[s][i] = ok;
                 }
             }
@@ -747,8 +791,12 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_kernel(KA
             for (int i = 0; i < AV; ++i) {
                 const int kk = k0 + (t + i * NT) / AVPR;
                 bool ok = arow_ok[i] && kk < kend_i;
-                const float* ptr = args.b + (ok ? ((long)kk * g.K + arow_base[i]) : 0);
-                ld(ptr, areg[s][i]);
+                if constexpr (VW == 4) {
+                    ldb(rsb, ok, kk * g.K + arow_base[i], areg[s][i]);
+                } else {
+                    const float* ptr = args.b + (ok ? ((long)kk * g.K + arow_base[i]) : 0);
+                    ld(ptr, areg[s][i]);
+                }
                 aok[s][i] = ok;
             }
             // ---- B: B[kk = (n,p,q)][j = (r,s,c)] = x[n, p*st-pad+r, q*st-pad+s, c] ----
@@ -764,9 +812,13 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_kernel(KA
                 int h = p * g.st - g.pad + bcol_r, w = q * g.st - g.pad + bcol_s;
                 bool ok = bcol_ok && kin && (unsigned)h < (unsigned)g.H &&
                           (unsigned)w < (unsigned)g.W;
-                const float* ptr =
-                    args.a + (ok ? ((((long)n * g.H + h) * g.W + w) * g.C + bcol_c) : 0);
-                ld(ptr, breg[s][i]);
+                if constexpr (VW == 4) {
+                    ldb(rsa, ok, ((n * g.H + h) * g.W + w) * g.C + bcol_c, breg[s][i]);
+                } else {
+                    const float* ptr =
+                        args.a + (ok ? ((((long)n * g.H + h) * g.W + w) * g.C + bcol_c) : 0);
+                    ld(ptr, breg[s][i]);
+                }
                 bok[s][i] = ok;
                 bone[s][i] = bcol_ones && kin;
             }
@@ -783,13 +835,13 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_kernel(KA
                 int row = (t + i * NT) / KVPR;
 #pragma unroll
                 for (int j = 0; j < VW; ++j)
-                    As[(akv + j) * LDA + row] = aok[s][i] ? areg[s][i][j] : 0.f;
+                    As[(akv + j) * LDA + row] = (VW == 4 || aok[s][i]) ? areg[s][i][j] : 0.f;
             } else {
                 int kr = (t + i * NT) / AVPR;
                 int col = ((t + i * NT) % AVPR) * VW;
 #pragma unroll
                 for (int j = 0; j < VW; ++j)
-                    As[kr * LDA + col + j] = aok[s][i] ? areg[s][i][j] : 0.f;
+                    As[kr * LDA + col + j] = (VW == 4 || aok[s][i]) ? areg[s][i][j] : 0.f;
             }
         }
 #pragma unroll
@@ -798,15 +850,19 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_kernel(KA
                 int row = (t + i * NT) / KVPR;
 #pragma unroll
                 for (int j = 0; j < VW; ++j)
-                    Bs[(bkv + j) * LDB + row] = bok[s][i] ? breg[s][i][j] : 0.f;
+                    Bs[(bkv + j) * LDB + row] = (VW == 4 || bok[s][i]) ? breg[s][i][j] : 0.f;
             } else {
                 int kr = (t + i * NT) / BVPR;
                 int col = ((t + i * NT) % BVPR) * VW;
 #pragma unroll
                 for (int j = 0; j < VW; ++j) {
                     // the appended column of ones (bias gradient) in lane 0
-                    const float one = (j == 0 && bone[s][i]) ? 1.f : 0.f;
-                    Bs[kr * LDB + col + j] = bok[s][i] ? breg[s][i][j] : one;
+                    // (VW = 4: an element off the problem was read as zero, and
+                    // the ones column, weight gradient only, is read past the end)
+                    const bool ones = OP == OP_WGRAD && bone[s][i];
+                    const float one = (j == 0 && ones) ? 1.f : 0.f;
+                    Bs[kr * LDB + col + j] = (VW == 4) ? (ones ? one : breg[s][i][j])
+                                                       : (bok[s][i] ? breg[s][i][j] : one);
                 }
             }
         }
@@ -893,7 +949,6 @@ constexpr int BKH = 32;
 constexpr int LDH = BKH + 8;
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef unsigned uintx4 __attribute__((ext_vector_type(4)));
 typedef unsigned uintx2 __attribute__((ext_vector_type(2)));
 
 template <int OP, int BM, int BN, int WM, int WN, int VW>
@@ -1590,13 +1645,6 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_h16_kerne
 // of x pixel (h, w) shifted by the tap when both are even, and nothing
 // otherwise.  Same LDS layout, MFMA loop and two-tile-deep staging as
 // igemm_h16_kernel.
-constexpr unsigned BUF_OOB = 0x80000000u;      // buffer offset past any operand here
-constexpr int BUF_CFG = 0x00020000;            // buffer descriptor word 3 (gfx9 family)
-
-__device__ __forceinline__ uintx4 buf_load16(__amdgpu_buffer_rsrc_t rs, unsigned voff,
-                                             unsigned soff) {
-    return __builtin_amdgcn_raw_buffer_load_b128(rs, (int)voff, (int)soff, 0);
-}
 
 template <int OP, int BM, int BN, int WM, int WN, int BKX>
 __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_h16k_kernel(KArgs args) {
@@ -2521,6 +2569,14 @@ int choose_cfg(int op, long M, long N, long Kred) {
 
 }  // namespace
 
+// The fp32 vector kernels address their operands with 32-bit buffer offsets:
+// every operand below 2 GB (else the kernels of one element per load take it).
+static bool fits_buffer(const ConvGeo& g) {
+    const long lim = (1L << 31) - 16;
+    return (long)g.N * g.H * g.W * g.C * 4 < lim && (long)g.N * g.P * g.Q * g.K * 4 < lim &&
+           (long)g.K * g.R * g.S * g.C * 4 < lim;
+}
+
 GemmPlan plan_gemm(int op, const ConvGeo& g, int bf16, int num_cus, int bias_col, int allow_h16d) {
     GemmPlan p{};
     p.op = op;
@@ -2534,7 +2590,8 @@ GemmPlan plan_gemm(int op, const ConvGeo& g, int bf16, int num_cus, int bias_col
         p.M = g.K; p.Ncols = (long)g.R * g.S * g.C + (p.bias_col ? 1 : 0);
         p.Kred = (long)g.N * g.P * g.Q;
     }
-    const bool v4 = (op == OP_FWD) ? (g.C % 4 == 0) : (g.C % 4 == 0 && g.K % 4 == 0);
+    const bool v4 = ((op == OP_FWD) ? (g.C % 4 == 0) : (g.C % 4 == 0 && g.K % 4 == 0)) &&
+                    fits_buffer(g);
     // bf16 operands in memory: every contiguous axis a multiple of 8 (16 bytes)
     p.h16 = (bf16 && g.C % 8 == 0 && g.K % 8 == 0) ? 1 : 0;
     p.cfg = choose_cfg(op, p.M, p.Ncols, p.Kred);
@@ -2701,7 +2758,7 @@ hipError_t launch_gemm(const GemmPlan& plan, const ConvGeo& g, const float* a, c
     // vector width 4 needs the contiguous axes to be multiples of 4 and the
     // operand bases 16-byte aligned
     bool v4 = (plan.op == OP_FWD) ? (g.C % 4 == 0) : (g.C % 4 == 0 && g.K % 4 == 0);
-    v4 = v4 && ((((uintptr_t)a) | ((uintptr_t)b)) & 15) == 0;
+    v4 = v4 && fits_buffer(g) && ((((uintptr_t)a) | ((uintptr_t)b)) & 15) == 0;
     // DGRAD on k-major operands takes the transposed weights b16t
     const uint16_t* bk16 = plan.op == OP_DGRAD ? b16t : b16;
     if (plan.op == OP_WGRAD) {
