@@ -7,12 +7,17 @@ sampled element of every 64 x 64 block of each output matrix -- the stage
 output or the logits and loss, every parameter segment of the weight
 gradient, the input gradient.
 
-  * Forward results (stage output or logits, loss): element by element,
-    max |a - r| / max(|r|, 1e-2 max|r|) <= 1e-3, the maximum over the whole
-    tensor taken from the oracle's full result.
+  * Forward results (stage output or logits): element by element,
+    max |a - r| / max(|r|, 1e-2 max|r|) against max(1e-3, 2 x the oracle's
+    own element-wise movement when its weights are perturbed by a relative
+    1e-6), the maximum over the whole tensor taken from the oracle's full
+    result; the loss to 1e-3.  A ReLU tie moves an output only by round-off,
+    but a deep stage with batch norms amplifies round-off (the ResNet-152
+    middle stage's output moves 6e-4 normwise under that perturbation),
+    which the oracle's own movement measures.
   * Backward results (weight-gradient segments, input gradient): normwise
-    over the samples against max(1e-3, 2 x the oracle's own movement when its
-    weights are perturbed by a relative 1e-6).  A ReLU whose pre-activation
+    over the samples against max(1e-3, 2 x the oracle's own movement under
+    the same perturbations, the largest over two seeds).  A ReLU whose pre-activation
     lies within fp32 round-off of zero is decided either way by correct
     implementations, and each such decision moves whole-stage gradients by a
     full upstream-gradient term (a few 1e-3 per flipped position at full
@@ -100,8 +105,9 @@ def test_full_size_stage_step(dev, path):  # noqa: F811
             if nw > bound:
                 bad.append(f"{key}: normwise {nw:.3e} > {bound:.3e}")
         else:
-            print(f"{gold['workload']} {key}: element-wise {e:.3e}")
-            if e > FP32_TOL:
-                bad.append(f"{key}: element-wise {e:.3e}")
+            bound = max(FP32_TOL, 2 * t.get("sens_elem", 0.0))
+            print(f"{gold['workload']} {key}: element-wise {e:.3e} (bound {bound:.3e})")
+            if e > bound:
+                bad.append(f"{key}: element-wise {e:.3e} > {bound:.3e}")
     assert not bad, f"{gold['workload']}: " + ", ".join(bad[:20])
     assert n > 1000
