@@ -2684,11 +2684,13 @@ GemmPlan plan_gemm(int op, const ConvGeo& g, int bf16, int num_cus, int bias_col
         }
         if (splits > 1) tfull = rounds * slots;
     } else {
-        // too few tiles: cut every tile so that one round is filled.  Long
-        // fp32 reductions (weight gradients over N*P*Q) are cut for two
+        // too few tiles: cut every tile so that one round is filled, each
+        // chunk keeping at least 8 k tiles (fp32) or 16 (bf16: with fewer,
+        // the partial tiles' writes and their reduction cost ResNet-152 3 %).
+        // Long fp32 reductions (weight gradients over N*P*Q) are cut for two
         // workgroups per slot as long as a chunk keeps 64 K tiles: a chunk
         // that long outweighs writing and re-reading its partial tile.
-        splits = std::min<long>(slots / tiles, ktiles / 8);
+        splits = std::min<long>(slots / tiles, ktiles / (bf16 ? 16 : 8));
         if (!bf16) splits = std::max(splits, std::min<long>(2 * slots / tiles, ktiles / 64));
         if (splits >= 2) tfull = 0;
         else splits = 1;
