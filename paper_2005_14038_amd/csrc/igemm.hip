@@ -2671,12 +2671,12 @@ GemmPlan plan_gemm(int op, const ConvGeo& g, int bf16, int num_cus, int bias_col
         // whole rounds of whole tiles; cut the tiles of a partial last round
         // into s chunks when that shortens it: time ~ ceil(rem*s/slots)/s
         const long rounds = tiles / slots, rem = tiles - rounds * slots;
-        // the direct-to-LDS tiles are large: writing and re-reading the
-        // partial tile of each chunk (8 bytes per output at about 5 TB/s over
-        // the whole device) is weighed against the round it shortens (2 Kred
-        // flops per output at about 60% of one CU's MFMA rate), about
-        // 4.7 / Kred rounds per chunk
-        const double pc = p.h16d ? 4.7 / (double)p.Kred : 0.0;
+        // bf16: writing and re-reading the partial tile of each chunk (8 bytes
+        // per output at about 5 TB/s over the whole device) is weighed
+        // against the round it shortens (2 Kred flops per output at about 60%
+        // of one CU's MFMA rate), about 4.7 / Kred rounds per chunk (measured:
+        // VGG-19 in bf16 +1 %, ResNet-152 +0.3 % against no such term)
+        const double pc = bf16 ? 4.7 / (double)p.Kred : 0.0;
         double best = 1.0;
         for (long s = 2; rem && s <= 16 && s * 4 <= ktiles; ++s) {
             double t = (double)((rem * s + slots - 1) / slots) / s + 0.01 * s + pc * rem * s;
