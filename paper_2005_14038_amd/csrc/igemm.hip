@@ -2683,17 +2683,41 @@ GemmPlan plan_gemm(int op, const ConvGeo& g, int bf16, int num_cus, int bias_col
             if (t < best) { best = t; splits = s; }
         }
         if (splits > 1) tfull = rounds * slots;
-    } else {
+    } else if (bf16) {
         // too few tiles: cut every tile so that one round is filled, each
-        // chunk keeping at least 8 k tiles (fp32) or 16 (bf16: with fewer,
-        // the partial tiles' writes and their reduction cost ResNet-152 3 %).
-        // Long fp32 reductions (weight gradients over N*P*Q) are cut for two
-        // workgroups per slot as long as a chunk keeps 64 K tiles: a chunk
-        // that long outweighs writing and re-reading its partial tile.
-        splits = std::min<long>(slots / tiles, ktiles / (bf16 ? 16 : 8));
-        if (!bf16) splits = std::max(splits, std::min<long>(2 * slots / tiles, ktiles / 64));
+        // chunk keeping at least 16 k tiles (with fewer, the partial tiles'
+        // writes and their reduction cost ResNet-152 3 %)
+        splits = std::min<long>(slots / tiles, ktiles / 16);
         if (splits >= 2) tfull = 0;
         else splits = 1;
+    } else {
+        // fp32, too few tiles: the cut s (chunks of at least 8 k tiles) that
+        // minimises an estimate of the time, in k tiles of a workgroup that
+        // shares its CU.  The most loaded CU runs ceil(tiles s / CUs)
+        // workgroups, occ at a time; a last, partial round takes max(its
+        // share, 0.65) of a full one (a lone workgroup gets more than half of
+        // the CU's matrix cores); each workgroup adds about 2 k tiles of
+        // prologue and epilogue; and each partial tile, written and re-read
+        // (8 bytes per output at about 4 TB/s over the device, against 2 BK
+        // flops per output at about 75 % of a CU's MFMA rate shared by occ
+        // workgroups), costs 0.0288 / occ k tiles.  Measured against cutting
+        // to fill one or two rounds: VGG-19 +1.6 %, the ResNet-152 middle
+        // stage +1.5 % (the 14 x 14 layers of VGG-19 take five chunks
+        // instead of four: 1.96 rounds instead of 1.53).
+        auto cost = [&](long s) {
+            const long wgs = tiles * s, n = (wgs + num_cus - 1) / num_cus;
+            const long full = n / occ, part = n - full * occ;
+            const double r = (double)full + (part ? std::max(0.65, (double)part / occ) : 0.0);
+            return r * ((double)ktiles / s + 2.0) + (s > 1 ? (double)wgs * 0.0288 / occ : 0.0);
+        };
+        const long smax = std::min<long>(ktiles / 8, 4 * slots / tiles + 16);
+        double best = cost(1);
+        splits = 1;
+        for (long s = 2; s <= smax; ++s) {
+            const double t = cost(s);
+            if (t < best) { best = t; splits = s; }
+        }
+        if (splits >= 2) tfull = 0;
     }
     long chunk_tiles = (ktiles + splits - 1) / splits;
     p.splits = (int)((ktiles + chunk_tiles - 1) / chunk_tiles);
