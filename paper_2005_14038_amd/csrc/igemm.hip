@@ -2667,20 +2667,53 @@ GemmPlan plan_gemm(int op, const ConvGeo& g, int bf16, int num_cus, int bias_col
         occ = 1;
     const long slots = (long)num_cus * occ;
     long tfull = tiles, splits = 1;
+    // fp32: the time of `cut` tiles each cut into s chunks, in k tiles of a
+    // workgroup that shares its CU.  The most loaded CU runs ceil(cut s /
+    // CUs) workgroups, occ at a time; a last, partial round takes max(its
+    // share, 0.65) of a full one (a lone workgroup gets more than half of the
+    // CU's matrix cores); each workgroup adds about 2 k tiles of prologue and
+    // epilogue; and each partial tile, written and re-read (8 bytes per
+    // output at about 4 TB/s over the device, against 2 BK flops per output
+    // at about 75 % of a CU's MFMA rate shared by occ workgroups), costs
+    // 0.0288 / occ k tiles.  Measured against the rules it replaced (cut to
+    // fill one or two rounds where every tile is cut; the round count of
+    // the bf16 rule below otherwise): VGG-19 +1.7 %, the ResNet-152 middle
+    // stage +1.9 %, VGG-19 stage 1 +0.6 % (the 14 x 14 layers of VGG-19 take
+    // five chunks instead of four: 1.96 rounds instead of 1.53).
+    auto f32_cost = [&](long cut, long s) {
+        const long wgs = cut * s, n = (wgs + num_cus - 1) / num_cus;
+        const long full = n / occ, part = n - full * occ;
+        const double r = (double)full + (part ? std::max(0.65, (double)part / occ) : 0.0);
+        return r * ((double)ktiles / s + 2.0) + (s > 1 ? (double)wgs * 0.0288 / occ : 0.0);
+    };
+    auto f32_cut = [&](long cut, long smax) {
+        double best = f32_cost(cut, 1);
+        long sb = 1;
+        for (long s = 2; s <= smax; ++s) {
+            const double t = f32_cost(cut, s);
+            if (t < best) { best = t; sb = s; }
+        }
+        return sb;
+    };
     if (tiles >= slots) {
-        // whole rounds of whole tiles; cut the tiles of a partial last round
-        // into s chunks when that shortens it: time ~ ceil(rem*s/slots)/s
+        // whole rounds of whole tiles; the tiles of a partial last round cut
+        // into s chunks when that shortens it (chunks of at least 4 k tiles)
         const long rounds = tiles / slots, rem = tiles - rounds * slots;
-        // bf16: writing and re-reading the partial tile of each chunk (8 bytes
-        // per output at about 5 TB/s over the whole device) is weighed
-        // against the round it shortens (2 Kred flops per output at about 60%
-        // of one CU's MFMA rate), about 4.7 / Kred rounds per chunk (measured:
-        // VGG-19 in bf16 +1 %, ResNet-152 +0.3 % against no such term)
-        const double pc = bf16 ? 4.7 / (double)p.Kred : 0.0;
-        double best = 1.0;
-        for (long s = 2; rem && s <= 16 && s * 4 <= ktiles; ++s) {
-            double t = (double)((rem * s + slots - 1) / slots) / s + 0.01 * s + pc * rem * s;
-            if (t < best) { best = t; splits = s; }
+        if (bf16) {
+            // time ~ ceil(rem*s/slots)/s; writing and re-reading the partial
+            // tile of each chunk (8 bytes per output at about 5 TB/s over the
+            // whole device) is weighed against the round it shortens (2 Kred
+            // flops per output at about 60% of one CU's MFMA rate), about
+            // 4.7 / Kred rounds per chunk (measured: VGG-19 in bf16 +1 %,
+            // ResNet-152 +0.3 % against no such term)
+            const double pc = 4.7 / (double)p.Kred;
+            double best = 1.0;
+            for (long s = 2; rem && s <= 16 && s * 4 <= ktiles; ++s) {
+                double t = (double)((rem * s + slots - 1) / slots) / s + 0.01 * s + pc * rem * s;
+                if (t < best) { best = t; splits = s; }
+            }
+        } else if (rem) {
+            splits = f32_cut(rem, std::min<long>(16, ktiles / 4));
         }
         if (splits > 1) tfull = rounds * slots;
     } else if (bf16) {
@@ -2691,32 +2724,8 @@ GemmPlan plan_gemm(int op, const ConvGeo& g, int bf16, int num_cus, int bias_col
         if (splits >= 2) tfull = 0;
         else splits = 1;
     } else {
-        // fp32, too few tiles: the cut s (chunks of at least 8 k tiles) that
-        // minimises an estimate of the time, in k tiles of a workgroup that
-        // shares its CU.  The most loaded CU runs ceil(tiles s / CUs)
-        // workgroups, occ at a time; a last, partial round takes max(its
-        // share, 0.65) of a full one (a lone workgroup gets more than half of
-        // the CU's matrix cores); each workgroup adds about 2 k tiles of
-        // prologue and epilogue; and each partial tile, written and re-read
-        // (8 bytes per output at about 4 TB/s over the device, against 2 BK
-        // flops per output at about 75 % of a CU's MFMA rate shared by occ
-        // workgroups), costs 0.0288 / occ k tiles.  Measured against cutting
-        // to fill one or two rounds: VGG-19 +1.6 %, the ResNet-152 middle
-        // stage +1.5 % (the 14 x 14 layers of VGG-19 take five chunks
-        // instead of four: 1.96 rounds instead of 1.53).
-        auto cost = [&](long s) {
-            const long wgs = tiles * s, n = (wgs + num_cus - 1) / num_cus;
-            const long full = n / occ, part = n - full * occ;
-            const double r = (double)full + (part ? std::max(0.65, (double)part / occ) : 0.0);
-            return r * ((double)ktiles / s + 2.0) + (s > 1 ? (double)wgs * 0.0288 / occ : 0.0);
-        };
-        const long smax = std::min<long>(ktiles / 8, 4 * slots / tiles + 16);
-        double best = cost(1);
-        splits = 1;
-        for (long s = 2; s <= smax; ++s) {
-            const double t = cost(s);
-            if (t < best) { best = t; splits = s; }
-        }
+        // fp32, too few tiles: every tile cut, chunks of at least 8 k tiles
+        splits = f32_cut(tiles, std::min<long>(ktiles / 8, 4 * slots / tiles + 16));
         if (splits >= 2) tfull = 0;
     }
     long chunk_tiles = (ktiles + splits - 1) / splits;
