@@ -330,7 +330,10 @@ int build_stage(hp_stage* st, const hp_layer* layers, int n_layers) {
                 // a small weight gradient (under 20 GFLOP) leaves most of the GPU
                 // idle: it runs beside the data-gradient chain; a large one fills
                 // the GPU by itself and stays in stream order
-                nd.wgrad_side = 2.0 * nd.wgrad.M * nd.wgrad.Ncols * nd.wgrad.Kred < 2e10;
+                // (not the fully connected kernel, which streams its output at the
+                // rate of the whole device)
+                nd.wgrad_side = 2.0 * nd.wgrad.M * nd.wgrad.Ncols * nd.wgrad.Kred < 2e10 &&
+                                !nd.wgrad.fcw;
                 size_t& wsw = nd.wgrad_side ? st->ws2_floats : st->ws_floats;
                 if (L.bias && !nd.bias_in_wgrad)
                     wsw = std::max(wsw, colsum_ws_floats((long)B * P * Q, L.K));

@@ -609,12 +609,16 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_kernel(KA
             bcol_ones = true;      // the appended column of ones (bias gradient)
             bcol_ok = false;
         }
-        long cc = bcol_ok ? col : 0;
+        const int cc = bcol_ok ? (int)col : 0;      // below R*S*C < 2^31
         if constexpr (OP == OP_WGRAD) {  // col = (r, s, c)
-            bcol_c = (int)(cc % g.C); long tt = cc / g.C;
-            bcol_s = (int)(tt % g.S); bcol_r = (int)(tt / g.S);
+            if (g.R * g.S == 1) {
+                bcol_c = cc;
+            } else {
+                bcol_c = cc % g.C; const int tt = cc / g.C;
+                bcol_s = tt % g.S; bcol_r = tt / g.S;
+            }
         } else {                          // DGRAD: col = c
-            bcol_c = (int)cc;
+            bcol_c = cc;
         }
 #pragma unroll
         for (int i = 0; i < BV; ++i) { brow_n[i] = 0; brow_ok[i] = true; }
@@ -800,14 +804,26 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_kernel(KA
                 aok[s][i] = ok;
             }
             // ---- B: B[kk = (n,p,q)][j = (r,s,c)] = x[n, p*st-pad+r, q*st-pad+s, c] ----
+            // (one output pixel per image, as in a fully connected layer: the
+            // reduction index is the image)
+            const bool px1 = g.P * g.Q == 1;
             const int q0 = nq, p0 = np, n0i = nn;
-            nq += BK;      // the next tile
-            while (nq >= g.Q) { nq -= g.Q; if (++np == g.P) { np = 0; ++nn; } }
+            if (px1) {     // the next tile
+                nn += BK;
+            } else {
+                nq += BK;
+                while (nq >= g.Q) { nq -= g.Q; if (++np == g.P) { np = 0; ++nn; } }
+            }
 #pragma unroll
             for (int i = 0; i < BV; ++i) {
                 const int kr = (t + i * NT) / BVPR;
                 int q = q0 + kr, p = p0, n = n0i;
-                while (q >= g.Q) { q -= g.Q; if (++p == g.P) { p = 0; ++n; } }
+                if (px1) {
+                    q = 0;
+                    n = n0i + kr;
+                } else {
+                    while (q >= g.Q) { q -= g.Q; if (++p == g.P) { p = 0; ++n; } }
+                }
                 const bool kin = k0 + kr < kend_i;
                 int h = p * g.st - g.pad + bcol_r, w = q * g.st - g.pad + bcol_s;
                 bool ok = bcol_ok && kin && (unsigned)h < (unsigned)g.H &&
@@ -929,6 +945,109 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_kernel(KA
     write_tile<BM, BN, TM, TN, WIDE>(args, wk, acc, wm, wn, lane,
                                      reinterpret_cast<float*>(smem) + wave * SLOT_FLOATS,
                                      reinterpret_cast<float*>(smem));
+}
+
+// ---- fp32 weight gradient of a fully connected layer -------------------------
+// dW[m][n] = sum_k dy[k][m] x[k][n], the reduction over a batch of at most 32
+// images: a rank-k update that writes far more than it computes (4 bytes per
+// output against 2k flops), so the order of its writes sets its speed.  A
+// fixed grid of workgroups walks the FCW_BM x FCW_BN tiles in row-major order
+// (workgroup w takes tiles w, w + G, w + 2G, ... of G workgroups), so the
+// tiles being written at any time form one contiguous run of whole output
+// rows.  Each tile stages its dy and x rows (both read from L2) through LDS,
+// the next tile's loads in flight while the current one is multiplied and
+// written.  Four waves of 64 x 64 (2 x 2 MFMA 32x32x2 tiles); rows k past the
+// batch are zeros.  The epilogue is a plain store (no bias, activation, mask
+// or accumulation applies to a weight gradient).  The bias gradient (the sum of dy over the batch, in batch
+// order) is written with the first tile of each row block.
+constexpr int FCW_BM = 64, FCW_BN = 256, FCW_KMAX = 32;
+constexpr int FCW_LDA = FCW_BM + PAD_V, FCW_LDB = FCW_BN + PAD_V;
+
+__global__ void __launch_bounds__(256, 2) fcw_kernel(KArgs args) {
+    static_assert((FCW_BM / 64) * (FCW_BN / 64) == 4, "four waves of 64 x 64");
+    __shared__ float sA[FCW_KMAX * FCW_LDA];
+    __shared__ float sB[FCW_KMAX * FCW_LDB];
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    constexpr int WAVES_N = FCW_BN / 64;
+    const int wm = (wave / WAVES_N) * 64, wn = (wave % WAVES_N) * 64;
+    const int bias = (args.epi & EPI_BIASCOL) ? 1 : 0;
+    const int M = (int)args.M, Nw = (int)args.Ncols - bias, K = (int)args.Kred;
+    const int tiles_n = (Nw + FCW_BN - 1) / FCW_BN;
+    const int tiles = args.tiles_m * tiles_n;
+    const float* dy = args.b;          // [K][M]
+    const float* x = args.a;           // [K][Nw]
+    // staging: thread t holds 4 columns of rows t / (B/4) + (1024/B) i
+    constexpr int AT = FCW_BM / 4, AR = 256 / AT, AV = FCW_KMAX / AR;
+    constexpr int BT = FCW_BN / 4, BR = 256 / BT, BV = FCW_KMAX / BR;
+    float4 na[AV], nb[BV];
+    auto load = [&](int T) {
+        const int m0 = (T / tiles_n) * FCW_BM, n0 = (T % tiles_n) * FCW_BN;
+#pragma unroll
+        for (int i = 0; i < AV; ++i) {
+            const int k = t / AT + AR * i, m = m0 + (t % AT) * 4;
+            na[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (k < K && m < M) na[i] = *reinterpret_cast<const float4*>(dy + (long)k * M + m);
+        }
+#pragma unroll
+        for (int i = 0; i < BV; ++i) {
+            const int k = t / BT + BR * i, n = n0 + (t % BT) * 4;
+            nb[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (k < K && n < Nw) nb[i] = *reinterpret_cast<const float4*>(x + (long)k * Nw + n);
+        }
+    };
+    const int lr = lane & 31, lk = lane >> 5;
+    const int kp = (K + 1) & ~1;
+    if ((int)blockIdx.x < tiles) load(blockIdx.x);
+    for (int T = blockIdx.x; T < tiles; T += gridDim.x) {
+        const int mt = T / tiles_n, nt = T - mt * tiles_n;
+#pragma unroll
+        for (int i = 0; i < AV; ++i)
+            *reinterpret_cast<float4*>(sA + (t / AT + AR * i) * FCW_LDA + (t % AT) * 4) = na[i];
+#pragma unroll
+        for (int i = 0; i < BV; ++i)
+            *reinterpret_cast<float4*>(sB + (t / BT + BR * i) * FCW_LDB + (t % BT) * 4) = nb[i];
+        __syncthreads();
+        if (T + (int)gridDim.x < tiles) load(T + gridDim.x);
+        if (bias && nt == 0 && t < FCW_BM && mt * FCW_BM + t < M) {
+            float s = 0.f;
+            for (int k = 0; k < K; ++k) s += sA[k * FCW_LDA + t];
+            args.bias_out[mt * FCW_BM + t] = s;
+        }
+        floatx16 acc[2][2];
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+            for (int j = 0; j < 2; ++j)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+        for (int kk = 0; kk < kp; kk += 2) {
+            const float* ar = sA + (kk + lk) * FCW_LDA + wm + lr;
+            const float* br = sB + (kk + lk) * FCW_LDB + wn + lr;
+            const float av[2] = {ar[0], ar[32]}, bv[2] = {br[0], br[32]};
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+#pragma unroll
+                for (int j = 0; j < 2; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[i], bv[j], acc[i][j], 0, 0,
+                                                                    0);
+        }
+        __syncthreads();               // sA, sB free for the next tile
+        // the tile straight from the accumulators: a store writes 32
+        // consecutive columns (128 bytes) of two rows
+        const int r0 = mt * FCW_BM + wm + 4 * lk;
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            const int col = nt * FCW_BN + wn + 32 * j + lr;
+            if (col >= Nw) continue;
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) {
+                    const int row = r0 + 32 * i + 8 * (v >> 2) + (v & 3);
+                    if (row < M) args.out[(long)row * Nw + col] = acc[i][j][v];
+                }
+        }
+    }
 }
 
 // ---- bf16 kernel ------------------------------------------------------------
@@ -2730,6 +2849,25 @@ GemmPlan plan_gemm(int op, const ConvGeo& g, int bf16, int num_cus, int bias_col
     }
     long chunk_tiles = (ktiles + splits - 1) / splits;
     p.splits = (int)((ktiles + chunk_tiles - 1) / chunk_tiles);
+    // fp32 weight gradient of a fully connected layer over at most 32 images:
+    // fcw_kernel, whole FCW_BM x FCW_BN tiles, two workgroups per CU
+    p.fcw = 0;
+    if (!bf16 && op == OP_WGRAD && g.H == 1 && g.W == 1 && g.R == 1 && g.S == 1 &&
+        p.Kred <= FCW_KMAX && g.C % 4 == 0 && g.K % 4 == 0 && fits_buffer(g)) {
+        const long tm = (p.M + FCW_BM - 1) / FCW_BM;
+        const long tn = (p.Ncols - p.bias_col + FCW_BN - 1) / FCW_BN;
+        p.fcw = 1;
+        p.cfg = 0;
+        p.splits = 1;
+        p.kchunk = (int)p.Kred;
+        p.tfull = (int)(((p.M + kCfgs[0].bm - 1) / kCfgs[0].bm) *
+                        ((p.Ncols + kCfgs[0].bn - 1) / kCfgs[0].bn));
+        p.nwg = (int)std::min<long>(tm * tn, 2L * num_cus);
+        p.ws_floats = 0;
+        p.bm = FCW_BM;
+        p.bn = FCW_BN;
+        return p;
+    }
     p.kchunk = (int)(chunk_tiles * bk);
     p.tfull = (int)(p.splits > 1 ? tfull : tiles);
     p.nwg = (int)(p.tfull + (tiles - p.tfull) * p.splits);
@@ -2809,6 +2947,12 @@ hipError_t launch_gemm(const GemmPlan& plan, const ConvGeo& g, const float* a, c
                               : plan.bf16 ? (v4 ? KF_BF_4 : KF_BF_1)
                                           : (v4 ? (plan.wide ? KF_F32_4W : KF_F32_4)
                                                 : (plan.wide ? KF_F32_1W : KF_F32_1));
+    if (plan.fcw) {
+        if (!v4) return hipErrorInvalidValue;
+        k.tiles_m = (int)((plan.M + FCW_BM - 1) / FCW_BM);
+        hipLaunchKernelGGL(fcw_kernel, dim3(plan.nwg), dim3(256), 0, s, k);
+        return hipGetLastError();
+    }
     KernelRef kr = kernel_for(plan.op, plan.cfg, kf);
     void* kargs[] = {&k};
     hipError_t e = hipLaunchKernel(kr.fn, dim3(plan.nwg), dim3(kr.nt), kargs, 0, s);
