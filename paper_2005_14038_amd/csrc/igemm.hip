@@ -1050,6 +1050,97 @@ __global__ void __launch_bounds__(256, 2) fcw_kernel(KArgs args) {
     }
 }
 
+// ---- fp32 forward of a fully connected layer ----------------------------------
+// y[m][n] = sum_k x[m][k] w[n][k] over at most 32 images: the layer streams
+// its weights (4 bytes each) for 2M flops per weight, so how the weight rows
+// are read sets its speed.  A workgroup owns FCF_BN output columns and one
+// chunk of the reduction; its four waves take each 128-wide k step of the
+// chunk in four 32-wide parts, so a step reads its weight rows in 512-byte
+// runs.  No LDS staging: a lane loads 16-byte pieces of one x row and of two
+// weight rows straight into MFMA operand registers.  The 32x32x2 MFMA's two k
+// slots are taken as the two lane halves' 16-element runs and its sixteen
+// issues as the elements of the runs, for both operands alike, which leaves
+// the sum unchanged.  The waves' sums are added in LDS in wave order and
+// written as the chunk's partial tile (32 x FCF_BN); the cut-tile reduction
+// adds the chunks in order and applies bias and ReLU.
+constexpr int FCF_BN = 64, FCF_KW = 32, FCF_KSTEP = 4 * FCF_KW, FCF_NS = 2;
+
+__global__ void __launch_bounds__(256, 2) fcf_kernel(KArgs args) {
+    __shared__ float red[4][2][16][64];
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    const int lr = lane & 31, lh = lane >> 5;
+    const int nt = blockIdx.x % args.tiles_n, z = blockIdx.x / args.tiles_n;
+    const int M = (int)args.M, N = (int)args.Ncols, K = (int)args.Kred;
+    const int kbeg = z * args.kchunk, kend = min(kbeg + args.kchunk, K);
+    const __amdgpu_buffer_rsrc_t rx = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<float*>(args.a), (short)0, M * K * 4, BUF_CFG);
+    const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<float*>(args.b), (short)0, N * K * 4, BUF_CFG);
+    const int n0 = nt * FCF_BN;
+    const bool mok = lr < M, nok0 = n0 + lr < N, nok1 = n0 + 32 + lr < N;
+    const unsigned xrow = (unsigned)(lr * K), w0 = (unsigned)((n0 + lr) * K);
+    const unsigned w1 = (unsigned)((n0 + 32 + lr) * K);
+    floatx16 acc[2];
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[j][v] = 0.f;
+    // FCF_NS register stages: the loads of the wave's next FCF_NS - 1 parts
+    // are in flight while one part is multiplied
+    uintx4 xa[FCF_NS][4], wa[FCF_NS][2][4];
+    auto load = [&](int s, int k0) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int k = k0 + 16 * lh + 4 * q;
+            const bool kin = k < kend;
+            xa[s][q] = buf_load16(rx, (mok && kin) ? (xrow + k) * 4u : BUF_OOB, 0u);
+            wa[s][0][q] = buf_load16(rw, (nok0 && kin) ? (w0 + k) * 4u : BUF_OOB, 0u);
+            wa[s][1][q] = buf_load16(rw, (nok1 && kin) ? (w1 + k) * 4u : BUF_OOB, 0u);
+        }
+    };
+    auto mma = [&](int s) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+#pragma unroll
+                for (int j = 0; j < 2; ++j)
+                    acc[j] = __builtin_amdgcn_mfma_f32_32x32x2f32(
+                        __uint_as_float(xa[s][q][e]), __uint_as_float(wa[s][j][q][e]), acc[j], 0,
+                        0, 0);
+    };
+    const int kq = kbeg + FCF_KW * wave;     // the wave's first part
+#pragma unroll
+    for (int s = 0; s < FCF_NS - 1; ++s)
+        if (kq + s * FCF_KSTEP < kend) load(s, kq + s * FCF_KSTEP);
+    for (int base = kq; base < kend; base += FCF_NS * FCF_KSTEP) {
+#pragma unroll
+        for (int s = 0; s < FCF_NS; ++s) {
+            const int k = base + s * FCF_KSTEP;
+            if (k < kend) {
+                const int kn = k + (FCF_NS - 1) * FCF_KSTEP;
+                if (kn < kend) load((s + FCF_NS - 1) % FCF_NS, kn);
+                mma(s);
+            }
+        }
+    }
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) red[wave][j][v][lane] = acc[j][v];
+    __syncthreads();
+    if (wave < 2) {
+        const int j = wave;
+        float* dst = args.ws + ((long)nt * args.splits + z) * (32 * FCF_BN);
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+            const float s = ((red[0][j][v][lane] + red[1][j][v][lane]) + red[2][j][v][lane]) +
+                            red[3][j][v][lane];
+            dst[(8 * (v >> 2) + 4 * lh + (v & 3)) * FCF_BN + 32 * j + lr] = s;
+        }
+    }
+}
+
 // ---- bf16 kernel ------------------------------------------------------------
 // The same three contractions on v_mfma_f32_32x32x16_bf16.  Operands are
 // gathered in fp32 exactly as above, rounded to bf16 and staged row-major in
@@ -2851,6 +2942,29 @@ GemmPlan plan_gemm(int op, const ConvGeo& g, int bf16, int num_cus, int bias_col
     p.splits = (int)((ktiles + chunk_tiles - 1) / chunk_tiles);
     // fp32 weight gradient of a fully connected layer over at most 32 images:
     // fcw_kernel, whole FCW_BM x FCW_BN tiles, two workgroups per CU
+    // fp32 forward of a fully connected layer over at most 32 images:
+    // fcf_kernel, FCF_BN-column tiles each cut into chunks of whole 128-wide k
+    // steps, about two workgroups per CU
+    p.fcf = 0;
+    if (!bf16 && op == OP_FWD && g.H == 1 && g.W == 1 && g.R == 1 && g.S == 1 && p.M <= 32 &&
+        g.C % 4 == 0 && fits_buffer(g)) {
+        const long tn = (p.Ncols + FCF_BN - 1) / FCF_BN;
+        const long kst = (p.Kred + FCF_KSTEP - 1) / FCF_KSTEP;
+        long sp = std::max<long>(1, std::min<long>(kst, (2L * num_cus + tn - 1) / tn));
+        const long per = (kst + sp - 1) / sp;
+        sp = (kst + per - 1) / per;
+        p.fcf = 1;
+        p.fcw = 0;
+        p.cfg = 0;
+        p.splits = (int)sp;
+        p.kchunk = (int)(per * FCF_KSTEP);
+        p.tfull = 0;
+        p.nwg = (int)(tn * sp);
+        p.ws_floats = (size_t)(tn * sp) * 32 * FCF_BN;
+        p.bm = 32;
+        p.bn = FCF_BN;
+        return p;
+    }
     p.fcw = 0;
     if (!bf16 && op == OP_WGRAD && g.H == 1 && g.W == 1 && g.R == 1 && g.S == 1 &&
         p.Kred <= FCW_KMAX && g.C % 4 == 0 && g.K % 4 == 0 && fits_buffer(g)) {
@@ -2891,7 +3005,8 @@ void div_magic(int d, unsigned* m, int* sh) {
 }  // namespace
 
 bool plan_stats(const GemmPlan& plan, int flags) {
-    return (flags & ~EPI_BIAS) == 0 && (plan.bf16 || plan.wide) && !plan.h16d;
+    return (flags & ~EPI_BIAS) == 0 && (plan.bf16 || plan.wide) && !plan.h16d && !plan.fcf &&
+           !plan.fcw;
 }
 
 hipError_t launch_gemm(const GemmPlan& plan, const ConvGeo& g, const float* a, const float* b,
@@ -2947,6 +3062,23 @@ hipError_t launch_gemm(const GemmPlan& plan, const ConvGeo& g, const float* a, c
                               : plan.bf16 ? (v4 ? KF_BF_4 : KF_BF_1)
                                           : (v4 ? (plan.wide ? KF_F32_4W : KF_F32_4)
                                                 : (plan.wide ? KF_F32_1W : KF_F32_1));
+    if (plan.fcf) {
+        if (!v4) return hipErrorInvalidValue;
+        k.tiles_m = 1;
+        k.tiles_n = (int)((plan.Ncols + FCF_BN - 1) / FCF_BN);
+        k.tfull = 0;
+        hipLaunchKernelGGL(fcf_kernel, dim3(plan.nwg), dim3(256), 0, s, k);
+        if (plan.splits <= SK_LANES) {
+            const long total = (long)k.tiles_n * 32 * FCF_BN / 4;
+            const int blocks = (int)std::min<long>((total + 255) / 256, 16384);
+            hipLaunchKernelGGL(igemm_cut_reduce_kernel, dim3(blocks), dim3(256), 0, s, k, 32,
+                               FCF_BN);
+        } else {
+            hipLaunchKernelGGL(igemm_splitk_reduce_kernel, dim3(k.tiles_n * (32 * FCF_BN / SK_EL)),
+                               dim3(SK_EL * SK_LANES), 0, s, k, 32, FCF_BN);
+        }
+        return hipGetLastError();
+    }
     if (plan.fcw) {
         if (!v4) return hipErrorInvalidValue;
         k.tiles_m = (int)((plan.M + FCW_BM - 1) / FCW_BM);

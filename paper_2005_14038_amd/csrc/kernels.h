@@ -28,6 +28,7 @@ struct GemmPlan {
     int h16k;          // h16 and both operands k-major (FWD; DGRAD with stride 1 or 2 and b16t)
     int h16d;          // h16k on the 256 x 128 direct-to-LDS kernel (FWD, stride-1 DGRAD)
     int wide;          // fp32 with the wide (LDS-staged, 16-byte) epilogue: short reductions
+    int fcf;           // fp32 forward of a fully connected layer on fcf_kernel
     int fcw;           // fp32 weight gradient of a fully connected layer on fcw_kernel
     int bias_col;      // OP_WGRAD: Ncols includes the bias-gradient column
     int cfg;           // tile configuration

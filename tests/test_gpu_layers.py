@@ -93,7 +93,11 @@ def test_conv_random_geometry(dev, case, dtype):  # noqa: F811
     test_conv(dev, case, dtype)
 
 
-FC = [(4, 1, 1, 37, 50), (32, 2, 3, 16, 96), (5, 3, 3, 64, 260)]
+# the last two: a 32-image fully connected weight gradient of 64 x 256 tiles
+# that the fixed grid walks more than once (1024 tiles, 512 workgroups at most),
+# and 33 images, one past the batch that kernel takes
+FC = [(4, 1, 1, 37, 50), (32, 2, 3, 16, 96), (5, 3, 3, 64, 260), (32, 1, 1, 4096, 4096),
+      (33, 1, 1, 256, 128)]
 
 
 @pytest.mark.parametrize("case", FC)
