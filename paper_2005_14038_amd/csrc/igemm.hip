@@ -504,12 +504,16 @@ __device__ __forceinline__ void load_vec(const float* p, bool ok, float* v) {
     }
 }
 
-// DS1: a data gradient of stride 1 (the gathered dy rows need no division by
-// the stride nor its exact-tap test; VGG-19 +1.1 %, its first stage +1.3 %).
+// FAST: a forward or stride-1 data-gradient contraction whose reduction
+// channel count (C, or K) is a multiple of the k tile, with the tap-inner
+// order and the unit stride fixed at compile time: no k tile crosses a tap,
+// so the per-thread wrap of the channel index, the linear-order paths and the
+// stride's division and exact-tap test drop out of the k loop (the data
+// gradient's stride alone: VGG-19 +1.1 %, its first stage +1.3 %).
 template <int OP, int BM, int BN, int BK, int WM, int WN, int VW, bool WIDE = false,
-          bool DS1 = false>
+          bool FAST = false>
 __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_kernel(KArgs args) {
-    static_assert(!DS1 || OP == OP_DGRAD, "stride-1 variant of the data gradient only");
+    static_assert(!FAST || OP != OP_WGRAD, "forward and data gradient only");
     constexpr int NT = 64 * (BM / WM) * (BN / WN);
     constexpr int TM = WM / 32, TN = WN / 32;  // MFMA tiles per wave
     constexpr bool A_KMAJ = (OP != OP_WGRAD);
@@ -539,7 +543,7 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_kernel(KA
     // Otherwise tiles follow the linear reduction index.
     const int CCH = (OP == OP_FWD) ? g.C : g.K;
     const int RSN = g.R * g.S;
-    const bool tap_inner = (OP != OP_WGRAD) && (CCH % BK == 0) && RSN > 1;
+    const bool tap_inner = FAST || ((OP != OP_WGRAD) && (CCH % BK == 0) && RSN > 1);
     const int tbeg = (int)(kbeg / BK), tend = (int)((kend + BK - 1) / BK);
 
     // ---- per-thread staging coordinates ----
@@ -720,8 +724,9 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_kernel(KA
             // ---- A: k-major gathered rows ----
             {
                 int c = c0 + akv, r = r0, sx = s0;
-                while (c >= CC) { c -= CC; if (++sx == g.S) { sx = 0; ++r; } }
-                const bool kin = k0 + akv < kend_i;
+                if constexpr (!FAST)
+                    while (c >= CC) { c -= CC; if (++sx == g.S) { sx = 0; ++r; } }
+                const bool kin = FAST ? tin : k0 + akv < kend_i;
 #pragma unroll
                 for (int i = 0; i < AV; ++i) {
                     if constexpr (OP == OP_FWD) {
@@ -740,7 +745,7 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_kernel(KA
                         int tp = arow_h[i] - r, tq = arow_w[i] - sx;
                         int p = tp, q = tq;
                         bool ok;
-                        if constexpr (DS1) {
+                        if constexpr (FAST) {
                             ok = arow_ok[i] && kin && (unsigned)p < (unsigned)g.P &&
                                  (unsigned)q < (unsigned)g.Q;
                         } else {
@@ -2707,10 +2712,10 @@ struct KernelRef {
 // (general gather), bf16 operands in memory, both k-major (FWD and stride-1
 // DGRAD with a reduction channel count that is a multiple of the k tile), and
 // fp32 (vector width 4 or 1) with the wide epilogue.
-// KF_F32_4D1 / KF_F32_4WD1: the fp32 vector kernels with the stride-1 data
-// gradient (the same kernels as KF_F32_4 / KF_F32_4W for the other contractions).
+// KF_F32_4F / KF_F32_4WF: the fp32 vector kernels in their FAST form (forward and
+// stride-1 data gradient with a channel count that is a multiple of the k tile).
 enum { KF_F32_1, KF_F32_4, KF_BF_1, KF_BF_4, KF_H16, KF_H16K, KF_F32_4W, KF_F32_1W, KF_H16D,
-       KF_F32_4D1, KF_F32_4WD1 };
+       KF_F32_4F, KF_F32_4WF };
 
 template <int OP, int CFG, int KF>
 KernelRef kref() {
@@ -2728,13 +2733,13 @@ KernelRef kref() {
     else if constexpr (KF == KF_BF_1 || KF == KF_BF_4)
         return {reinterpret_cast<const void*>(
                     &igemm_bf16_kernel<OP, c.bm, c.bn, c.wm, c.wn, KF == KF_BF_4 ? 4 : 1>), nt};
-    else if constexpr (KF == KF_F32_4WD1)
+    else if constexpr (KF == KF_F32_4WF)
         return {reinterpret_cast<const void*>(
-                    &igemm_kernel<OP, c.bm, c.bn, c.bk, c.wm, c.wn, 4, true, OP == OP_DGRAD>),
+                    &igemm_kernel<OP, c.bm, c.bn, c.bk, c.wm, c.wn, 4, true, OP != OP_WGRAD>),
                 nt};
-    else if constexpr (KF == KF_F32_4D1)
+    else if constexpr (KF == KF_F32_4F)
         return {reinterpret_cast<const void*>(
-                    &igemm_kernel<OP, c.bm, c.bn, c.bk, c.wm, c.wn, 4, false, OP == OP_DGRAD>),
+                    &igemm_kernel<OP, c.bm, c.bn, c.bk, c.wm, c.wn, 4, false, OP != OP_WGRAD>),
                 nt};
     else if constexpr (KF == KF_F32_4W || KF == KF_F32_1W)
         return {reinterpret_cast<const void*>(
@@ -2774,8 +2779,8 @@ KernelRef kref_op(int cfg, int kf) {
         case KF_H16: return kref_cfg<OP, KF_H16>(cfg);
         case KF_H16K: return kref_cfg<OP, KF_H16K>(cfg);
         case KF_F32_4W: return kref_cfg<OP, KF_F32_4W>(cfg);
-        case KF_F32_4D1: return kref_cfg<OP, KF_F32_4D1>(cfg);
-        case KF_F32_4WD1: return kref_cfg<OP, KF_F32_4WD1>(cfg);
+        case KF_F32_4F: return kref_cfg<OP, KF_F32_4F>(cfg);
+        case KF_F32_4WF: return kref_cfg<OP, KF_F32_4WF>(cfg);
         case KF_F32_1W: return kref_cfg<OP, KF_F32_1W>(cfg);
         default: return kref_cfg<OP, KF_F32_1>(cfg);
     }
@@ -2825,7 +2830,11 @@ GemmPlan plan_gemm(int op, const ConvGeo& g, int bf16, int num_cus, int bias_col
     }
     const bool v4 = ((op == OP_FWD) ? (g.C % 4 == 0) : (g.C % 4 == 0 && g.K % 4 == 0)) &&
                     fits_buffer(g);
-    const bool ds1 = op == OP_DGRAD && g.st == 1;
+    // the FAST fp32 kernels (the k tile is 16 in every fp32 configuration)
+    static_assert(kCfgs[0].bk == 16 && kCfgs[1].bk == 16 && kCfgs[2].bk == 16 &&
+                      kCfgs[3].bk == 16 && kCfgs[4].bk == 16,
+                  "fp32 k tile");
+    const bool fast32 = (op == OP_FWD && g.C % 16 == 0) || (op == OP_DGRAD && g.st == 1 && g.K % 16 == 0);
     // bf16 operands in memory: every contiguous axis a multiple of 8 (16 bytes)
     p.h16 = (bf16 && g.C % 8 == 0 && g.K % 8 == 0) ? 1 : 0;
     p.cfg = choose_cfg(op, p.M, p.Ncols, p.Kred);
@@ -2853,7 +2862,7 @@ GemmPlan plan_gemm(int op, const ConvGeo& g, int bf16, int num_cus, int bias_col
     // occupancy gives them more resident workgroups and reduction chunks.
     if (!bf16) {
         int occ_n = 0;
-        const KernelRef kn = kernel_for(op, p.cfg, v4 ? (ds1 ? KF_F32_4D1 : KF_F32_4) : KF_F32_1);
+        const KernelRef kn = kernel_for(op, p.cfg, v4 ? (fast32 ? KF_F32_4F : KF_F32_4) : KF_F32_1);
         if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ_n, kn.fn, kn.nt, 0) != hipSuccess ||
             occ_n < 1)
             occ_n = 1;
@@ -2894,8 +2903,8 @@ GemmPlan plan_gemm(int op, const ConvGeo& g, int bf16, int num_cus, int bias_col
                               p.h16d ? KF_H16D : p.h16k ? KF_H16K
                                      : p.h16 ? KF_H16
                                              : bf16 ? (v4 ? KF_BF_4 : KF_BF_1)
-                                                    : (v4 ? (p.wide ? (ds1 ? KF_F32_4WD1 : KF_F32_4W)
-                                                                    : (ds1 ? KF_F32_4D1 : KF_F32_4))
+                                                    : (v4 ? (p.wide ? (fast32 ? KF_F32_4WF : KF_F32_4W)
+                                                                    : (fast32 ? KF_F32_4F : KF_F32_4))
                                                           : (p.wide ? KF_F32_1W : KF_F32_1)));
     int occ = 0;
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, kr.fn, kr.nt, 0) != hipSuccess || occ < 1)
@@ -3072,7 +3081,8 @@ hipError_t launch_gemm(const GemmPlan& plan, const ConvGeo& g, const float* a, c
     // operand bases 16-byte aligned
     bool v4 = (plan.op == OP_FWD) ? (g.C % 4 == 0) : (g.C % 4 == 0 && g.K % 4 == 0);
     v4 = v4 && fits_buffer(g) && ((((uintptr_t)a) | ((uintptr_t)b)) & 15) == 0;
-    const bool ds1 = plan.op == OP_DGRAD && g.st == 1;
+    const bool fast32 = (plan.op == OP_FWD && g.C % 16 == 0) ||
+                     (plan.op == OP_DGRAD && g.st == 1 && g.K % 16 == 0);
     // DGRAD on k-major operands takes the transposed weights b16t
     const uint16_t* bk16 = plan.op == OP_DGRAD ? b16t : b16;
     if (plan.op == OP_WGRAD) {
@@ -3086,8 +3096,8 @@ hipError_t launch_gemm(const GemmPlan& plan, const ConvGeo& g, const float* a, c
     const int kf = (h16k && plan.h16d) ? KF_H16D : h16k ? KF_H16K
                         : h16 ? KF_H16
                               : plan.bf16 ? (v4 ? KF_BF_4 : KF_BF_1)
-                                          : (v4 ? (plan.wide ? (ds1 ? KF_F32_4WD1 : KF_F32_4W)
-                                                            : (ds1 ? KF_F32_4D1 : KF_F32_4))
+                                          : (v4 ? (plan.wide ? (fast32 ? KF_F32_4WF : KF_F32_4W)
+                                                            : (fast32 ? KF_F32_4F : KF_F32_4))
                                                 : (plan.wide ? KF_F32_1W : KF_F32_1));
     if (plan.fcf) {
         if (!v4) return hipErrorInvalidValue;
