@@ -509,11 +509,13 @@ __device__ __forceinline__ void load_vec(const float* p, bool ok, float* v) {
 // order and the unit stride fixed at compile time: no k tile crosses a tap,
 // so the per-thread wrap of the channel index, the linear-order paths and the
 // stride's division and exact-tap test drop out of the k loop (the data
-// gradient's stride alone: VGG-19 +1.1 %, its first stage +1.3 %).
+// gradient's stride alone: VGG-19 +1.1 %, its first stage +1.3 %).  For a
+// weight gradient: an output width Q that is a multiple of the k tile, so that
+// no k tile (16 output pixels) crosses an output row and the pixel's image
+// and row are the tile's.
 template <int OP, int BM, int BN, int BK, int WM, int WN, int VW, bool WIDE = false,
           bool FAST = false>
 __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_kernel(KArgs args) {
-    static_assert(!FAST || OP != OP_WGRAD, "forward and data gradient only");
     constexpr int NT = 64 * (BM / WM) * (BN / WN);
     constexpr int TM = WM / 32, TN = WN / 32;  // MFMA tiles per wave
     constexpr bool A_KMAJ = (OP != OP_WGRAD);
@@ -543,7 +545,7 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_kernel(KA
     // Otherwise tiles follow the linear reduction index.
     const int CCH = (OP == OP_FWD) ? g.C : g.K;
     const int RSN = g.R * g.S;
-    const bool tap_inner = FAST || ((OP != OP_WGRAD) && (CCH % BK == 0) && RSN > 1);
+    const bool tap_inner = (OP != OP_WGRAD) && (FAST || ((CCH % BK == 0) && RSN > 1));
     const int tbeg = (int)(kbeg / BK), tend = (int)((kend + BK - 1) / BK);
 
     // ---- per-thread staging coordinates ----
@@ -821,9 +823,12 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_kernel(KA
             // ---- B: B[kk = (n,p,q)][j = (r,s,c)] = x[n, p*st-pad+r, q*st-pad+s, c] ----
             // (one output pixel per image, as in a fully connected layer: the
             // reduction index is the image)
-            const bool px1 = g.P * g.Q == 1;
+            const bool px1 = !FAST && g.P * g.Q == 1;
             const int q0 = nq, p0 = np, n0i = nn;
-            if (px1) {     // the next tile
+            if constexpr (FAST) {  // the next tile: the next 16 pixels of the row, or the next row
+                nq += BK;
+                if (nq == g.Q) { nq = 0; if (++np == g.P) { np = 0; ++nn; } }
+            } else if (px1) {
                 nn += BK;
             } else {
                 nq += BK;
@@ -833,11 +838,13 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_kernel(KA
             for (int i = 0; i < BV; ++i) {
                 const int kr = (t + i * NT) / BVPR;
                 int q = q0 + kr, p = p0, n = n0i;
-                if (px1) {
-                    q = 0;
-                    n = n0i + kr;
-                } else {
-                    while (q >= g.Q) { q -= g.Q; if (++p == g.P) { p = 0; ++n; } }
+                if constexpr (!FAST) {
+                    if (px1) {
+                        q = 0;
+                        n = n0i + kr;
+                    } else {
+                        while (q >= g.Q) { q -= g.Q; if (++p == g.P) { p = 0; ++n; } }
+                    }
                 }
                 const bool kin = k0 + kr < kend_i;
                 int h = p * g.st - g.pad + bcol_r, w = q * g.st - g.pad + bcol_s;
@@ -2713,7 +2720,8 @@ struct KernelRef {
 // DGRAD with a reduction channel count that is a multiple of the k tile), and
 // fp32 (vector width 4 or 1) with the wide epilogue.
 // KF_F32_4F / KF_F32_4WF: the fp32 vector kernels in their FAST form (forward and
-// stride-1 data gradient with a channel count that is a multiple of the k tile).
+// stride-1 data gradient with a channel count that is a multiple of the k tile;
+// weight gradient with an output width that is one).
 enum { KF_F32_1, KF_F32_4, KF_BF_1, KF_BF_4, KF_H16, KF_H16K, KF_F32_4W, KF_F32_1W, KF_H16D,
        KF_F32_4F, KF_F32_4WF };
 
@@ -2735,11 +2743,11 @@ KernelRef kref() {
                     &igemm_bf16_kernel<OP, c.bm, c.bn, c.wm, c.wn, KF == KF_BF_4 ? 4 : 1>), nt};
     else if constexpr (KF == KF_F32_4WF)
         return {reinterpret_cast<const void*>(
-                    &igemm_kernel<OP, c.bm, c.bn, c.bk, c.wm, c.wn, 4, true, OP != OP_WGRAD>),
+                    &igemm_kernel<OP, c.bm, c.bn, c.bk, c.wm, c.wn, 4, true, true>),
                 nt};
     else if constexpr (KF == KF_F32_4F)
         return {reinterpret_cast<const void*>(
-                    &igemm_kernel<OP, c.bm, c.bn, c.bk, c.wm, c.wn, 4, false, OP != OP_WGRAD>),
+                    &igemm_kernel<OP, c.bm, c.bn, c.bk, c.wm, c.wn, 4, false, true>),
                 nt};
     else if constexpr (KF == KF_F32_4W || KF == KF_F32_1W)
         return {reinterpret_cast<const void*>(
@@ -2834,7 +2842,9 @@ GemmPlan plan_gemm(int op, const ConvGeo& g, int bf16, int num_cus, int bias_col
     static_assert(kCfgs[0].bk == 16 && kCfgs[1].bk == 16 && kCfgs[2].bk == 16 &&
                       kCfgs[3].bk == 16 && kCfgs[4].bk == 16,
                   "fp32 k tile");
-    const bool fast32 = (op == OP_FWD && g.C % 16 == 0) || (op == OP_DGRAD && g.st == 1 && g.K % 16 == 0);
+    const bool fast32 = (op == OP_FWD && g.C % 16 == 0) ||
+                        (op == OP_DGRAD && g.st == 1 && g.K % 16 == 0) ||
+                        (op == OP_WGRAD && g.Q % 16 == 0);
     // bf16 operands in memory: every contiguous axis a multiple of 8 (16 bytes)
     p.h16 = (bf16 && g.C % 8 == 0 && g.K % 8 == 0) ? 1 : 0;
     p.cfg = choose_cfg(op, p.M, p.Ncols, p.Kred);
@@ -3082,7 +3092,8 @@ hipError_t launch_gemm(const GemmPlan& plan, const ConvGeo& g, const float* a, c
     bool v4 = (plan.op == OP_FWD) ? (g.C % 4 == 0) : (g.C % 4 == 0 && g.K % 4 == 0);
     v4 = v4 && fits_buffer(g) && ((((uintptr_t)a) | ((uintptr_t)b)) & 15) == 0;
     const bool fast32 = (plan.op == OP_FWD && g.C % 16 == 0) ||
-                     (plan.op == OP_DGRAD && g.st == 1 && g.K % 16 == 0);
+                        (plan.op == OP_DGRAD && g.st == 1 && g.K % 16 == 0) ||
+                        (plan.op == OP_WGRAD && g.Q % 16 == 0);
     // DGRAD on k-major operands takes the transposed weights b16t
     const uint16_t* bk16 = plan.op == OP_DGRAD ? b16t : b16;
     if (plan.op == OP_WGRAD) {
