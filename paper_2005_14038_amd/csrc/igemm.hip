@@ -637,12 +637,14 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_kernel(KA
     // data gradient: when K is a multiple of the k tile no tile crosses a
     // tap, and row kr of a tile in tap (r, s) at channel c0 reads weight
     // (c0 + kr)*R*S*C + (r*S + s)*C + c: the thread's part is fixed
-    const long rsc = (long)g.R * g.S * g.C;
-    const bool dg_one_tap = (OP == OP_DGRAD) && (g.K % BK == 0);
-    long b_thr[BV];
+    // (32-bit with the buffer loads, whose operands are below 2 GB)
+    using BOff = std::conditional_t<VW == 4, int, long>;
+    const BOff rsc = (BOff)g.R * g.S * g.C;
+    const bool dg_one_tap = (OP == OP_DGRAD) && (FAST || g.K % BK == 0);
+    BOff b_thr[BV];
 #pragma unroll
     for (int i = 0; i < BV; ++i)
-        b_thr[i] = (long)((t + i * NT) / BVPR) * rsc + bcol_c;
+        b_thr[i] = (BOff)((t + i * NT) / BVPR) * rsc + bcol_c;
 
     // two register sets of staged operands (tile kt+2 loads while kt+1 waits
     // to be written to LDS) and their masks; loads are unconditional (masked
@@ -791,7 +793,7 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_kernel(KA
                     if (dg_one_tap) {
                         // the tile lies within tap (r0, s0): a uniform base plus
                         // this thread's constant offset
-                        off = (long)c0 * rsc + ((long)r0 * g.S + s0) * g.C + b_thr[i];
+                        off = (BOff)c0 * rsc + ((BOff)r0 * g.S + s0) * g.C + b_thr[i];
                     } else {
                         int k = c0 + kr, r = r0, sx = s0;
                         while (k >= CC) { k -= CC; if (++sx == g.S) { sx = 0; ++r; } }
