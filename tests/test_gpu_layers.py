@@ -33,6 +33,13 @@ CONV = [
     (2, 15, 13, 32, 64, 3, 2, 1, False),   # stride-2 data gradient, 128x64 tile, odd sizes
     (2, 14, 14, 64, 128, 1, 2, 0, False),  # stride-2 1x1 projection shape
     (2, 16, 12, 128, 128, 3, 2, 1, False), # stride-2 data gradient, 128x128 tile
+    # fp32 FAST instantiations (forward with C, stride-1 data gradient with K,
+    # weight gradient with Q a multiple of 16) and their neighbours
+    (2, 32, 32, 16, 32, 3, 1, 1, True),    # all three FAST; bias column in the weight gradient
+    (3, 17, 48, 32, 48, 3, 1, 1, False),   # FAST weight gradient across images, ragged M
+    (16, 16, 16, 64, 64, 3, 1, 1, False),  # FAST weight gradient cut into reduction chunks
+    (2, 33, 35, 16, 24, 3, 2, 1, False),   # FAST forward, strided data and weight gradients
+    (2, 12, 12, 20, 16, 3, 1, 1, False),   # C % 16 != 0 forward, FAST data gradient
 ]
 
 
