@@ -707,7 +707,9 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_kernel(KA
     auto gload = [&](int kt, auto S) {
         constexpr int s = decltype(S)::value;
         const int T = tbeg + kt;
-        const bool tin = T < tend;
+        // FAST: the loads of the (at most two) tiles past the end read in-range or
+        // range-checked offsets and are never staged, so no test is needed
+        const bool tin = FAST || T < tend;
         const int k0 = tap_inner ? (tin ? ntap * CCH + nc : 0) : (int)(kbeg + (long)kt * BK);
         // reduction bound of a tile's rows: whole tiles in tap order
         const int kend_i = tap_inner ? (tin ? k0 + BK : 0) : (int)kend;
