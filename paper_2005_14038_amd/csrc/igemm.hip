@@ -815,7 +815,7 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_kernel(KA
 #pragma unroll
             for (int i = 0; i < AV; ++i) {
                 const int kk = k0 + (t + i * NT) / AVPR;
-                bool ok = arow_ok[i] && kk < kend_i;
+                bool ok = arow_ok[i] && (FAST || kk < kend_i);
                 if constexpr (VW == 4) {
                     ldb(rsb, ok, kk * g.K + arow_base[i], areg[s][i]);
                 } else {
@@ -850,7 +850,7 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_kernel(KA
                         while (q >= g.Q) { q -= g.Q; if (++p == g.P) { p = 0; ++n; } }
                     }
                 }
-                const bool kin = k0 + kr < kend_i;
+                const bool kin = FAST || k0 + kr < kend_i;
                 int h = p * g.st - g.pad + bcol_r, w = q * g.st - g.pad + bcol_s;
                 bool ok = bcol_ok && kin && (unsigned)h < (unsigned)g.H &&
                           (unsigned)w < (unsigned)g.W;
