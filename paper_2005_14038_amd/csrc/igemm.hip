@@ -509,7 +509,9 @@ __device__ __forceinline__ void load_vec(const float* p, bool ok, float* v) {
 // order and the unit stride fixed at compile time: no k tile crosses a tap,
 // so the per-thread wrap of the channel index, the linear-order paths and the
 // stride's division and exact-tap test drop out of the k loop (the data
-// gradient's stride alone: VGG-19 +1.1 %, its first stage +1.3 %).  For a
+// gradient's stride alone: VGG-19 +1.1 %, its first stage +1.3 %).  The tap
+// index steps by selects and (r, s) follow from it by a multiply and shift,
+// exact for at most 7 x 7 taps (the host's condition).  For a
 // weight gradient: an output width Q that is a multiple of the k tile, so that
 // no k tile (16 output pixels) crosses an output row and the pixel's image
 // and row are the tile's.
@@ -684,6 +686,7 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_kernel(KA
     // FWD / DGRAD tap (nr, ns), its index ntap and the channel offset nc
     // within it; WGRAD the pixel (nn, np, nq).
     int nr = 0, ns = 0, nc = 0, ntap = 0, nq = 0, np = 0, nn = 0;
+    const int magS = (256 + g.S - 1) / g.S;   // (t * magS) >> 8 = t / S for t < R*S <= 49
     if constexpr (OP == OP_FWD || OP == OP_DGRAD) {
         if (tap_inner) {
             ntap = tbeg % RSN;
@@ -717,7 +720,12 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_kernel(KA
             const int CC = CCH;                               // contiguous axis of a tap
             const int c0 = nc, r0 = nr, s0 = ns;
             // the next tile
-            if (tap_inner) {
+            if constexpr (FAST) {      // tap index and its (r, s) by a multiply-shift
+                ntap = (ntap + 1 == RSN) ? 0 : ntap + 1;
+                nc = (ntap == 0) ? nc + BK : nc;
+                nr = (ntap * magS) >> 8;
+                ns = ntap - nr * g.S;
+            } else if (tap_inner) {
                 ++ntap;
                 if (++ns == g.S) {
                     ns = 0;
@@ -2846,8 +2854,10 @@ GemmPlan plan_gemm(int op, const ConvGeo& g, int bf16, int num_cus, int bias_col
     static_assert(kCfgs[0].bk == 16 && kCfgs[1].bk == 16 && kCfgs[2].bk == 16 &&
                       kCfgs[3].bk == 16 && kCfgs[4].bk == 16,
                   "fp32 k tile");
-    const bool fast32 = (op == OP_FWD && g.C % 16 == 0) ||
-                        (op == OP_DGRAD && g.st == 1 && g.K % 16 == 0) ||
+    // (forward and data gradient: at most 7 x 7 taps, which their tap stepping assumes)
+    const bool taps7 = g.R <= 7 && g.S <= 7;
+    const bool fast32 = (op == OP_FWD && g.C % 16 == 0 && taps7) ||
+                        (op == OP_DGRAD && g.st == 1 && g.K % 16 == 0 && taps7) ||
                         (op == OP_WGRAD && g.Q % 16 == 0);
     // bf16 operands in memory: every contiguous axis a multiple of 8 (16 bytes)
     p.h16 = (bf16 && g.C % 8 == 0 && g.K % 8 == 0) ? 1 : 0;
@@ -3095,8 +3105,9 @@ hipError_t launch_gemm(const GemmPlan& plan, const ConvGeo& g, const float* a, c
     // operand bases 16-byte aligned
     bool v4 = (plan.op == OP_FWD) ? (g.C % 4 == 0) : (g.C % 4 == 0 && g.K % 4 == 0);
     v4 = v4 && fits_buffer(g) && ((((uintptr_t)a) | ((uintptr_t)b)) & 15) == 0;
-    const bool fast32 = (plan.op == OP_FWD && g.C % 16 == 0) ||
-                        (plan.op == OP_DGRAD && g.st == 1 && g.K % 16 == 0) ||
+    const bool taps7 = g.R <= 7 && g.S <= 7;
+    const bool fast32 = (plan.op == OP_FWD && g.C % 16 == 0 && taps7) ||
+                        (plan.op == OP_DGRAD && g.st == 1 && g.K % 16 == 0 && taps7) ||
                         (plan.op == OP_WGRAD && g.Q % 16 == 0);
     // DGRAD on k-major operands takes the transposed weights b16t
     const uint16_t* bk16 = plan.op == OP_DGRAD ? b16t : b16;

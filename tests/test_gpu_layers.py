@@ -40,6 +40,8 @@ CONV = [
     (16, 16, 16, 64, 64, 3, 1, 1, False),  # FAST weight gradient cut into reduction chunks
     (2, 33, 35, 16, 24, 3, 2, 1, False),   # FAST forward, strided data and weight gradients
     (2, 12, 12, 20, 16, 3, 1, 1, False),   # C % 16 != 0 forward, FAST data gradient
+    (2, 14, 14, 16, 32, 7, 1, 3, False),   # FAST 7 x 7 taps (the largest the tap stepping takes)
+    (2, 12, 12, 16, 32, 5, 1, 2, True),    # FAST 5 x 5 taps
 ]
 
 
