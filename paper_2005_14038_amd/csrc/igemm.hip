@@ -992,8 +992,9 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_kernel(KA
 // the next tile's loads in flight while the current one is multiplied and
 // written.  Four waves of 64 x 64 (2 x 2 MFMA 32x32x2 tiles); rows k past the
 // batch are zeros.  The epilogue is a plain store (no bias, activation, mask
-// or accumulation applies to a weight gradient).  The bias gradient (the sum of dy over the batch, in batch
-// order) is written with the first tile of each row block.
+// or accumulation applies to a weight gradient).  The bias gradient (the sum
+// of dy over the batch, in batch order) is written with the first tile of
+// each row block.
 constexpr int FCW_BM = 64, FCW_BN = 256, FCW_KMAX = 32;
 constexpr int FCW_LDA = FCW_BM + PAD_V, FCW_LDB = FCW_BN + PAD_V;
 
