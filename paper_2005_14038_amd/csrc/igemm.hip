@@ -582,12 +582,16 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_kernel(KA
                 arow_base[i] = n * g.H * g.W * g.C;
                 arow_h[i] = p * g.st - g.pad;
                 arow_w[i] = q * g.st - g.pad;
+                // FAST: a row past M gets a row coordinate that no tap brings
+                // into the image, so its range test needs no row mask
+                if (FAST && !arow_ok[i]) arow_h[i] = -g.H - g.R;
             } else {  // DGRAD: m = (n, h, w)
                 int w = (int)(mm % g.W); long tt = mm / g.W;
                 int h = (int)(tt % g.H); int n = (int)(tt / g.H);
                 arow_base[i] = n * g.P * g.Q * g.K;
                 arow_h[i] = h + g.pad;
                 arow_w[i] = w + g.pad;
+                if (FAST && !arow_ok[i]) arow_h[i] = -g.P - g.R;
             }
         }
     } else {
@@ -745,7 +749,7 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_kernel(KA
                 for (int i = 0; i < AV; ++i) {
                     if constexpr (OP == OP_FWD) {
                         int h = arow_h[i] + r, w = arow_w[i] + sx;
-                        bool ok = arow_ok[i] && kin && (unsigned)h < (unsigned)g.H &&
+                        bool ok = (FAST || arow_ok[i]) && kin && (unsigned)h < (unsigned)g.H &&
                                   (unsigned)w < (unsigned)g.W;
                         if constexpr (VW == 4) {
                             ldb(rsa, ok, arow_base[i] + (h * g.W + w) * g.C + c, areg[s][i]);
@@ -760,7 +764,7 @@ __global__ void __launch_bounds__(64 * (BM / WM) * (BN / WN), 2) igemm_kernel(KA
                         int p = tp, q = tq;
                         bool ok;
                         if constexpr (FAST) {
-                            ok = arow_ok[i] && kin && (unsigned)p < (unsigned)g.P &&
+                            ok = kin && (unsigned)p < (unsigned)g.P &&
                                  (unsigned)q < (unsigned)g.Q;
                         } else {
                             bool on_grid = true;
